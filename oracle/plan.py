@@ -1,0 +1,215 @@
+"""Integer re-derivation of the host plan: validation, phase classification,
+split-K partition of decode sequences and the prefill tile list.
+
+TEST INFRASTRUCTURE (same rules as oracle/attention.py): imported only by
+tests/. Written from the plan contract below, not from the library's C++; the
+two are compared bit-exactly through ``flex_attn_plan_export``.
+
+Role in the method. The paper's daemon validates every request before dispatch
+(Sec. 3.2) and keeps separate prefill and decode queues (Sec. 3.4,
+"Phase-Aware Dispatch"); the plan is that step for one mixed batch: it
+classifies each sequence by its number of new tokens and lays out the work of
+each phase. The partition itself is not in the paper (it defines no kernel);
+the contract is:
+
+* classification: n = 1 -> decode, n >= 2 -> prefill, n = 0 -> nothing.
+* decode split-K: P_s = ceil(L_s / P); W = work-groups per decode item
+  (Hkv for grouped-query attention, Hq / 64 for the 576/512 latent layout);
+  pps = max(min_pps, ceil(W * sum_s P_s / (cus_decode * wg_per_cu)));
+  n_s = ceil(P_s / pps); if n_s > max_splits then pps_s = ceil(P_s / max_splits),
+  n_s = ceil(P_s / pps_s), else pps_s = pps; split j covers keys
+  [j * pps_s * P, min(L_s, (j + 1) * pps_s * P)). Items: decode sequences in
+  batch order, splits ascending.
+* prefill tiles of BM rows: rows [t*BM, min(n, (t+1)*BM)), key_end =
+  L - n + row_end; ordered by key_end descending, then sequence, then tile.
+* co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
+  the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
+  prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
+
+Blob layout (int32): 16-word header, 8 words per decode item, 8 per prefill
+item; see ``build_plan``.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
+MAGIC = 0x46504C58
+VERSION = 1
+HEADER = 16
+ITEM = 8
+
+
+def cdiv(a: int, b: int) -> int:
+    return (a + b - 1) // b
+
+
+@dataclass
+class Shape:
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim_qk: int
+    head_dim_v: int
+    page_size: int
+    sm_scale: float
+    v_aliases_k: int
+
+
+@dataclass
+class Opts:
+    cus_total: int = 0           # 0 -> 256
+    cus_decode: int = 0          # 0 -> all; -1 -> cost model
+    bm: int = 0                  # 0 -> 128 (64 for the 576/512 layout)
+    min_split_tokens: int = 0    # 0 -> 256
+    max_splits: int = 0          # 0 -> 32
+    wg_per_cu: int = 0           # 0 -> 4
+    split_granule: int = 0       # 0 -> 64
+    hbm_gbps: float = 0.0        # 0 -> 8000
+    decode_gbps_per_cu: float = 0.0   # 0 -> 60
+    prefill_tflops_per_cu: float = 0.0  # 0 -> 5
+
+
+@dataclass
+class PlanResult:
+    status: int
+    blob: Optional[List[int]] = None
+    info: Optional[dict] = None
+
+
+MLA_ROWS_PER_WG = 64
+
+
+def _supported(sh: Shape) -> bool:
+    pair = (sh.head_dim_qk, sh.head_dim_v)
+    if pair not in ((64, 64), (128, 128), (576, 512)):
+        return False
+    if sh.page_size not in (16, 64):
+        return False
+    if pair == (576, 512):
+        return bool(sh.v_aliases_k) and sh.num_q_heads % MLA_ROWS_PER_WG == 0
+    return (sh.num_q_heads // sh.num_kv_heads) <= 16
+
+
+def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Sequence[int],
+               max_pages_per_seq: int) -> PlanResult:
+    o = opts or Opts()
+    B = len(seq_lens)
+    if len(qsl) != B + 1:
+        return PlanResult(ERR_INVALID_ARG)
+    # --- shape checks
+    if sh.num_q_heads <= 0 or sh.num_kv_heads <= 0 or sh.num_q_heads % sh.num_kv_heads:
+        return PlanResult(ERR_INVALID_ARG)
+    if not (math.isfinite(sh.sm_scale) and sh.sm_scale > 0):
+        return PlanResult(ERR_INVALID_ARG)
+    if sh.v_aliases_k and (sh.num_kv_heads != 1 or sh.head_dim_v > sh.head_dim_qk):
+        return PlanResult(ERR_INVALID_ARG)
+    if not _supported(sh):
+        return PlanResult(ERR_UNSUPPORTED)
+    # --- option checks / defaults
+    cus_total = o.cus_total or 256
+    wg_per_cu = o.wg_per_cu or 4
+    max_splits = o.max_splits or 32
+    min_tokens = o.min_split_tokens or 256
+    granule = o.split_granule or 64
+    mla = sh.head_dim_qk == 576
+    bm = o.bm or (64 if mla else 128)
+    if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:
+        return PlanResult(ERR_INVALID_ARG)
+    if o.cus_decode < -1 or o.cus_decode > cus_total:
+        return PlanResult(ERR_INVALID_ARG)
+    if bm not in (64, 128) or (mla and bm != 64):
+        return PlanResult(ERR_UNSUPPORTED)
+    # --- integer metadata checks
+    if max_pages_per_seq < 0:
+        return PlanResult(ERR_INVALID_ARG)
+    if B > 0 and qsl[0] != 0:
+        return PlanResult(ERR_INVALID_ARG)
+    P = sh.page_size
+    for s in range(B):
+        n = qsl[s + 1] - qsl[s]
+        L = seq_lens[s]
+        if n < 0 or L < 0 or n > L or L > max_pages_per_seq * P:
+            return PlanResult(ERR_INVALID_ARG)
+    if B > 0 and qsl[B] > 2**31 - 1:
+        return PlanResult(ERR_INVALID_ARG)
+
+    W = (sh.num_q_heads // MLA_ROWS_PER_WG) if mla else sh.num_kv_heads
+    rows_per_wg = MLA_ROWS_PER_WG if mla else sh.num_q_heads // sh.num_kv_heads
+    dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1]
+    pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= 2]
+
+    # --- co-run CU split
+    dec_bytes = 0
+    kv_row = sh.num_kv_heads * (sh.head_dim_qk if sh.v_aliases_k else sh.head_dim_qk + sh.head_dim_v) * 2
+    for s in dec:
+        dec_bytes += seq_lens[s] * kv_row
+    pre_flops = 0
+    for s in pre:
+        n, L = qsl[s + 1] - qsl[s], seq_lens[s]
+        pre_flops += sh.num_q_heads * 2 * (sh.head_dim_qk + sh.head_dim_v) * (n * (L - n) + n * (n + 1) // 2)
+    if o.cus_decode == 0 or not dec or not pre:
+        cus_decode = cus_total
+    elif o.cus_decode > 0:
+        cus_decode = o.cus_decode
+    else:
+        hbm = (o.hbm_gbps or 8000.0) * 1e9
+        bw_cu = (o.decode_gbps_per_cu or 60.0) * 1e9
+        fl_cu = (o.prefill_tflops_per_cu or 5.0) * 1e12
+        best, best_t = None, None
+        nd = granule
+        while nd < cus_total:
+            t = max(dec_bytes / min(hbm, nd * bw_cu), pre_flops / ((cus_total - nd) * fl_cu))
+            if best_t is None or t < best_t:
+                best, best_t = nd, t
+            nd += granule
+        cus_decode = best if best is not None else cus_total
+    cus_prefill = cus_total - cus_decode if (dec and pre and cus_decode < cus_total) else cus_total
+
+    # --- decode split-K partition
+    min_pps = cdiv(min_tokens, P)
+    total_pages = sum(cdiv(seq_lens[s], P) for s in dec)
+    pps = max(min_pps, cdiv(W * total_pages, cus_decode * wg_per_cu)) if dec else 0
+    dec_items = []
+    for d, s in enumerate(dec):
+        Ps = cdiv(seq_lens[s], P)
+        nspl = cdiv(Ps, pps)
+        pps_s = pps
+        if nspl > max_splits:
+            pps_s = cdiv(Ps, max_splits)
+            nspl = cdiv(Ps, pps_s)
+        first = len(dec_items)
+        for j in range(nspl):
+            k0 = j * pps_s * P
+            k1 = min(seq_lens[s], (j + 1) * pps_s * P)
+            dec_items.append([s, j, nspl, k0, k1, first, d, 0])
+
+    # --- prefill tiles, longest key range first
+    tiles = []
+    for s in pre:
+        n, L = qsl[s + 1] - qsl[s], seq_lens[s]
+        for t in range(cdiv(n, bm)):
+            r0, r1 = t * bm, min(n, (t + 1) * bm)
+            tiles.append([s, t, r0, r1, L - n + r1, 0, 0, 0])
+    tiles.sort(key=lambda it: (-it[4], it[0], it[1]))
+
+    nd_, np_ = len(dec_items), len(tiles)
+    total = HEADER + ITEM * (nd_ + np_)
+    pre_height = sh.num_q_heads
+    hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
+           HEADER, HEADER + ITEM * nd_, pps, cus_decode, cus_prefill, bm, total]
+    blob = hdr + [x for it in dec_items for x in it] + [x for it in tiles for x in it]
+    if nd_ == 0:
+        ws = 0
+    else:
+        counters = cdiv(len(dec) * W * 4, 256) * 256
+        stats = nd_ * W * rows_per_wg * 2 * 4
+        ws = counters + cdiv(stats, 256) * 256 + nd_ * W * rows_per_wg * sh.head_dim_v * 4
+    info = dict(num_seqs=B, n_decode_seqs=len(dec), n_prefill_seqs=len(pre),
+                n_decode_items=nd_, n_prefill_items=np_, decode_wg_width=W,
+                prefill_grid_y=pre_height, pages_per_split=pps,
+                cus_decode=cus_decode, cus_prefill=cus_prefill, bm=bm,
+                plan_words=total, device_plan_bytes=cdiv(total * 4, 256) * 256,
+                workspace_bytes=ws, decode_bytes=dec_bytes, prefill_flops=pre_flops)
+    return PlanResult(OK, blob, info)
