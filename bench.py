@@ -1,0 +1,214 @@
+#!/usr/bin/env python3
+"""Benchmark one mixed prefill/decode attention step on one MI355X.
+
+A step is one pass of the whole path over one synthetic batch: the plan
+(built once, outside the timed region, like the paper's off-path policy
+plane), the prefill kernel and the decode kernel with its split merge, run
+either co-located on two CU-masked streams (the default, the paper's dynamic
+co-location analog) or serially. Inputs are resident in HBM before timing;
+the KV cache is rotated over several copies so the 256 MB Infinity Cache
+cannot serve repeated steps.
+
+Default workload: the Qwen2.5-7B-shaped mixed step (one 2048-token chunk on
+4096 cached tokens plus 128 decodes with context U[1024, 8192], GQA 28/4,
+head_dim 128, page 16). Prints one JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+METRIC = "decode attn HBM GB/s, prefill attn TFLOP/s, mixed-batch step µs (Qwen2.5-7B)"
+HBM_PEAK_GBPS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6   # 256 CUs x 2.4 GHz x 4096 dense bf16 flop/clk
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(b, seconds_target=15.0):
+    """Time the fp64 oracle on a bounded sample of the batch; scale to one step."""
+    import numpy as np
+    import oracle.attention as OA
+    w = b.workload
+    qsl = b.query_start_loc.tolist()
+    ls = b.seq_lens.tolist()
+    dec = [s for s in range(len(ls)) if qsl[s + 1] - qsl[s] == 1]
+    pre = [s for s in range(len(ls)) if qsl[s + 1] - qsl[s] >= 2]
+    kw = dict(num_kv_heads=w.num_kv_heads, page_size=w.page_size, head_dim_v=w.head_dim_v,
+              v_aliases_k=w.v_aliases_k)
+    t_dec = t_pre = 0.0
+    keys_dec_sample = keys_pre_sample = 0
+    n_dec_sample = n_pre_rows = 0
+    # decode: whole sequences, in batch order, until about half the time budget
+    t0 = time.perf_counter()
+    for s in dec:
+        OA.attention_rows(b.q, b.k_cache, b.v_cache, b.block_table, b.seq_lens, b.query_start_loc,
+                          w.sm_scale, [(s, 0)], **kw)
+        keys_dec_sample += ls[s]
+        n_dec_sample += 1
+        if time.perf_counter() - t0 > seconds_target / 2:
+            break
+    t_dec = time.perf_counter() - t0
+    # prefill: rows spread over each chunk, all heads
+    t0 = time.perf_counter()
+    for s in pre:
+        n, L = qsl[s + 1] - qsl[s], ls[s]
+        rows = list(range(0, n, max(1, n // 32)))
+        picks = [(s, i) for i in rows]
+        OA.attention_rows(b.q, b.k_cache, b.v_cache, b.block_table, b.seq_lens, b.query_start_loc,
+                          w.sm_scale, picks, **kw)
+        keys_pre_sample += sum(L - n + i + 1 for i in rows)
+        n_pre_rows += len(rows)
+        if time.perf_counter() - t0 > seconds_target / 2:
+            break
+    t_pre = time.perf_counter() - t0
+    keys_dec_all = sum(ls[s] for s in dec)
+    keys_pre_all = sum(sum(ls[s] - (qsl[s + 1] - qsl[s]) + i + 1 for i in range(qsl[s + 1] - qsl[s])) for s in pre)
+    est = 0.0
+    if keys_dec_sample:
+        est += t_dec * keys_dec_all / keys_dec_sample
+    if keys_pre_sample:
+        est += t_pre * keys_pre_all / keys_pre_sample
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
+    except Exception:
+        cores = os.cpu_count() or 1
+    return {"value": est * 1e6, "unit": "us", "cores": cores, "kind": "oracle",
+            "sample": f"{n_dec_sample} of {len(dec)} decode sequences ({keys_dec_sample} keys) + "
+                      f"{n_pre_rows} prefill query rows x {w.num_q_heads} heads ({keys_pre_sample} causal keys); "
+                      f"{t_dec + t_pre:.1f} s of fp64 numpy, scaled by causal key count to the whole step",
+            "measured_s": t_dec + t_pre}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mixed")
+    ap.add_argument("--split", default="128:128", help="prefill:decode CUs for co-run")
+    ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over steps")
+    ap.add_argument("--no-serial", action="store_true", help="skip the serial comparison leg")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this path has no multi-GPU component "
+              "(sequences shard across GPUs with no exchange; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_04415_amd import flexattn as F
+    from paper_2606_04415_amd.workloads import WORKLOADS, algorithmic_work, make_batch
+
+    w = WORKLOADS[args.workload]
+    log(f"drawing workload '{w.name}': {w.description}")
+    b = make_batch(w, seed=0, poison=False)
+    ns, ls = b.extra["ns"], b.extra["ls"]
+    work = algorithmic_work(w, ns, ls)
+    dev = torch.device("cuda:0")
+    q = b.q.to(dev)
+    kv = []
+    for i in range(max(1, args.pools)):
+        k = b.k_cache.to(dev)
+        v = b.v_cache.to(dev) if b.v_cache is not None else None
+        kv.append((k, v))
+    bt = b.block_table.to(dev)
+    sl = b.seq_lens.to(dev)
+    qsl = b.query_start_loc.to(dev)
+
+    cp, cd = (int(x) for x in args.split.split(":"))
+    shape = F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v, w.page_size,
+                         w.sm_scale, w.v_aliases_k)
+    t0 = time.perf_counter()
+    pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd), b.query_start_loc.tolist(), b.seq_lens.tolist(),
+                          b.block_table.shape[1])
+    plan_us = (time.perf_counter() - t0) * 1e6
+    info = pa.plan.info
+    out, lse = pa.alloc_out(q)
+    arglist = [pa.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+    corun = F.Corun(cp, cd)
+    log(f"plan: {info['n_decode_items']} decode items x {info['decode_wg_width']}, "
+        f"{info['n_prefill_items']} prefill tiles x {info['prefill_grid_y']}; co-run {cp}/{cd} CUs")
+
+    def timed(mode, steps, warmup):
+        corun.set_timing(True)
+        for i in range(warmup):
+            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, corun=corun)
+        torch.cuda.synchronize()
+        corun.set_timing(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        e0.record()
+        for i in range(steps):
+            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, corun=corun)
+        e1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_wall
+        ms = e0.elapsed_time(e1) / steps
+        pre, dec = corun.timing_read()
+        return ms, wall, sum(pre) / len(pre), sum(dec) / len(dec)
+
+    log(f"co-run: {args.warmup} warmup + {args.steps} timed steps")
+    c_ms, c_wall, c_pre, c_dec = timed(F.FLEX_MODE_CORUN, args.steps, args.warmup)
+    log(f"co-run step {c_ms * 1e3:.1f} us (prefill {c_pre * 1e3:.1f} us, decode {c_dec * 1e3:.1f} us)")
+    s_ms = s_pre = s_dec = None
+    if not args.no_serial:
+        s_ms, _, s_pre, s_dec = timed(F.FLEX_MODE_SERIAL, args.steps, args.warmup)
+        log(f"serial step {s_ms * 1e3:.1f} us (prefill {s_pre * 1e3:.1f} us, decode {s_dec * 1e3:.1f} us)")
+    corun.close()
+
+    dec_bytes = work["decode"]["bytes"]
+    pre_flops = work["prefill"]["flops"]
+    # dominant kernel: the one with the larger share of the co-run step
+    if dec_bytes and (not pre_flops or c_dec >= c_pre):
+        achieved = dec_bytes / (c_dec * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                "kernel": "decode_gqa_kernel" if w.head_dim_qk != 576 else "rowpar_kernel (latent decode)",
+                "algorithmic_bytes_per_launch": dec_bytes, "avg_launch_us": round(c_dec * 1e3, 2),
+                "cus": cd}
+    else:
+        achieved = pre_flops / (c_pre * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "kernel": "rowpar_kernel (prefill)", "algorithmic_flops_per_launch": pre_flops,
+                "avg_launch_us": round(c_pre * 1e3, 2), "cus": cp}
+
+    result = {
+        "metric": METRIC, "value": round(c_ms * 1e3, 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(c_ms, 5), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.description}", "batch": len(ls), "query_tokens": sum(ns),
+                   "kv_tokens": sum(ls), "mode": "corun", "cus_prefill": cp, "cus_decode": cd,
+                   "kv_pools": len(kv), "plan_host_us": round(plan_us, 1)},
+        "phases_us": {"corun_prefill": round(c_pre * 1e3, 2), "corun_decode": round(c_dec * 1e3, 2)},
+        "roofline": roof,
+    }
+    if s_ms is not None:
+        result["serial_us"] = round(s_ms * 1e3, 2)
+        result["corun_speedup_vs_serial"] = round(s_ms / c_ms, 4)
+        result["phases_us"].update({"serial_prefill": round(s_pre * 1e3, 2), "serial_decode": round(s_dec * 1e3, 2)})
+        if dec_bytes:
+            result["decode_GBps_all_cus"] = round(dec_bytes / (s_dec * 1e-3) / 1e9, 1)
+        if pre_flops:
+            result["prefill_TFLOPs_all_cus"] = round(pre_flops / (s_pre * 1e-3) / 1e12, 2)
+    result["bound_us"] = round(max((dec_bytes + work["prefill"]["bytes"]) / (HBM_PEAK_GBPS * 1e3),
+                                   (pre_flops + work["decode"]["flops"]) / (BF16_PEAK_TFLOPS * 1e6)), 1)
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,242 @@
+/*
+ * flexattn: mixed prefill/decode paged attention on one MI355X (gfx950).
+ *
+ * What the library computes. FlexNPU co-locates the prefill and decode phases
+ * of LLM serving on one device and schedules them by phase: prefill is
+ * compute-intensive, decode is bound by memory bandwidth and KV-cache reads,
+ * and both read one shared KV pool (Abstract; Sec. 1; Sec. 3; Sec. 3.3;
+ * Sec. 3.4 "Phase-Aware Dispatch", "Memory Locality"). The data-parallel work
+ * inside such a co-located step is attention over one mixed batch:
+ *
+ *   for sequence s with n_s new query tokens and L_s keys (0 <= n_s <= L_s),
+ *   query i sits at absolute position L_s - n_s + i and attends keys
+ *   0 .. L_s - n_s + i (bottom-right causal alignment; decode is n_s = 1);
+ *   key t of s is row (block_table[s][t / P], t % P) of the paged caches;
+ *   query head h reads KV head h / (Hq / Hkv);
+ *   out = softmax(sm_scale * q K^T) V,  lse = log-sum-exp of the scaled scores
+ *   (natural log).
+ *
+ * The paper writes none of this down (it defines no kernel); the definition
+ * is textbook scaled dot-product attention, and every reading of a detail the
+ * paper leaves open (layout, causal alignment, head mapping, rounding) is
+ * listed with its reason in the repository's design notes.
+ *
+ * Conventions for every call:
+ *  - Every call returns an int status (FLEX_OK or a negative FLEX_ERR_*);
+ *    nothing throws across this boundary. flex_attn_last_error() returns a
+ *    thread-local text describing the last failure on the calling thread.
+ *  - Device memory is owned by the caller; the library never allocates device
+ *    memory. Host plan objects and co-run stream pairs are owned by the
+ *    library until their destroy call.
+ *  - Run calls (decode, prefill, mixed, debug gather, workspace init) only
+ *    enqueue work on the given HIP stream (a hipStream_t passed as void*;
+ *    NULL is the null stream) and return; they never synchronise.
+ *  - Tensors are bf16 with the innermost dimension contiguous; every base
+ *    pointer and every row stride must be a multiple of 16 bytes.
+ */
+#ifndef FLEXATTN_H
+#define FLEXATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define FLEX_OK 0
+#define FLEX_ERR_INVALID_ARG (-1)  /* malformed metadata, null/misaligned pointer, inconsistent args */
+#define FLEX_ERR_UNSUPPORTED (-2)  /* well-formed but outside the supported shapes */
+#define FLEX_ERR_WORKSPACE (-3)    /* device plan or workspace buffer too small */
+#define FLEX_ERR_HIP (-4)          /* a HIP runtime call failed; text in flex_attn_last_error() */
+#define FLEX_ERR_INTERNAL (-5)
+
+/* Modes of flex_attn_mixed. */
+#define FLEX_MODE_SERIAL 0  /* prefill then decode on the caller stream, all CUs */
+#define FLEX_MODE_CORUN 1   /* prefill and decode on two CU-masked streams, joined */
+
+/* Attention geometry of one layer.
+ * Supported: (head_dim_qk, head_dim_v) in {(64,64), (128,128)} with
+ * num_q_heads / num_kv_heads <= 16, or (576, 512) with v_aliases_k = 1,
+ * num_kv_heads = 1 and num_q_heads a multiple of 64 (absorbed latent attention:
+ * the value row of a key is the first 512 columns of its 576-wide key row);
+ * page_size in {16, 64}. sm_scale must be finite and > 0. */
+typedef struct flex_attn_shape {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim_qk;
+  int32_t head_dim_v;
+  int32_t page_size;
+  float sm_scale;
+  int32_t v_aliases_k;
+} flex_attn_shape;
+
+/* Planner tunables; a zero field takes the default in brackets.
+ * cus_decode: CUs the decode phase is partitioned for and, in co-run mode,
+ * runs on [0 = all]; -1 asks the cost model to choose the split among
+ * multiples of split_granule from the rates below. */
+typedef struct flex_attn_plan_opts {
+  int32_t cus_total;          /* [256] */
+  int32_t cus_decode;         /* [0 = all CUs] */
+  int32_t bm;                 /* prefill rows per tile [128; 64 for 576/512] */
+  int32_t min_split_tokens;   /* smallest decode split, in keys [256] */
+  int32_t max_splits;         /* most splits per decode sequence [32] */
+  int32_t wg_per_cu;          /* decode work-groups aimed at per CU [4] */
+  int32_t split_granule;      /* co-run split granularity in CUs [64] */
+  double hbm_gbps;            /* cost model: device HBM bandwidth [8000] */
+  double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws [60] */
+  double prefill_tflops_per_cu; /* cost model: prefill rate of one CU [5] */
+} flex_attn_plan_opts;
+
+/* Summary of a plan. */
+typedef struct flex_attn_plan_info {
+  int32_t num_seqs;
+  int32_t n_decode_seqs;     /* sequences with one new token */
+  int32_t n_prefill_seqs;    /* sequences with two or more new tokens */
+  int32_t n_decode_items;    /* (sequence, split) work items */
+  int32_t n_prefill_items;   /* (sequence, row tile) work items */
+  int32_t decode_wg_width;   /* work-groups per decode item (grid y) */
+  int32_t prefill_grid_y;    /* work-groups per prefill tile (grid y) */
+  int32_t pages_per_split;
+  int32_t cus_decode;
+  int32_t cus_prefill;
+  int32_t bm;
+  int32_t plan_words;        /* int32 words in the exported / uploaded plan */
+  size_t device_plan_bytes;  /* bytes the device copy of the plan needs */
+  size_t workspace_bytes;    /* bytes of workspace decode needs (0 if none) */
+  double decode_bytes;       /* algorithmic KV bytes of the decode phase */
+  double prefill_flops;      /* algorithmic flops of the prefill phase */
+} flex_attn_plan_info;
+
+/* Device tensors of one run. Strides are in elements.
+ *  q        bf16 [T, Hq, d_qk], contiguous (T = query_start_loc[B]).
+ *  k_cache  bf16 pages: element (page, slot, kv_head, d) at
+ *           page*k_stride[0] + slot*k_stride[1] + kv_head*k_stride[2] + d.
+ *  v_cache  same with v_stride and d < d_v; ignored (may be NULL) when the
+ *           shape has v_aliases_k.
+ *  block_table int32 [B, >= max_pages_per_seq], row stride block_table_stride;
+ *           entries 0 .. ceil(L_s / P) - 1 of row s must lie in [0, num_pages).
+ *  seq_lens int32 [B], query_start_loc int32 [B+1]: the same values the plan
+ *           was built from (a mismatch is undefined behaviour).
+ *  out      bf16 [T, Hq, d_v], contiguous; rows of sequences with n_s = 0 are
+ *           untouched.
+ *  lse      fp32 [T, Hq] or NULL.
+ *  d_plan   the plan uploaded with flex_attn_plan_upload.
+ *  workspace  device scratch of >= flex_attn_plan_info.workspace_bytes; it
+ *           must be zero-filled before its first use, and every completed
+ *           decode leaves its counters at zero again. Two runs in flight at
+ *           once must not share a workspace. */
+typedef struct flex_attn_args {
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  int64_t k_stride[3];
+  int64_t v_stride[3];
+  int32_t num_pages;
+  const int32_t* block_table;
+  int32_t block_table_stride;
+  const int32_t* seq_lens;
+  const int32_t* query_start_loc;
+  void* out;
+  float* lse;
+  const void* d_plan;
+  size_t d_plan_bytes;
+  void* workspace;
+  size_t workspace_bytes;
+} flex_attn_args;
+
+typedef struct flex_attn_plan flex_attn_plan_t;
+typedef struct flex_attn_corun flex_attn_corun_t;
+
+/* Text of a status code (static storage). */
+const char* flex_attn_status_string(int status);
+/* Detail of the last failure on this thread (thread-local, valid until the next call). */
+const char* flex_attn_last_error(void);
+
+/* Build a host plan: validate the integer metadata, classify each sequence by
+ * its new-token count (1 -> decode, >= 2 -> prefill, 0 -> nothing), split each
+ * decode sequence's keys into page-aligned ranges, tile each prefill chunk into
+ * rows, longest key range first, and fix the co-run CU split. This mirrors the
+ * daemon's validate-then-enqueue step and its per-phase queues (Sec. 3.2;
+ * Sec. 3.4 "Phase-Aware Dispatch"). Host only: makes no HIP call.
+ * h_query_start_loc [num_seqs+1] and h_seq_lens [num_seqs] are host arrays.
+ * opts may be NULL (defaults). On success *out_plan owns a new plan.
+ * Errors: FLEX_ERR_INVALID_ARG (query_start_loc[0] != 0 or decreasing, n_s > L_s,
+ * L_s > max_pages_per_seq * page_size, Hq % Hkv != 0, bad scale, bad opts,
+ * null pointers), FLEX_ERR_UNSUPPORTED (shape outside the supported set). */
+int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan_opts* opts,
+                   int32_t num_seqs, const int32_t* h_query_start_loc,
+                   const int32_t* h_seq_lens, int32_t max_pages_per_seq,
+                   flex_attn_plan_t** out_plan);
+
+/* Copy the plan summary into *out. */
+int flex_attn_plan_info_get(const flex_attn_plan_t* plan, flex_attn_plan_info* out);
+
+/* Copy the plan's int32 words (header, decode items, prefill items) to host
+ * memory h_dst of n_words >= plan_words; FLEX_ERR_WORKSPACE if too small. */
+int flex_attn_plan_export(const flex_attn_plan_t* plan, int32_t* h_dst, size_t n_words);
+
+/* Enqueue an H2D copy of the plan words into device buffer d_dst of
+ * dst_bytes >= device_plan_bytes on stream. The plan must outlive the copy. */
+int flex_attn_plan_upload(const flex_attn_plan_t* plan, void* d_dst, size_t dst_bytes, void* stream);
+
+void flex_attn_plan_destroy(flex_attn_plan_t* plan);
+
+/* Decode phase (sequences with one new token): split-K attention over each
+ * sequence's pages, streamed from HBM, and the merge of the splits
+ * (out = sum_j e^{m_j - M} O_j / sum_j e^{m_j - M} l_j, M = max_j m_j), done
+ * by the last work-group to finish each (sequence, KV head). */
+int flex_attn_decode(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream);
+
+/* Prefill phase (sequences with two or more new tokens): causal flash
+ * attention over key tiles gathered through block_table into LDS, with QK^T
+ * and PV on bf16 matrix cores and fp32 accumulation. */
+int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream);
+
+/* One mixed step: both phases of the plan. FLEX_MODE_SERIAL runs prefill then
+ * decode on stream; FLEX_MODE_CORUN forks stream into the two CU-masked
+ * streams of corun (prefill on its prefill stream, decode on its decode
+ * stream) and joins them back into stream, the one-device analog of the
+ * paper's dynamic co-location (Sec. 3.4). Outputs are bit-identical between
+ * the modes for the same plan. For SERIAL, corun may be NULL; if given, it is
+ * used only for phase timing (flex_attn_corun_set_timing). */
+int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode,
+                    void* stream, flex_attn_corun_t* corun);
+
+/* Create two streams on the current device, restricted by CU masks to
+ * cus_prefill and cus_decode compute units (disjoint, balanced over the
+ * chip's XCDs), plus the events that fork and join them. Each count must be
+ * a positive multiple of 64 and their sum at most the device's CU count. */
+int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, flex_attn_corun_t** out);
+void flex_attn_corun_destroy(flex_attn_corun_t* corun);
+/* The two streams (hipStream_t) of a co-run pair. */
+int flex_attn_corun_streams(const flex_attn_corun_t* corun, void** prefill_stream, void** decode_stream);
+
+/* Per-phase timing, the runtime profile the paper's scheduler consumes
+ * (operator execution time per phase, Sec. 3.3). With timing enabled, every
+ * flex_attn_mixed call given this corun object (in either mode) records HIP
+ * events around each phase's kernel on the stream that kernel runs on, into
+ * a ring of FLEX_TIMING_RING steps. Enabling clears the ring. */
+#define FLEX_TIMING_RING 1024
+int flex_attn_corun_set_timing(flex_attn_corun_t* corun, int enable);
+/* Wait for the recorded steps and copy their phase durations in milliseconds
+ * (oldest first; a phase with no work reads 0) into prefill_ms / decode_ms of
+ * capacity max_steps each; *n_steps receives the count copied. */
+int flex_attn_corun_timing_read(flex_attn_corun_t* corun, float* prefill_ms, float* decode_ms,
+                                int32_t max_steps, int32_t* n_steps);
+
+/* Test aid: copy the L_s key rows (and value rows unless v_aliases_k) of
+ * sequence seq, gathered through block_table by the same page-address
+ * arithmetic the attention kernels use, into contiguous k_out [L_s, Hkv, d_qk]
+ * and v_out [L_s, Hkv, d_v] (bf16). seq_len is L_s on the host. */
+int flex_attn_debug_gather(const flex_attn_plan_t* plan, const flex_attn_args* args, int32_t seq,
+                           int32_t seq_len, void* k_out, void* v_out, void* stream);
+
+/* Zero the first bytes of a workspace on stream with a fill kernel. */
+int flex_attn_workspace_init(void* workspace, size_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLEXATTN_H */

@@ -1,0 +1,357 @@
+// Run calls of the C ABI: argument checks, kernel parameter blocks, serial and
+// co-run launch, plan upload, debug gather and workspace fill.
+//
+// Co-run is the one-device analog of the paper's dynamic prefill/decode
+// co-location (Sec. 3.4): the two phases of one step share the device and its
+// KV pool, each restricted to its own set of compute units through a CU-masked
+// stream, instead of running back to back on all units.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "host_common.h"
+#include "kernels.h"
+
+using namespace flexattn;
+
+struct flex_attn_corun {
+  hipStream_t prefill = nullptr;
+  hipStream_t decode = nullptr;
+  hipEvent_t fork = nullptr;
+  hipEvent_t join_p = nullptr;
+  hipEvent_t join_d = nullptr;
+  int device = 0;
+  int cus_prefill = 0;
+  int cus_decode = 0;
+  // phase timing ring: events around each phase's kernel, per recorded step
+  bool timing = false;
+  int64_t t_count = 0;
+  std::vector<hipEvent_t> ev;        // 4 per slot: prefill start/end, decode start/end
+  std::vector<unsigned char> has;    // 2 per slot: prefill ran, decode ran
+};
+
+namespace {
+
+int hip_fail(hipError_t e, const char* what) {
+  return set_error(FLEX_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks shared by every run call; fills the kernel parameter block.
+int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p) {
+  if (!plan || !a) return set_error(FLEX_ERR_INVALID_ARG, "plan or args is NULL");
+  const flex_attn_shape& sh = plan->shape;
+  const flex_attn_plan_info& info = plan->info;
+  const bool has_work = info.n_decode_items + info.n_prefill_items > 0;
+  std::memset(p, 0, sizeof(*p));
+  if (!has_work) return FLEX_OK;
+  if (!a->q || !a->k_cache || !a->block_table || !a->seq_lens || !a->query_start_loc || !a->out || !a->d_plan)
+    return set_error(FLEX_ERR_INVALID_ARG, "a required device pointer is NULL");
+  const void* v = sh.v_aliases_k ? a->k_cache : a->v_cache;
+  if (!v) return set_error(FLEX_ERR_INVALID_ARG, "v_cache is NULL");
+  if (!aligned16(a->q) || !aligned16(a->k_cache) || !aligned16(v) || !aligned16(a->out) || !aligned16(a->d_plan))
+    return set_error(FLEX_ERR_INVALID_ARG, "q, caches, out and d_plan must be 16-byte aligned");
+  const int64_t* vs = sh.v_aliases_k ? a->k_stride : a->v_stride;
+  for (int i = 0; i < 3; ++i) {
+    if (a->k_stride[i] <= 0 || vs[i] <= 0 || (a->k_stride[i] * 2) % 16 || (vs[i] * 2) % 16)
+      return set_error(FLEX_ERR_INVALID_ARG, "cache strides must be positive multiples of 16 bytes");
+  }
+  if (a->k_stride[2] < sh.head_dim_qk || vs[2] < (sh.v_aliases_k ? sh.head_dim_qk : sh.head_dim_v))
+    return set_error(FLEX_ERR_INVALID_ARG, "cache head stride smaller than the head dimension");
+  if (a->num_pages <= 0) return set_error(FLEX_ERR_INVALID_ARG, "num_pages must be positive");
+  if (a->block_table_stride < 1) return set_error(FLEX_ERR_INVALID_ARG, "block_table_stride < 1");
+  if (a->d_plan_bytes < info.device_plan_bytes)
+    return set_error(FLEX_ERR_WORKSPACE, "d_plan_bytes smaller than the plan's device_plan_bytes");
+  if (info.n_decode_items > 0) {
+    if (!a->workspace) return set_error(FLEX_ERR_INVALID_ARG, "workspace is NULL");
+    if (!aligned16(a->workspace)) return set_error(FLEX_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (a->workspace_bytes < info.workspace_bytes)
+      return set_error(FLEX_ERR_WORKSPACE, "workspace_bytes smaller than the plan's workspace_bytes");
+  }
+  p->q = static_cast<const uint16_t*>(a->q);
+  p->kc = CacheRef{static_cast<const uint16_t*>(a->k_cache), a->k_stride[0], a->k_stride[1], a->k_stride[2]};
+  p->vc = CacheRef{static_cast<const uint16_t*>(v), vs[0], vs[1], vs[2]};
+  p->bt = a->block_table;
+  p->bt_stride = a->block_table_stride;
+  p->seq_lens = a->seq_lens;
+  p->qsl = a->query_start_loc;
+  p->out = static_cast<uint16_t*>(a->out);
+  p->lse = a->lse;
+  p->Hq = sh.num_q_heads;
+  p->Hkv = sh.num_kv_heads;
+  p->G = sh.num_q_heads / sh.num_kv_heads;
+  p->P = sh.page_size;
+  p->rows_per_wg = plan->rows_per_wg;
+  p->scale_log2 = sh.sm_scale * 1.4426950408889634f;
+  if (info.n_decode_items > 0) {
+    const int32_t W = info.decode_wg_width;
+    const size_t counters = ((size_t(info.n_decode_seqs) * W * 4 + 255) / 256) * 256;
+    const size_t stats = size_t(info.n_decode_items) * W * plan->rows_per_wg * 2 * 4;
+    char* ws = static_cast<char*>(a->workspace);
+    p->counters = reinterpret_cast<uint32_t*>(ws);
+    p->ws_stats = reinterpret_cast<float*>(ws + counters);
+    p->ws_o = reinterpret_cast<float*>(ws + counters + ((stats + 255) / 256) * 256);
+  }
+  return FLEX_OK;
+}
+
+int run_decode(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args* a, hipStream_t s) {
+  const flex_attn_plan_info& info = plan->info;
+  if (info.n_decode_items == 0) return FLEX_OK;
+  p.items = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_DEC];
+  p.n_items = info.n_decode_items;
+  p.grid_y = info.decode_wg_width;
+  const hipError_t e = launch_decode(p, plan->shape.head_dim_qk, s);
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "decode launch");
+}
+
+int run_prefill(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args* a, hipStream_t s) {
+  const flex_attn_plan_info& info = plan->info;
+  if (info.n_prefill_items == 0) return FLEX_OK;
+  p.items = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_PRE];
+  p.n_items = info.n_prefill_items;
+  p.grid_y = info.prefill_grid_y;
+  const hipError_t e = launch_prefill(p, plan->shape.head_dim_qk, info.bm, s);
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "prefill launch");
+}
+
+// CU mask with `count` units out of `total`: bit i is set when
+// ((i >> 3) & 3) falls in [lo, lo + count/64), so each group of 32 bits and
+// each residue class of i mod 8 get the same number of units. Whether the
+// device maps mask bits to XCDs by i mod 8 or by i / 32, the units then spread
+// evenly over all eight XCDs and every XCD keeps some units for the stream.
+void build_mask(int lo_quarter, int quarters, int total, uint32_t* mask, int words) {
+  for (int i = 0; i < words; ++i) mask[i] = 0;
+  for (int i = 0; i < total; ++i) {
+    const int q = (i >> 3) & 3;
+    if (q >= lo_quarter && q < lo_quarter + quarters) mask[i >> 5] |= 1u << (i & 31);
+  }
+}
+
+// Launch one phase, bracketed by timing events when the co-run object asks for them.
+template <typename Fn>
+int timed_phase(flex_attn_corun* c, int phase, bool has_work, hipStream_t s, Fn&& launch) {
+  if (!c || !c->timing || !has_work) return launch(s);
+  const int64_t slot = c->t_count % FLEX_TIMING_RING;
+  hipError_t e = hipEventRecord(c->ev[slot * 4 + 2 * phase], s);
+  if (e != hipSuccess) return hip_fail(e, "timing record");
+  const int st = launch(s);
+  if (st != FLEX_OK) return st;
+  if ((e = hipEventRecord(c->ev[slot * 4 + 2 * phase + 1], s)) != hipSuccess) return hip_fail(e, "timing record");
+  c->has[slot * 2 + phase] = 1;
+  return FLEX_OK;
+}
+
+void timing_begin_step(flex_attn_corun* c) {
+  if (!c || !c->timing) return;
+  const int64_t slot = c->t_count % FLEX_TIMING_RING;
+  c->has[slot * 2] = c->has[slot * 2 + 1] = 0;
+}
+
+void timing_end_step(flex_attn_corun* c) {
+  if (c && c->timing) ++c->t_count;
+}
+
+}  // namespace
+
+extern "C" int flex_attn_plan_upload(const flex_attn_plan_t* plan, void* d_dst, size_t dst_bytes, void* stream) {
+  clear_error();
+  if (!plan || !d_dst) return set_error(FLEX_ERR_INVALID_ARG, "plan or destination is NULL");
+  const size_t bytes = plan->words.size() * sizeof(int32_t);
+  if (dst_bytes < bytes) return set_error(FLEX_ERR_WORKSPACE, "destination smaller than the plan");
+  const hipError_t e = hipMemcpyAsync(d_dst, plan->words.data(), bytes, hipMemcpyHostToDevice,
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "plan upload");
+}
+
+extern "C" int flex_attn_decode(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream) {
+  clear_error();
+  AttnParams p;
+  const int st = prepare(plan, args, &p);
+  if (st != FLEX_OK) return st;
+  return run_decode(plan, p, args, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream) {
+  clear_error();
+  AttnParams p;
+  const int st = prepare(plan, args, &p);
+  if (st != FLEX_OK) return st;
+  return run_prefill(plan, p, args, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode, void* stream,
+                               flex_attn_corun_t* corun) {
+  clear_error();
+  if (mode != FLEX_MODE_SERIAL && mode != FLEX_MODE_CORUN) return set_error(FLEX_ERR_INVALID_ARG, "unknown mode");
+  AttnParams p;
+  int st = prepare(plan, args, &p);
+  if (st != FLEX_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool has_pre = plan->info.n_prefill_items > 0, has_dec = plan->info.n_decode_items > 0;
+  auto pre = [&](hipStream_t ps) { return run_prefill(plan, p, args, ps); };
+  auto dec = [&](hipStream_t ds) { return run_decode(plan, p, args, ds); };
+  if (mode == FLEX_MODE_SERIAL) {
+    timing_begin_step(corun);
+    st = timed_phase(corun, 0, has_pre, s, pre);
+    if (st != FLEX_OK) return st;
+    st = timed_phase(corun, 1, has_dec, s, dec);
+    if (st != FLEX_OK) return st;
+    timing_end_step(corun);
+    return FLEX_OK;
+  }
+  if (!corun) return set_error(FLEX_ERR_INVALID_ARG, "co-run mode needs a co-run stream pair");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != corun->device) return set_error(FLEX_ERR_INVALID_ARG, "co-run pair belongs to another device");
+  if ((e = hipEventRecord(corun->fork, s)) != hipSuccess) return hip_fail(e, "fork record");
+  if ((e = hipStreamWaitEvent(corun->prefill, corun->fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
+  if ((e = hipStreamWaitEvent(corun->decode, corun->fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
+  timing_begin_step(corun);
+  st = timed_phase(corun, 0, has_pre, corun->prefill, pre);
+  if (st != FLEX_OK) return st;
+  st = timed_phase(corun, 1, has_dec, corun->decode, dec);
+  if (st != FLEX_OK) return st;
+  timing_end_step(corun);
+  if ((e = hipEventRecord(corun->join_p, corun->prefill)) != hipSuccess) return hip_fail(e, "join record");
+  if ((e = hipEventRecord(corun->join_d, corun->decode)) != hipSuccess) return hip_fail(e, "join record");
+  if ((e = hipStreamWaitEvent(s, corun->join_p, 0)) != hipSuccess) return hip_fail(e, "join wait");
+  if ((e = hipStreamWaitEvent(s, corun->join_d, 0)) != hipSuccess) return hip_fail(e, "join wait");
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, flex_attn_corun_t** out) {
+  clear_error();
+  if (!out) return set_error(FLEX_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  hipDeviceProp_t prop;
+  if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+  const int total = prop.multiProcessorCount;
+  if (cus_prefill <= 0 || cus_decode <= 0 || cus_prefill % 64 || cus_decode % 64 || cus_prefill + cus_decode > total ||
+      total % 256)
+    return set_error(FLEX_ERR_UNSUPPORTED, "co-run CU counts must be positive multiples of 64 summing to at most " +
+                                               std::to_string(total) + " on a device whose CU count is a multiple of 256");
+  const int words = (total + 31) / 32;
+  uint32_t mask_p[64], mask_d[64];
+  if (words > 64) return set_error(FLEX_ERR_UNSUPPORTED, "too many CUs");
+  // With 256 CUs a quarter is 64 units; decode takes the low quarters.
+  const int per_quarter = total / 4;
+  build_mask(0, cus_decode / per_quarter, total, mask_d, words);
+  build_mask(cus_decode / per_quarter, cus_prefill / per_quarter, total, mask_p, words);
+  flex_attn_corun* c = new (std::nothrow) flex_attn_corun();
+  if (!c) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
+  c->device = dev;
+  c->cus_prefill = cus_prefill;
+  c->cus_decode = cus_decode;
+  if ((e = hipExtStreamCreateWithCUMask(&c->prefill, words, mask_p)) != hipSuccess ||
+      (e = hipExtStreamCreateWithCUMask(&c->decode, words, mask_d)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&c->join_p, hipEventDisableTiming)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&c->join_d, hipEventDisableTiming)) != hipSuccess) {
+    const int st = hip_fail(e, "co-run stream/event creation");
+    flex_attn_corun_destroy(c);
+    return st;
+  }
+  *out = c;
+  return FLEX_OK;
+}
+
+extern "C" void flex_attn_corun_destroy(flex_attn_corun_t* c) {
+  if (!c) return;
+  for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
+  if (c->prefill) (void)hipStreamDestroy(c->prefill);
+  if (c->decode) (void)hipStreamDestroy(c->decode);
+  if (c->fork) (void)hipEventDestroy(c->fork);
+  if (c->join_p) (void)hipEventDestroy(c->join_p);
+  if (c->join_d) (void)hipEventDestroy(c->join_d);
+  delete c;
+}
+
+extern "C" int flex_attn_corun_streams(const flex_attn_corun_t* c, void** p, void** d) {
+  clear_error();
+  if (!c || !p || !d) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  *p = c->prefill;
+  *d = c->decode;
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_corun_set_timing(flex_attn_corun_t* c, int enable) {
+  clear_error();
+  if (!c) return set_error(FLEX_ERR_INVALID_ARG, "corun is NULL");
+  if (enable && c->ev.empty()) {
+    c->ev.assign(size_t(FLEX_TIMING_RING) * 4, nullptr);
+    for (auto& e : c->ev) {
+      const hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return hip_fail(r, "timing event creation");
+    }
+    c->has.assign(size_t(FLEX_TIMING_RING) * 2, 0);
+  }
+  c->timing = enable != 0;
+  c->t_count = 0;
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_corun_timing_read(flex_attn_corun_t* c, float* prefill_ms, float* decode_ms,
+                                           int32_t max_steps, int32_t* n_steps) {
+  clear_error();
+  if (!c || !prefill_ms || !decode_ms || !n_steps || max_steps < 0)
+    return set_error(FLEX_ERR_INVALID_ARG, "NULL argument or negative capacity");
+  *n_steps = 0;
+  if (c->ev.empty()) return FLEX_OK;
+  const int64_t kept = std::min<int64_t>(c->t_count, FLEX_TIMING_RING);
+  const int64_t n = std::min<int64_t>(kept, max_steps);
+  for (int64_t k = 0; k < n; ++k) {
+    const int64_t slot = (c->t_count - kept + k) % FLEX_TIMING_RING;
+    float* dst[2] = {prefill_ms + k, decode_ms + k};
+    for (int ph = 0; ph < 2; ++ph) {
+      *dst[ph] = 0.f;
+      if (!c->has[slot * 2 + ph]) continue;
+      hipError_t e = hipEventSynchronize(c->ev[slot * 4 + 2 * ph + 1]);
+      if (e != hipSuccess) return hip_fail(e, "timing wait");
+      if ((e = hipEventElapsedTime(dst[ph], c->ev[slot * 4 + 2 * ph], c->ev[slot * 4 + 2 * ph + 1])) != hipSuccess)
+        return hip_fail(e, "timing read");
+    }
+  }
+  *n_steps = int32_t(n);
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_debug_gather(const flex_attn_plan_t* plan, const flex_attn_args* a, int32_t seq,
+                                      int32_t seq_len, void* k_out, void* v_out, void* stream) {
+  clear_error();
+  if (!plan || !a || !a->k_cache || !a->block_table || !k_out)
+    return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  const flex_attn_shape& sh = plan->shape;
+  if (seq < 0 || seq >= plan->info.num_seqs) return set_error(FLEX_ERR_INVALID_ARG, "seq out of range");
+  if (seq_len < 0) return set_error(FLEX_ERR_INVALID_ARG, "seq_len < 0");
+  const bool has_v = !sh.v_aliases_k;
+  if (has_v && (!a->v_cache || !v_out)) return set_error(FLEX_ERR_INVALID_ARG, "v_cache or v_out is NULL");
+  const CacheRef kc{static_cast<const uint16_t*>(a->k_cache), a->k_stride[0], a->k_stride[1], a->k_stride[2]};
+  const CacheRef vc{static_cast<const uint16_t*>(has_v ? a->v_cache : a->k_cache), a->v_stride[0], a->v_stride[1],
+                    a->v_stride[2]};
+  const hipError_t e = launch_gather(kc, vc, has_v, a->block_table + int64_t(seq) * a->block_table_stride, seq_len,
+                                     sh.page_size, sh.num_kv_heads, sh.head_dim_qk, sh.head_dim_v,
+                                     static_cast<uint16_t*>(k_out), static_cast<uint16_t*>(v_out),
+                                     static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "gather launch");
+}
+
+extern "C" int flex_attn_workspace_init(void* workspace, size_t bytes, void* stream) {
+  clear_error();
+  if (bytes == 0) return FLEX_OK;
+  if (!workspace || !aligned16(workspace) || bytes % 4)
+    return set_error(FLEX_ERR_INVALID_ARG, "workspace must be non-NULL, 16-byte aligned, whole 4-byte words");
+  const hipError_t e = launch_fill_zero(workspace, bytes, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "fill launch");
+}

@@ -1,0 +1,105 @@
+// Device helpers shared by the attention kernels (gfx950, wave64).
+//
+// Matrix-core convention used throughout (v_mfma_f32_16x16x32_bf16): a wave
+// computes D[16][16] += A[16][32] * B[32][16]. Lane l = 16*g + n supplies row
+// n of A and column n of B, each as 8 bf16 covering the 8 contraction slots
+// of lane group g; it receives D[4*g + r][n] for r = 0..3. Which contraction
+// index sits in which slot does not matter as long as A and B use the same
+// slots, which lets the kernels permute the contraction (head dims for QK^T,
+// keys for PV) freely.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flexattn {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ f32x4 mfma_16x16x32(const u32x4& a, const u32x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// Pack two floats into two bf16 (round to nearest even) in one dword, lo first.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = (__bf16)lo;
+  const __bf16 b = (__bf16)hi;
+  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+// Element offset of (page, slot, head) in a paged cache with element strides.
+struct PagedCache {
+  const uint16_t* base;
+  int64_t sp, ss, sh;
+  __device__ __forceinline__ const uint16_t* row(int32_t page, int32_t slot, int32_t head) const {
+    return base + int64_t(page) * sp + int64_t(slot) * ss + int64_t(head) * sh;
+  }
+};
+
+// Physical page of key t of a sequence whose block-table row is bt_row.
+__device__ __forceinline__ int32_t page_of(const int32_t* __restrict__ bt_row, int32_t t, int32_t P) {
+  return bt_row[t / P];
+}
+
+__device__ __forceinline__ u32x4 load16(const uint16_t* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ u32x2 load8(const uint16_t* p) {
+  return *reinterpret_cast<const u32x2*>(p);
+}
+
+// 8 key rows x 8 dims (row r holds dims 0..7 of key r as 4 dwords) ->
+// 8 B-operands, operand c holding dim c of keys 0..7 (dword w = keys 2w, 2w+1).
+__device__ __forceinline__ void transpose8x8(const u32x4 (&rows)[8], u32x4 (&ops)[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const int dw = c >> 1;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t x = rows[2 * w][dw], y = rows[2 * w + 1][dw];
+      ops[c][w] = (c & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+    }
+  }
+}
+
+// 8 key rows x 4 dims -> 4 B-operands (head_dim 64 layout).
+__device__ __forceinline__ void transpose8x4(const u32x2 (&rows)[8], u32x4 (&ops)[4]) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int dw = c >> 1;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t x = rows[2 * w][dw], y = rows[2 * w + 1][dw];
+      ops[c][w] = (c & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+    }
+  }
+}
+
+__device__ __forceinline__ float shfl_xor_f(float v, int mask) { return __shfl_xor(v, mask, 64); }
+__device__ __forceinline__ float shfl_f(float v, int src) { return __shfl(v, src, 64); }
+
+// Max / sum over the four lane groups g = 0..3 that share lane index n.
+__device__ __forceinline__ float group_max(float v) {
+  v = fmaxf(v, shfl_xor_f(v, 16));
+  return fmaxf(v, shfl_xor_f(v, 32));
+}
+__device__ __forceinline__ float group_sum(float v) {
+  v += shfl_xor_f(v, 16);
+  return v + shfl_xor_f(v, 32);
+}
+
+// Slot e (0..7) of a lane in group g within a 32-key chunk holds key
+// 16*(e/4) + 4*g + (e%4): exactly the keys whose scores the lane receives from
+// the two 16-key QK^T blocks, so P feeds the PV product with no data movement.
+__device__ __forceinline__ int chunk_key(int e, int g) { return 16 * (e >> 2) + 4 * g + (e & 3); }
+
+}  // namespace flexattn

@@ -1,0 +1,42 @@
+// Kernel parameter blocks and launchers (host-callable, defined in attention.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flexattn {
+
+struct CacheRef {
+  const uint16_t* base;
+  int64_t sp, ss, sh;  // element strides: page, slot, kv head
+};
+
+struct AttnParams {
+  const uint16_t* q;
+  CacheRef kc, vc;
+  const int32_t* bt;
+  int32_t bt_stride;
+  const int32_t* seq_lens;
+  const int32_t* qsl;
+  uint16_t* out;
+  float* lse;
+  const int32_t* items;   // device pointer to the first item of this phase
+  int32_t n_items;
+  uint32_t* counters;     // decode: one per (decode sequence, work-group column)
+  float* ws_stats;        // decode: [item][W][rows][2] (max in log2 units, sum)
+  float* ws_o;            // decode: [item][W][rows][d_v] unnormalised partial outputs
+  int32_t Hq, Hkv, G;     // G = query heads per KV head
+  int32_t P;
+  int32_t rows_per_wg;    // decode rows owned by one work-group
+  int32_t grid_y;
+  float scale_log2;       // sm_scale * log2(e)
+};
+
+hipError_t launch_decode(const AttnParams& p, int head_dim_qk, hipStream_t stream);
+hipError_t launch_prefill(const AttnParams& p, int head_dim_qk, int bm, hipStream_t stream);
+hipError_t launch_gather(const CacheRef& kc, const CacheRef& vc, bool has_v, const int32_t* bt_row,
+                         int32_t L, int32_t P, int32_t Hkv, int32_t dqk, int32_t dv,
+                         uint16_t* k_out, uint16_t* v_out, hipStream_t stream);
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace flexattn

@@ -1,0 +1,279 @@
+// Host planner: validation, phase classification, decode split-K partition,
+// prefill tile list and the co-run CU split. Pure integer (and one cost-model
+// comparison in double) host code; it makes no HIP call, so it runs and is
+// tested without a GPU.
+//
+// The paper's daemon validates each request and places it in a per-phase
+// queue before dispatch (Sec. 3.2; Sec. 3.4 "Phase-Aware Dispatch"). For one
+// mixed batch that becomes: classify each sequence by its number of new tokens
+// (one -> decode, two or more -> prefill, none -> nothing), then lay out each
+// phase's work so one kernel launch per phase covers the batch.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "host_common.h"
+
+namespace flexattn {
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool supported(const flex_attn_shape& s) {
+  const int dq = s.head_dim_qk, dv = s.head_dim_v;
+  const bool gqa = (dq == 64 && dv == 64) || (dq == 128 && dv == 128);
+  const bool latent = dq == 576 && dv == 512;
+  if (!gqa && !latent) return false;
+  if (s.page_size != 16 && s.page_size != 64) return false;
+  if (latent) return s.v_aliases_k && s.num_q_heads % kLatentRowsPerWG == 0;
+  return s.num_q_heads / s.num_kv_heads <= 16;
+}
+
+}  // namespace
+
+int set_error(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+const char* last_error() { return g_last_error.c_str(); }
+
+}  // namespace flexattn
+
+using namespace flexattn;
+
+extern "C" const char* flex_attn_status_string(int status) {
+  switch (status) {
+    case FLEX_OK: return "ok";
+    case FLEX_ERR_INVALID_ARG: return "invalid argument";
+    case FLEX_ERR_UNSUPPORTED: return "unsupported shape or option";
+    case FLEX_ERR_WORKSPACE: return "buffer too small";
+    case FLEX_ERR_HIP: return "HIP runtime error";
+    case FLEX_ERR_INTERNAL: return "internal error";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* flex_attn_last_error(void) { return flexattn::last_error(); }
+
+extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan_opts* opts,
+                              int32_t num_seqs, const int32_t* qsl, const int32_t* seq_lens,
+                              int32_t max_pages_per_seq, flex_attn_plan_t** out_plan) {
+  clear_error();
+  if (!out_plan) return set_error(FLEX_ERR_INVALID_ARG, "out_plan is NULL");
+  *out_plan = nullptr;
+  if (!shape) return set_error(FLEX_ERR_INVALID_ARG, "shape is NULL");
+  if (num_seqs < 0) return set_error(FLEX_ERR_INVALID_ARG, "num_seqs < 0");
+  if (!qsl || (num_seqs > 0 && !seq_lens))
+    return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc or seq_lens is NULL");
+  const flex_attn_shape sh = *shape;
+  if (sh.num_q_heads <= 0 || sh.num_kv_heads <= 0 || sh.num_q_heads % sh.num_kv_heads)
+    return set_error(FLEX_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (!std::isfinite(sh.sm_scale) || !(sh.sm_scale > 0.0f))
+    return set_error(FLEX_ERR_INVALID_ARG, "sm_scale must be finite and positive");
+  if (sh.v_aliases_k && (sh.num_kv_heads != 1 || sh.head_dim_v > sh.head_dim_qk))
+    return set_error(FLEX_ERR_INVALID_ARG, "v_aliases_k needs one KV head and head_dim_v <= head_dim_qk");
+  if (!supported(sh))
+    return set_error(FLEX_ERR_UNSUPPORTED, "shape outside (64,64)/(128,128) GQA with group <= 16, "
+                                           "or (576,512) aliased latent with Hq % 64 == 0; page 16/64");
+
+  flex_attn_plan_opts o;
+  std::memset(&o, 0, sizeof(o));
+  if (opts) o = *opts;
+  const bool latent = sh.head_dim_qk == 576;
+  const int64_t cus_total = o.cus_total ? o.cus_total : 256;
+  const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : 4;
+  const int64_t max_splits = o.max_splits ? o.max_splits : 32;
+  const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
+  const int64_t granule = o.split_granule ? o.split_granule : 64;
+  const int32_t bm = o.bm ? o.bm : (latent ? 64 : 128);
+  if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
+    return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
+  if (o.cus_decode < -1 || o.cus_decode > cus_total)
+    return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
+  if ((bm != 64 && bm != 128) || (latent && bm != 64))
+    return set_error(FLEX_ERR_UNSUPPORTED, "bm must be 64 or 128 (64 for the latent layout)");
+  if (max_pages_per_seq < 0) return set_error(FLEX_ERR_INVALID_ARG, "max_pages_per_seq < 0");
+  if (num_seqs > 0 && qsl[0] != 0) return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc[0] != 0");
+
+  const int64_t P = sh.page_size;
+  for (int32_t s = 0; s < num_seqs; ++s) {
+    const int64_t n = int64_t(qsl[s + 1]) - qsl[s];
+    const int64_t L = seq_lens[s];
+    if (n < 0) return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc decreases at " + std::to_string(s));
+    if (L < 0 || n > L)
+      return set_error(FLEX_ERR_INVALID_ARG, "sequence " + std::to_string(s) + ": need 0 <= n <= L");
+    if (L > int64_t(max_pages_per_seq) * P)
+      return set_error(FLEX_ERR_INVALID_ARG, "sequence " + std::to_string(s) + ": L > max_pages_per_seq * page_size");
+  }
+
+  const int32_t W = latent ? sh.num_q_heads / kLatentRowsPerWG : sh.num_kv_heads;
+  const int32_t rows_per_wg = latent ? kLatentRowsPerWG : sh.num_q_heads / sh.num_kv_heads;
+  std::vector<int32_t> dec, pre;
+  for (int32_t s = 0; s < num_seqs; ++s) {
+    const int32_t n = qsl[s + 1] - qsl[s];
+    if (n == 1) dec.push_back(s);
+    else if (n >= 2) pre.push_back(s);
+  }
+
+  // Algorithmic work of each phase (feeds the cost model and the plan info).
+  const int64_t kv_row = int64_t(sh.num_kv_heads) * 2 *
+                         (sh.v_aliases_k ? sh.head_dim_qk : sh.head_dim_qk + sh.head_dim_v);
+  int64_t dec_bytes = 0;
+  for (int32_t s : dec) dec_bytes += int64_t(seq_lens[s]) * kv_row;
+  int64_t pre_flops = 0;
+  for (int32_t s : pre) {
+    const int64_t n = qsl[s + 1] - qsl[s], L = seq_lens[s];
+    pre_flops += int64_t(sh.num_q_heads) * 2 * (sh.head_dim_qk + sh.head_dim_v) *
+                 (n * (L - n) + n * (n + 1) / 2);
+  }
+
+  // Co-run CU split: explicit, or the cost model's argmin of the slower phase.
+  int64_t cus_decode;
+  if (o.cus_decode == 0 || dec.empty() || pre.empty()) {
+    cus_decode = cus_total;
+  } else if (o.cus_decode > 0) {
+    cus_decode = o.cus_decode;
+  } else {
+    const double hbm = (o.hbm_gbps != 0.0 ? o.hbm_gbps : 8000.0) * 1e9;
+    const double bw_cu = (o.decode_gbps_per_cu != 0.0 ? o.decode_gbps_per_cu : 60.0) * 1e9;
+    const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : 5.0) * 1e12;
+    int64_t best = -1;
+    double best_t = 0.0;
+    for (int64_t nd = granule; nd < cus_total; nd += granule) {
+      const double t_dec = double(dec_bytes) / std::min(hbm, double(nd) * bw_cu);
+      const double t_pre = double(pre_flops) / (double(cus_total - nd) * fl_cu);
+      const double t = std::max(t_dec, t_pre);
+      if (best < 0 || t < best_t) { best = nd; best_t = t; }
+    }
+    cus_decode = best > 0 ? best : cus_total;
+  }
+  const int64_t cus_prefill =
+      (!dec.empty() && !pre.empty() && cus_decode < cus_total) ? cus_total - cus_decode : cus_total;
+
+  // Decode split-K partition: page-aligned key ranges sized so that the
+  // decode grid holds about wg_per_cu work-groups per decode CU.
+  const int64_t min_pps = cdiv(min_tokens, P);
+  int64_t total_pages = 0;
+  for (int32_t s : dec) total_pages += cdiv(seq_lens[s], P);
+  const int64_t pps = dec.empty() ? 0 : std::max(min_pps, cdiv(int64_t(W) * total_pages, cus_decode * wg_per_cu));
+  std::vector<int32_t> dec_words;
+  int32_t n_dec_items = 0;
+  for (size_t d = 0; d < dec.size(); ++d) {
+    const int32_t s = dec[d];
+    const int64_t Ps = cdiv(seq_lens[s], P);
+    int64_t nspl = cdiv(Ps, pps), pps_s = pps;
+    if (nspl > max_splits) {
+      pps_s = cdiv(Ps, max_splits);
+      nspl = cdiv(Ps, pps_s);
+    }
+    const int32_t first = n_dec_items;
+    for (int64_t j = 0; j < nspl; ++j) {
+      const int64_t k0 = j * pps_s * P;
+      const int64_t k1 = std::min<int64_t>(seq_lens[s], (j + 1) * pps_s * P);
+      const int32_t item[kItemWords] = {s, int32_t(j), int32_t(nspl), int32_t(k0), int32_t(k1),
+                                        first, int32_t(d), 0};
+      dec_words.insert(dec_words.end(), item, item + kItemWords);
+      ++n_dec_items;
+    }
+  }
+
+  // Prefill tiles of bm rows, the longest causal key range first.
+  struct Tile { int32_t s, t, r0, r1, kend; };
+  std::vector<Tile> tiles;
+  for (int32_t s : pre) {
+    const int32_t n = qsl[s + 1] - qsl[s], L = seq_lens[s];
+    for (int32_t t = 0; int64_t(t) * bm < n; ++t) {
+      const int32_t r0 = t * bm, r1 = std::min(n, (t + 1) * bm);
+      tiles.push_back({s, t, r0, r1, L - n + r1});
+    }
+  }
+  std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& a, const Tile& b) {
+    if (a.kend != b.kend) return a.kend > b.kend;
+    if (a.s != b.s) return a.s < b.s;
+    return a.t < b.t;
+  });
+
+  flex_attn_plan_t* plan = new (std::nothrow) flex_attn_plan_t();
+  if (!plan) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
+  plan->shape = sh;
+  plan->rows_per_wg = rows_per_wg;
+  const int32_t n_pre_items = int32_t(tiles.size());
+  const int32_t total = kHeaderWords + kItemWords * (n_dec_items + n_pre_items);
+  auto& w = plan->words;
+  w.assign(kHeaderWords, 0);
+  w[H_MAGIC] = kPlanMagic;
+  w[H_VERSION] = kPlanVersion;
+  w[H_NUM_SEQS] = num_seqs;
+  w[H_N_DEC_ITEMS] = n_dec_items;
+  w[H_N_PRE_ITEMS] = n_pre_items;
+  w[H_N_DEC_SEQS] = int32_t(dec.size());
+  w[H_N_PRE_SEQS] = int32_t(pre.size());
+  w[H_DEC_WIDTH] = W;
+  w[H_PRE_GRID_Y] = sh.num_q_heads;
+  w[H_OFF_DEC] = kHeaderWords;
+  w[H_OFF_PRE] = kHeaderWords + kItemWords * n_dec_items;
+  w[H_PPS] = int32_t(pps);
+  w[H_CUS_DEC] = int32_t(cus_decode);
+  w[H_CUS_PRE] = int32_t(cus_prefill);
+  w[H_BM] = bm;
+  w[H_TOTAL_WORDS] = total;
+  w.insert(w.end(), dec_words.begin(), dec_words.end());
+  for (const Tile& t : tiles) {
+    const int32_t item[kItemWords] = {t.s, t.t, t.r0, t.r1, t.kend, 0, 0, 0};
+    w.insert(w.end(), item, item + kItemWords);
+  }
+
+  size_t ws = 0;
+  if (n_dec_items > 0) {
+    const size_t counters = size_t(cdiv(int64_t(dec.size()) * W * 4, 256) * 256);
+    const size_t stats = size_t(n_dec_items) * W * rows_per_wg * 2 * 4;
+    ws = counters + size_t(cdiv(int64_t(stats), 256) * 256) +
+         size_t(n_dec_items) * W * rows_per_wg * sh.head_dim_v * 4;
+  }
+  flex_attn_plan_info& info = plan->info;
+  std::memset(&info, 0, sizeof(info));
+  info.num_seqs = num_seqs;
+  info.n_decode_seqs = int32_t(dec.size());
+  info.n_prefill_seqs = int32_t(pre.size());
+  info.n_decode_items = n_dec_items;
+  info.n_prefill_items = n_pre_items;
+  info.decode_wg_width = W;
+  info.prefill_grid_y = sh.num_q_heads;
+  info.pages_per_split = int32_t(pps);
+  info.cus_decode = int32_t(cus_decode);
+  info.cus_prefill = int32_t(cus_prefill);
+  info.bm = bm;
+  info.plan_words = total;
+  info.device_plan_bytes = size_t(cdiv(int64_t(total) * 4, 256) * 256);
+  info.workspace_bytes = ws;
+  info.decode_bytes = double(dec_bytes);
+  info.prefill_flops = double(pre_flops);
+  *out_plan = plan;
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_plan_info_get(const flex_attn_plan_t* plan, flex_attn_plan_info* out) {
+  clear_error();
+  if (!plan || !out) return set_error(FLEX_ERR_INVALID_ARG, "plan or out is NULL");
+  *out = plan->info;
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_plan_export(const flex_attn_plan_t* plan, int32_t* h_dst, size_t n_words) {
+  clear_error();
+  if (!plan || !h_dst) return set_error(FLEX_ERR_INVALID_ARG, "plan or destination is NULL");
+  if (n_words < plan->words.size())
+    return set_error(FLEX_ERR_WORKSPACE, "destination holds fewer words than the plan");
+  std::memcpy(h_dst, plan->words.data(), plan->words.size() * sizeof(int32_t));
+  return FLEX_OK;
+}
+
+extern "C" void flex_attn_plan_destroy(flex_attn_plan_t* plan) { delete plan; }

@@ -1,0 +1,352 @@
+"""ctypes binding of libflexattn.so (include/flexattn.h).
+
+Argument marshalling only: every step of the attention path runs in the HIP
+library. PyTorch supplies device memory and streams. Importing this module
+raises if the library has not been built; there is no fallback.
+
+Functions keep the C names (``flex_attn_plan``, ``flex_attn_decode``, ...);
+``PagedAttention`` bundles a plan with its device copy and workspace for the
+common case of running one batch.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflexattn.so")
+
+FLEX_OK = 0
+FLEX_ERR_INVALID_ARG = -1
+FLEX_ERR_UNSUPPORTED = -2
+FLEX_ERR_WORKSPACE = -3
+FLEX_ERR_HIP = -4
+FLEX_ERR_INTERNAL = -5
+FLEX_MODE_SERIAL = 0
+FLEX_MODE_CORUN = 1
+
+EXPORTED = [
+    "flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan", "flex_attn_plan_info_get",
+    "flex_attn_plan_export", "flex_attn_plan_upload", "flex_attn_plan_destroy", "flex_attn_decode",
+    "flex_attn_prefill", "flex_attn_mixed", "flex_attn_corun_create", "flex_attn_corun_destroy",
+    "flex_attn_corun_streams", "flex_attn_corun_set_timing", "flex_attn_corun_timing_read",
+    "flex_attn_debug_gather", "flex_attn_workspace_init",
+]
+FLEX_TIMING_RING = 1024
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim_qk", ctypes.c_int32), ("head_dim_v", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("sm_scale", ctypes.c_float),
+                ("v_aliases_k", ctypes.c_int32)]
+
+
+class PlanOpts(ctypes.Structure):
+    _fields_ = [("cus_total", ctypes.c_int32), ("cus_decode", ctypes.c_int32), ("bm", ctypes.c_int32),
+                ("min_split_tokens", ctypes.c_int32), ("max_splits", ctypes.c_int32),
+                ("wg_per_cu", ctypes.c_int32), ("split_granule", ctypes.c_int32),
+                ("hbm_gbps", ctypes.c_double), ("decode_gbps_per_cu", ctypes.c_double),
+                ("prefill_tflops_per_cu", ctypes.c_double)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("n_decode_seqs", ctypes.c_int32),
+                ("n_prefill_seqs", ctypes.c_int32), ("n_decode_items", ctypes.c_int32),
+                ("n_prefill_items", ctypes.c_int32), ("decode_wg_width", ctypes.c_int32),
+                ("prefill_grid_y", ctypes.c_int32), ("pages_per_split", ctypes.c_int32),
+                ("cus_decode", ctypes.c_int32), ("cus_prefill", ctypes.c_int32), ("bm", ctypes.c_int32),
+                ("plan_words", ctypes.c_int32), ("device_plan_bytes", ctypes.c_size_t),
+                ("workspace_bytes", ctypes.c_size_t), ("decode_bytes", ctypes.c_double),
+                ("prefill_flops", ctypes.c_double)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class Args(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+                ("k_stride", ctypes.c_int64 * 3), ("v_stride", ctypes.c_int64 * 3),
+                ("num_pages", ctypes.c_int32), ("block_table", ctypes.c_void_p),
+                ("block_table_stride", ctypes.c_int32), ("seq_lens", ctypes.c_void_p),
+                ("query_start_loc", ctypes.c_void_p), ("out", ctypes.c_void_p), ("lse", ctypes.c_void_p),
+                ("d_plan", ctypes.c_void_p), ("d_plan_bytes", ctypes.c_size_t),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class FlexAttnError(RuntimeError):
+    def __init__(self, status: int, what: str, detail: str):
+        super().__init__(f"{what}: status {status} ({detail})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libflexattn.so (once). Raises if it is missing: there is no fallback."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing; build it with "
+                           "`python -m paper_2606_04415_amd.build` (hipcc, gfx950)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    L.flex_attn_status_string.argtypes = [ctypes.c_int]
+    L.flex_attn_status_string.restype = ctypes.c_char_p
+    L.flex_attn_last_error.argtypes = []
+    L.flex_attn_last_error.restype = ctypes.c_char_p
+    L.flex_attn_plan.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(PlanOpts), i32,
+                                 ctypes.POINTER(i32), ctypes.POINTER(i32), i32, ctypes.POINTER(vp)]
+    L.flex_attn_plan_info_get.argtypes = [vp, ctypes.POINTER(PlanInfo)]
+    L.flex_attn_plan_export.argtypes = [vp, ctypes.POINTER(i32), sz]
+    L.flex_attn_plan_upload.argtypes = [vp, vp, sz, vp]
+    L.flex_attn_plan_destroy.argtypes = [vp]
+    L.flex_attn_plan_destroy.restype = None
+    for f in ("flex_attn_decode", "flex_attn_prefill"):
+        getattr(L, f).argtypes = [vp, ctypes.POINTER(Args), vp]
+    L.flex_attn_mixed.argtypes = [vp, ctypes.POINTER(Args), ctypes.c_int, vp, vp]
+    L.flex_attn_corun_create.argtypes = [i32, i32, ctypes.POINTER(vp)]
+    L.flex_attn_corun_destroy.argtypes = [vp]
+    L.flex_attn_corun_destroy.restype = None
+    L.flex_attn_corun_streams.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp)]
+    L.flex_attn_corun_set_timing.argtypes = [vp, ctypes.c_int]
+    L.flex_attn_corun_timing_read.argtypes = [vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float),
+                                              i32, ctypes.POINTER(i32)]
+    L.flex_attn_debug_gather.argtypes = [vp, ctypes.POINTER(Args), i32, i32, vp, vp, vp]
+    L.flex_attn_workspace_init.argtypes = [vp, sz, vp]
+    for f in EXPORTED:
+        if f not in ("flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan_destroy",
+                     "flex_attn_corun_destroy"):
+            getattr(L, f).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().flex_attn_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().flex_attn_last_error().decode()
+
+
+def check(status: int, what: str):
+    if status != FLEX_OK:
+        raise FlexAttnError(status, what, f"{status_string(status)}: {last_error()}")
+
+
+def _i32_array(values: Sequence[int]):
+    vals = [int(v) for v in values]
+    return (ctypes.c_int32 * max(1, len(vals)))(*vals)
+
+
+class Plan:
+    """Owning wrapper of a flex_attn_plan_t*."""
+
+    def __init__(self, handle: int):
+        self.handle = ctypes.c_void_p(handle)
+        info = PlanInfo()
+        check(lib().flex_attn_plan_info_get(self.handle, ctypes.byref(info)), "flex_attn_plan_info_get")
+        self.info = info.as_dict()
+
+    def export(self):
+        n = self.info["plan_words"]
+        buf = (ctypes.c_int32 * n)()
+        check(lib().flex_attn_plan_export(self.handle, buf, n), "flex_attn_plan_export")
+        return list(buf)
+
+    def close(self):
+        if self.handle and self.handle.value:
+            lib().flex_attn_plan_destroy(self.handle)
+            self.handle = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def make_shape(num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, page_size, sm_scale, v_aliases_k=False):
+    return Shape(num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, page_size, float(sm_scale),
+                 1 if v_aliases_k else 0)
+
+
+def make_opts(**kw) -> PlanOpts:
+    o = PlanOpts()
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def flex_attn_plan(shape: Shape, opts: Optional[PlanOpts], query_start_loc: Sequence[int],
+                   seq_lens: Sequence[int], max_pages_per_seq: int) -> Plan:
+    """Host plan (no HIP call). Raises FlexAttnError with the library's status on failure."""
+    qsl = [int(x) for x in query_start_loc]
+    sl = [int(x) for x in seq_lens]
+    out = ctypes.c_void_p()
+    st = lib().flex_attn_plan(ctypes.byref(shape), ctypes.byref(opts) if opts is not None else None,
+                              len(sl), _i32_array(qsl), _i32_array(sl), int(max_pages_per_seq),
+                              ctypes.byref(out))
+    check(st, "flex_attn_plan")
+    return Plan(out.value)
+
+
+def plan_status(shape: Shape, opts: Optional[PlanOpts], query_start_loc, seq_lens, max_pages_per_seq) -> int:
+    """Status code of flex_attn_plan for these inputs (the plan, if any, is freed)."""
+    out = ctypes.c_void_p()
+    qsl = list(query_start_loc)
+    sl = list(seq_lens)
+    st = lib().flex_attn_plan(ctypes.byref(shape), ctypes.byref(opts) if opts is not None else None,
+                              len(sl), _i32_array(qsl), _i32_array(sl), int(max_pages_per_seq),
+                              ctypes.byref(out))
+    if st == FLEX_OK:
+        lib().flex_attn_plan_destroy(out)
+    return st
+
+
+# ------------------------------------------------------- torch adapters ---
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def current_stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def make_args(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, lse=None,
+              d_plan=None, workspace=None) -> Args:
+    """Args from device tensors (bf16 caches [pages, P, Hkv, d] with unit inner stride)."""
+    a = Args()
+    a.q = q.data_ptr()
+    a.k_cache = k_cache.data_ptr()
+    a.v_cache = v_cache.data_ptr() if v_cache is not None else None
+    ks = k_cache.stride()
+    a.k_stride = (ctypes.c_int64 * 3)(ks[0], ks[1], ks[2])
+    vsrc = v_cache if v_cache is not None else k_cache
+    vs = vsrc.stride()
+    a.v_stride = (ctypes.c_int64 * 3)(vs[0], vs[1], vs[2])
+    a.num_pages = k_cache.shape[0]
+    a.block_table = block_table.data_ptr()
+    a.block_table_stride = block_table.stride(0)
+    a.seq_lens = seq_lens.data_ptr()
+    a.query_start_loc = query_start_loc.data_ptr()
+    a.out = out.data_ptr()
+    a.lse = lse.data_ptr() if lse is not None else None
+    if d_plan is not None:
+        a.d_plan = d_plan.data_ptr()
+        a.d_plan_bytes = d_plan.numel() * d_plan.element_size()
+    if workspace is not None:
+        a.workspace = workspace.data_ptr()
+        a.workspace_bytes = workspace.numel() * workspace.element_size()
+    return a
+
+
+def flex_attn_plan_upload(plan: Plan, d_plan, stream=None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_plan_upload(plan.handle, ctypes.c_void_p(d_plan.data_ptr()),
+                                      d_plan.numel() * d_plan.element_size(), s), "flex_attn_plan_upload")
+
+
+def flex_attn_decode(plan: Plan, args: Args, stream=None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_decode(plan.handle, ctypes.byref(args), s), "flex_attn_decode")
+
+
+def flex_attn_prefill(plan: Plan, args: Args, stream=None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_prefill(plan.handle, ctypes.byref(args), s), "flex_attn_prefill")
+
+
+def flex_attn_mixed(plan: Plan, args: Args, mode: int, stream=None, corun: "Corun" = None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_mixed(plan.handle, ctypes.byref(args), mode, s,
+                                corun.handle if corun is not None else None), "flex_attn_mixed")
+
+
+def flex_attn_debug_gather(plan: Plan, args: Args, seq: int, seq_len: int, k_out, v_out=None, stream=None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_debug_gather(plan.handle, ctypes.byref(args), seq, seq_len, _ptr(k_out),
+                                       _ptr(v_out), s), "flex_attn_debug_gather")
+
+
+def flex_attn_workspace_init(workspace, stream=None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_workspace_init(ctypes.c_void_p(workspace.data_ptr()),
+                                         workspace.numel() * workspace.element_size(), s),
+          "flex_attn_workspace_init")
+
+
+class Corun:
+    """Owning wrapper of a co-run stream pair (two CU-masked streams)."""
+
+    def __init__(self, cus_prefill: int, cus_decode: int):
+        h = ctypes.c_void_p()
+        check(lib().flex_attn_corun_create(cus_prefill, cus_decode, ctypes.byref(h)), "flex_attn_corun_create")
+        self.handle = h
+        self.cus_prefill = cus_prefill
+        self.cus_decode = cus_decode
+
+    def streams(self):
+        p, d = ctypes.c_void_p(), ctypes.c_void_p()
+        check(lib().flex_attn_corun_streams(self.handle, ctypes.byref(p), ctypes.byref(d)),
+              "flex_attn_corun_streams")
+        return p.value, d.value
+
+    def set_timing(self, enable: bool = True):
+        check(lib().flex_attn_corun_set_timing(self.handle, 1 if enable else 0), "flex_attn_corun_set_timing")
+
+    def timing_read(self):
+        """(prefill_ms, decode_ms) lists of the recorded steps, oldest first (waits for them)."""
+        n = FLEX_TIMING_RING
+        pre = (ctypes.c_float * n)()
+        dec = (ctypes.c_float * n)()
+        cnt = ctypes.c_int32()
+        check(lib().flex_attn_corun_timing_read(self.handle, pre, dec, n, ctypes.byref(cnt)),
+              "flex_attn_corun_timing_read")
+        return list(pre[:cnt.value]), list(dec[:cnt.value])
+
+    def close(self):
+        if self.handle and self.handle.value:
+            lib().flex_attn_corun_destroy(self.handle)
+            self.handle = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class PagedAttention:
+    """One batch's plan, its device copy and its workspace (torch-allocated).
+
+    ``inputs`` holds the device tensors: q, k_cache, v_cache (or None when V
+    aliases K), block_table, seq_lens, query_start_loc (int32). ``run`` calls
+    the library on the current torch stream.
+    """
+
+    def __init__(self, shape: Shape, opts: Optional[PlanOpts], h_query_start_loc, h_seq_lens,
+                 max_pages_per_seq: int, device="cuda"):
+        import torch
+        self.shape = shape
+        self.plan = flex_attn_plan(shape, opts, h_query_start_loc, h_seq_lens, max_pages_per_seq)
+        info = self.plan.info
+        self.d_plan = torch.empty(max(256, info["device_plan_bytes"]), dtype=torch.uint8, device=device)
+        self.workspace = torch.zeros(max(256, info["workspace_bytes"]), dtype=torch.uint8, device=device)
+        flex_attn_plan_upload(self.plan, self.d_plan)
+
+    def args(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, lse=None) -> Args:
+        return make_args(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, lse,
+                         self.d_plan, self.workspace)
+
+    def alloc_out(self, q, with_lse=False):
+        import torch
+        T, Hq = q.shape[0], q.shape[1]
+        out = torch.empty((T, Hq, self.shape.head_dim_v), dtype=torch.bfloat16, device=q.device)
+        lse = torch.empty((T, Hq), dtype=torch.float32, device=q.device) if with_lse else None
+        return out, lse

@@ -1,0 +1,226 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Small batches (several tiles, ragged tails, split decode sequences) are
+compared in full; the five workloads at full size are compared on sampled
+rows the oracle computes one by one. Unused pages hold NaN and tail slots
+hold +/-1e4 (see workloads.make_batch), so a wrong page index or an unmasked
+tail read breaks parity.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle.attention as OA
+from paper_2606_04415_amd import flexattn as F
+from paper_2606_04415_amd.workloads import WORKLOADS, make_batch
+
+from gpu_common import check_close, custom_batch, device_inputs, log, run
+
+pytestmark = pytest.mark.gpu
+
+QW = WORKLOADS["decode"]     # Qwen2.5-7B geometry
+TINY = WORKLOADS["tiny"]
+MLA = WORKLOADS["mla"]
+
+
+def oracle_full(b):
+    w = b.workload
+    return OA.paged_attention(b.q, b.k_cache, b.v_cache, b.block_table, b.seq_lens, b.query_start_loc,
+                              w.sm_scale, num_kv_heads=w.num_kv_heads, page_size=w.page_size,
+                              head_dim_v=w.head_dim_v, v_aliases_k=w.v_aliases_k)
+
+
+def full_check(b, opts=None, what=""):
+    out, lse, _ = run(b, opts=opts)
+    ref_o, ref_l = oracle_full(b)
+    rows = ~np.isnan(ref_l[:, 0])
+    check_close(out, ref_o, f"{what} out", rows)
+    check_close(lse, ref_l, f"{what} lse", rows)
+    return out, lse
+
+
+def test_tiny_workload_full():
+    log("tiny mixed workload (2 prompts x 64 + 4 decodes x 128, GQA 4/1, d 64, page 16)")
+    b = make_batch(TINY, seed=0)
+    full_check(b, what="tiny")
+
+
+RAGGED_GQA = [
+    # (n, L) per sequence: decodes over ragged contexts, chunked and whole prompts, an empty sequence
+    ([1, 1, 1, 1, 1, 1, 1, 0, 200, 100, 2, 129, 1], [1, 15, 16, 17, 129, 1000, 4095, 7, 200, 300, 5, 129, 33]),
+]
+
+
+@pytest.mark.parametrize("min_split", [0, 16])
+def test_ragged_gqa_d128_page16(min_split):
+    ns, ls = RAGGED_GQA[0]
+    b = custom_batch(QW, ns, ls, seed=3)
+    opts = F.make_opts(min_split_tokens=min_split, max_splits=4 if min_split else 0)
+    log(f"ragged GQA 28/4 d128 page16, min_split_tokens={min_split}")
+    full_check(b, opts, "ragged-d128")
+
+
+def test_ragged_gqa_d64_page64_group16():
+    ns = [1, 1, 1, 70, 1, 130, 3]
+    ls = [1, 63, 65, 70, 2000, 400, 3]
+    b = custom_batch(QW, ns, ls, seed=4, num_q_heads=32, num_kv_heads=2, head_dim_qk=64, head_dim_v=64,
+                     page_size=64, sm_scale=0.125)
+    log("ragged GQA 32/2 (group 16) d64 page64")
+    full_check(b, F.make_opts(min_split_tokens=64), "ragged-d64")
+
+
+def test_gqa_bm64_tiles():
+    ns, ls = [77, 1, 150], [77, 500, 300]
+    b = custom_batch(QW, ns, ls, seed=5)
+    log("GQA prefill with 64-row tiles")
+    full_check(b, F.make_opts(bm=64), "bm64")
+
+
+@pytest.mark.parametrize("hq", [64, 128])
+def test_ragged_latent(hq):
+    ns = [1, 1, 1, 1, 130, 70, 1]
+    ls = [1, 63, 65, 3000, 130, 200, 700]
+    b = custom_batch(MLA, ns, ls, seed=6, num_q_heads=hq)
+    log(f"ragged latent 576/512 page64, {hq} heads, forced splits")
+    full_check(b, F.make_opts(min_split_tokens=128, max_splits=8), f"latent-h{hq}")
+
+
+def test_single_key_is_exact():
+    """L = 1: the one weight is exactly 1, so out must equal V[0] bit for bit."""
+    b = custom_batch(QW, [1, 1], [1, 1], seed=7)
+    out, _, _ = run(b)
+    for s in range(2):
+        page = int(b.block_table[s, 0])
+        v0 = b.v_cache[page, 0]                       # [Hkv, d]
+        ref = v0.repeat_interleave(QW.num_q_heads // QW.num_kv_heads, 0)
+        assert torch.equal(out[s], ref)
+
+
+def test_gather_bit_exact():
+    for name in ("tiny", "decode"):
+        w = WORKLOADS[name]
+        b = make_batch(w, seed=0)
+        d = device_inputs(b)
+        pa = F.PagedAttention(F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v,
+                                           w.page_size, w.sm_scale, w.v_aliases_k), None,
+                              b.query_start_loc.tolist(), b.seq_lens.tolist(), b.block_table.shape[1])
+        out, _ = pa.alloc_out(d["q"])
+        args = pa.args(d["q"], d["k_cache"], d["v_cache"], d["block_table"], d["seq_lens"],
+                       d["query_start_loc"], out)
+        seqs = range(len(b.seq_lens))
+        log(f"{name}: gather every sequence ({len(b.seq_lens)})")
+        for s in seqs:
+            L = int(b.seq_lens[s])
+            ko = torch.empty((L, w.num_kv_heads, w.head_dim_qk), dtype=torch.bfloat16, device="cuda")
+            vo = torch.empty((L, w.num_kv_heads, w.head_dim_v), dtype=torch.bfloat16, device="cuda")
+            F.flex_attn_debug_gather(pa.plan, args, s, L, ko, vo)
+            t = torch.arange(L)
+            pages = b.block_table[s, t // w.page_size].long()
+            kref = b.k_cache[pages, t % w.page_size]
+            vref = b.v_cache[pages, t % w.page_size]
+            torch.cuda.synchronize()
+            assert torch.equal(ko.cpu().view(torch.int16), kref.view(torch.int16)), f"K of seq {s}"
+            assert torch.equal(vo.cpu().view(torch.int16), vref.view(torch.int16)), f"V of seq {s}"
+
+
+def test_page_permutation_bitwise():
+    """Same logical batch in two physical page orders: bit-identical outputs."""
+    ns, ls = [1, 1, 60, 1], [700, 31, 90, 2000]
+    b1 = custom_batch(QW, ns, ls, seed=8)
+    b2 = custom_batch(QW, ns, ls, seed=8)
+    # re-place b1's logical pages at a new permutation in b2
+    rng = torch.Generator().manual_seed(99)
+    perm = torch.randperm(b1.k_cache.shape[0], generator=rng)
+    b2.k_cache = torch.empty_like(b1.k_cache)
+    b2.v_cache = torch.empty_like(b1.v_cache)
+    b2.k_cache[perm] = b1.k_cache
+    b2.v_cache[perm] = b1.v_cache
+    b2.block_table = perm[b1.block_table.long()].to(torch.int32)
+    o1, l1, _ = run(b1)
+    o2, l2, _ = run(b2)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+def test_run_to_run_bitwise():
+    ns, ls = RAGGED_GQA[0]
+    b = custom_batch(QW, ns, ls, seed=9)
+    opts = F.make_opts(min_split_tokens=16, max_splits=8)
+    o1, l1, pa = run(b, opts=opts)
+    d = device_inputs(b)
+    o2, l2, _ = run(b, d=d, pa=pa)
+    o3, l3, _ = run(b, d=d, pa=pa)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(o2.view(torch.int16), o3.view(torch.int16))
+    assert torch.equal(l1, l3)
+
+
+@pytest.mark.parametrize("split", [(128, 128), (192, 64), (64, 192)])
+def test_corun_bitwise_equals_serial(split):
+    cp, cd = split
+    ns, ls = [300, 1, 1, 1, 1, 120], [900, 1000, 17, 4000, 2500, 120]
+    b = custom_batch(QW, ns, ls, seed=10)
+    opts = F.make_opts(cus_decode=cd)
+    log(f"co-run prefill {cp} CUs / decode {cd} CUs vs serial")
+    d = device_inputs(b)
+    o_s, l_s, pa = run(b, d=d, opts=opts)
+    corun = F.Corun(cp, cd)
+    o_c, l_c, _ = run(b, d=d, pa=pa, mode=F.FLEX_MODE_CORUN, corun=corun)
+    assert torch.equal(o_s.view(torch.int16), o_c.view(torch.int16))
+    assert torch.equal(l_s, l_c)
+    ref_o, ref_l = oracle_full(b)
+    check_close(o_c, ref_o, "corun out", ~np.isnan(ref_l[:, 0]))
+    corun.close()
+
+
+def sampled_check(name, n_dec=6, n_pre_rows=12, mode=F.FLEX_MODE_SERIAL, split=None):
+    w = WORKLOADS[name]
+    log(f"{name}: drawing the full-size batch")
+    b = make_batch(w, seed=0)
+    d = device_inputs(b)
+    corun = None
+    opts = None
+    if split is not None:
+        opts = F.make_opts(cus_decode=split[1])
+        corun = F.Corun(*split)
+    out, lse, pa = run(b, d=d, mode=mode, opts=opts, corun=corun)
+    log(f"{name}: plan {pa.plan.info['n_decode_items']} decode items, {pa.plan.info['n_prefill_items']} tiles")
+    qsl = b.query_start_loc.tolist()
+    ls = b.seq_lens.tolist()
+    rng = np.random.default_rng(0)
+    dec = [s for s in range(len(ls)) if qsl[s + 1] - qsl[s] == 1]
+    pre = [s for s in range(len(ls)) if qsl[s + 1] - qsl[s] >= 2]
+    picks = []
+    if dec:
+        # the longest and shortest decode sequences plus random ones
+        order = sorted(dec, key=lambda s: ls[s])
+        chosen = {order[0], order[-1]} | set(rng.choice(dec, size=min(n_dec, len(dec)), replace=False).tolist())
+        picks += [(s, 0) for s in sorted(chosen)]
+    for s in pre:
+        n = qsl[s + 1] - qsl[s]
+        rows = {0, 1, n - 1, n // 2, 127 % n, 128 % n} | set(rng.integers(0, n, size=n_pre_rows).tolist())
+        picks += [(s, int(i)) for i in sorted(rows)]
+    ref_o, ref_l = OA.attention_rows(b.q, b.k_cache, b.v_cache, b.block_table, b.seq_lens, b.query_start_loc,
+                                     w.sm_scale, picks, num_kv_heads=w.num_kv_heads, page_size=w.page_size,
+                                     head_dim_v=w.head_dim_v, v_aliases_k=w.v_aliases_k)
+    idx = [qsl[s] + i for s, i in picks]
+    check_close(out[idx], ref_o, f"{name} sampled out ({len(picks)} rows)")
+    check_close(lse[idx], ref_l, f"{name} sampled lse")
+    # every row must be finite (NaN poison would propagate from a stray page)
+    assert torch.isfinite(out.float()).all()
+    if corun is not None:
+        corun.close()
+    return out
+
+
+@pytest.mark.parametrize("name", ["decode", "prefill", "mixed"])
+def test_full_workload_sampled(name):
+    sampled_check(name)
+
+
+def test_full_mixed_corun_sampled():
+    sampled_check("mixed", mode=F.FLEX_MODE_CORUN, split=(128, 128))
+
+
+def test_full_latent_sampled():
+    sampled_check("mla", n_dec=4, n_pre_rows=6)
