@@ -94,6 +94,7 @@ def main():
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--split", default="128:128", help="prefill:decode CUs for co-run")
     ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over steps")
+    ap.add_argument("--bm", type=int, default=0, help="prefill rows per tile (0: library default)")
     ap.add_argument("--no-serial", action="store_true", help="skip the serial comparison leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -129,7 +130,7 @@ def main():
     shape = F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v, w.page_size,
                          w.sm_scale, w.v_aliases_k)
     t0 = time.perf_counter()
-    pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd), b.query_start_loc.tolist(), b.seq_lens.tolist(),
+    pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd, bm=args.bm), b.query_start_loc.tolist(), b.seq_lens.tolist(),
                           b.block_table.shape[1])
     plan_us = (time.perf_counter() - t0) * 1e6
     info = pa.plan.info

@@ -79,7 +79,7 @@ typedef struct flex_attn_shape {
 typedef struct flex_attn_plan_opts {
   int32_t cus_total;          /* [256] */
   int32_t cus_decode;         /* [0 = all CUs] */
-  int32_t bm;                 /* prefill rows per tile [128; 64 for 576/512] */
+  int32_t bm;                 /* prefill rows per tile: 16 or 32 [32]; 64 for 576/512 */
   int32_t min_split_tokens;   /* smallest decode split, in keys [256] */
   int32_t max_splits;         /* most splits per decode sequence [32] */
   int32_t wg_per_cu;          /* decode work-groups aimed at per CU [4] */
@@ -96,6 +96,7 @@ typedef struct flex_attn_plan_info {
   int32_t n_prefill_seqs;    /* sequences with two or more new tokens */
   int32_t n_decode_items;    /* (sequence, split) work items */
   int32_t n_prefill_items;   /* (sequence, row tile) work items */
+  int32_t n_split_seqs;      /* decode sequences split into more than one item */
   int32_t decode_wg_width;   /* work-groups per decode item (grid y) */
   int32_t prefill_grid_y;    /* work-groups per prefill tile (grid y) */
   int32_t pages_per_split;
@@ -123,10 +124,12 @@ typedef struct flex_attn_plan_info {
  *           untouched.
  *  lse      fp32 [T, Hq] or NULL.
  *  d_plan   the plan uploaded with flex_attn_plan_upload.
- *  workspace  device scratch of >= flex_attn_plan_info.workspace_bytes; it
- *           must be zero-filled before its first use, and every completed
- *           decode leaves its counters at zero again. Two runs in flight at
- *           once must not share a workspace. */
+ *  workspace  device scratch of >= flex_attn_plan_info.workspace_bytes (may
+ *           be NULL when that is 0): the split decode items' partial results,
+ *           written by the decode kernel and read by the merge kernel that
+ *           follows it on the same stream. Its contents need no
+ *           initialisation. Two runs in flight at once must not share a
+ *           workspace. */
 typedef struct flex_attn_args {
   const void* q;
   const void* k_cache;
@@ -184,9 +187,9 @@ int flex_attn_plan_upload(const flex_attn_plan_t* plan, void* d_dst, size_t dst_
 void flex_attn_plan_destroy(flex_attn_plan_t* plan);
 
 /* Decode phase (sequences with one new token): split-K attention over each
- * sequence's pages, streamed from HBM, and the merge of the splits
- * (out = sum_j e^{m_j - M} O_j / sum_j e^{m_j - M} l_j, M = max_j m_j), done
- * by the last work-group to finish each (sequence, KV head). */
+ * sequence's pages, streamed from HBM, then (when some sequence is split) a
+ * second launch that merges the splits in split order:
+ * out = sum_j e^{m_j - M} O_j / sum_j e^{m_j - M} l_j, M = max_j m_j. */
 int flex_attn_decode(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream);
 
 /* Prefill phase (sequences with two or more new tokens): causal flash
@@ -233,7 +236,8 @@ int flex_attn_corun_timing_read(flex_attn_corun_t* corun, float* prefill_ms, flo
 int flex_attn_debug_gather(const flex_attn_plan_t* plan, const flex_attn_args* args, int32_t seq,
                            int32_t seq_len, void* k_out, void* v_out, void* stream);
 
-/* Zero the first bytes of a workspace on stream with a fill kernel. */
+/* Zero a buffer (e.g. a workspace) on stream with a fill kernel; bytes must
+ * be a multiple of 4. No run call requires it. */
 int flex_attn_workspace_init(void* workspace, size_t bytes, void* stream);
 
 #ifdef __cplusplus

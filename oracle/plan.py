@@ -20,8 +20,10 @@ the contract is:
   n_s = ceil(P_s / pps_s), else pps_s = pps; split j covers keys
   [j * pps_s * P, min(L_s, (j + 1) * pps_s * P)). Items: decode sequences in
   batch order, splits ascending.
-* prefill tiles of BM rows: rows [t*BM, min(n, (t+1)*BM)), key_end =
-  L - n + row_end; ordered by key_end descending, then sequence, then tile.
+* prefill tiles of BM rows (BM 32 by default for grouped-query heads, 64 for
+  the latent layout): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
+  ordered by key_end descending, then sequence, then tile. Each tile is served
+  by Hkv * ceil(G / 8) work-groups (grouped-query) or Hq (latent).
 * co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
@@ -61,7 +63,7 @@ class Shape:
 class Opts:
     cus_total: int = 0           # 0 -> 256
     cus_decode: int = 0          # 0 -> all; -1 -> cost model
-    bm: int = 0                  # 0 -> 128 (64 for the 576/512 layout)
+    bm: int = 0                  # 0 -> 32 (64 for the 576/512 layout)
     min_split_tokens: int = 0    # 0 -> 256
     max_splits: int = 0          # 0 -> 32
     wg_per_cu: int = 0           # 0 -> 4
@@ -114,12 +116,12 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     min_tokens = o.min_split_tokens or 256
     granule = o.split_granule or 64
     mla = sh.head_dim_qk == 576
-    bm = o.bm or (64 if mla else 128)
+    bm = o.bm or (64 if mla else 32)
     if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:
         return PlanResult(ERR_INVALID_ARG)
     if o.cus_decode < -1 or o.cus_decode > cus_total:
         return PlanResult(ERR_INVALID_ARG)
-    if bm not in (64, 128) or (mla and bm != 64):
+    if (mla and bm != 64) or (not mla and bm not in (16, 32)):
         return PlanResult(ERR_UNSUPPORTED)
     # --- integer metadata checks
     if max_pages_per_seq < 0:
@@ -172,6 +174,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     total_pages = sum(cdiv(seq_lens[s], P) for s in dec)
     pps = max(min_pps, cdiv(W * total_pages, cus_decode * wg_per_cu)) if dec else 0
     dec_items = []
+    n_split = 0
     for d, s in enumerate(dec):
         Ps = cdiv(seq_lens[s], P)
         nspl = cdiv(Ps, pps)
@@ -180,6 +183,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
             pps_s = cdiv(Ps, max_splits)
             nspl = cdiv(Ps, pps_s)
         first = len(dec_items)
+        n_split += nspl > 1
         for j in range(nspl):
             k0 = j * pps_s * P
             k1 = min(seq_lens[s], (j + 1) * pps_s * P)
@@ -196,18 +200,20 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
 
     nd_, np_ = len(dec_items), len(tiles)
     total = HEADER + ITEM * (nd_ + np_)
-    pre_height = sh.num_q_heads
+    G = sh.num_q_heads // sh.num_kv_heads
+    pre_height = sh.num_q_heads if mla else sh.num_kv_heads * cdiv(G, 8)
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
            HEADER, HEADER + ITEM * nd_, pps, cus_decode, cus_prefill, bm, total]
     blob = hdr + [x for it in dec_items for x in it] + [x for it in tiles for x in it]
-    if nd_ == 0:
+    # workspace: (max, sum) per decode item, column and row, then the partial outputs;
+    # only needed when some decode sequence is split
+    if n_split == 0:
         ws = 0
     else:
-        counters = cdiv(len(dec) * W * 4, 256) * 256
         stats = nd_ * W * rows_per_wg * 2 * 4
-        ws = counters + cdiv(stats, 256) * 256 + nd_ * W * rows_per_wg * sh.head_dim_v * 4
+        ws = cdiv(stats, 256) * 256 + nd_ * W * rows_per_wg * sh.head_dim_v * 4
     info = dict(num_seqs=B, n_decode_seqs=len(dec), n_prefill_seqs=len(pre),
-                n_decode_items=nd_, n_prefill_items=np_, decode_wg_width=W,
+                n_decode_items=nd_, n_prefill_items=np_, n_split_seqs=n_split, decode_wg_width=W,
                 prefill_grid_y=pre_height, pages_per_split=pps,
                 cus_decode=cus_decode, cus_prefill=cus_prefill, bm=bm,
                 plan_words=total, device_plan_bytes=cdiv(total * 4, 256) * 256,

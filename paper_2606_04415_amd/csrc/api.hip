@@ -69,7 +69,7 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
   if (a->block_table_stride < 1) return set_error(FLEX_ERR_INVALID_ARG, "block_table_stride < 1");
   if (a->d_plan_bytes < info.device_plan_bytes)
     return set_error(FLEX_ERR_WORKSPACE, "d_plan_bytes smaller than the plan's device_plan_bytes");
-  if (info.n_decode_items > 0) {
+  if (info.workspace_bytes > 0) {
     if (!a->workspace) return set_error(FLEX_ERR_INVALID_ARG, "workspace is NULL");
     if (!aligned16(a->workspace)) return set_error(FLEX_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
     if (a->workspace_bytes < info.workspace_bytes)
@@ -90,14 +90,12 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
   p->P = sh.page_size;
   p->rows_per_wg = plan->rows_per_wg;
   p->scale_log2 = sh.sm_scale * 1.4426950408889634f;
-  if (info.n_decode_items > 0) {
+  if (info.workspace_bytes > 0) {
     const int32_t W = info.decode_wg_width;
-    const size_t counters = ((size_t(info.n_decode_seqs) * W * 4 + 255) / 256) * 256;
     const size_t stats = size_t(info.n_decode_items) * W * plan->rows_per_wg * 2 * 4;
     char* ws = static_cast<char*>(a->workspace);
-    p->counters = reinterpret_cast<uint32_t*>(ws);
-    p->ws_stats = reinterpret_cast<float*>(ws + counters);
-    p->ws_o = reinterpret_cast<float*>(ws + counters + ((stats + 255) / 256) * 256);
+    p->ws_stats = reinterpret_cast<float*>(ws);
+    p->ws_o = reinterpret_cast<float*>(ws + ((stats + 255) / 256) * 256);
   }
   return FLEX_OK;
 }
@@ -108,7 +106,7 @@ int run_decode(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args*
   p.items = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_DEC];
   p.n_items = info.n_decode_items;
   p.grid_y = info.decode_wg_width;
-  const hipError_t e = launch_decode(p, plan->shape.head_dim_qk, s);
+  const hipError_t e = launch_decode(p, plan->shape.head_dim_qk, info.n_split_seqs > 0, s);
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "decode launch");
 }
 

@@ -16,6 +16,8 @@
 // order, so results are bit-identical run to run (no float atomics).
 #include <math.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -23,81 +25,150 @@ namespace flexattn {
 
 __device__ __forceinline__ PagedCache as_cache(const CacheRef& c) { return PagedCache{c.base, c.sp, c.ss, c.sh}; }
 
-// Combine the partials of splits first .. first+nspl-1 of one (sequence,
-// column) and write bf16 rows out_row0 .. out_row0+rows-1 (and their lse).
+// Split-K merge (flash-decoding combine), one work-group per (decode item,
+// column); only the first split of a split sequence does work. Runs as its own
+// launch after the decode kernel, so every partial is visible without
+// device-scope fences. Splits are combined in ascending order, so results are
+// bit-identical run to run:
+//   M = max_j m_j,  out = sum_j 2^{m_j - M} O_j / sum_j 2^{m_j - M} l_j,
+//   lse = (M + log2 sum_j 2^{m_j - M} l_j) * ln 2     (m_j in log2 units).
 template <int DV>
-__device__ void merge_splits(const AttnParams& p, int first, int nspl, int col, int W, int rows,
-                             int64_t out_row0, uint32_t* counter) {
-  for (int idx = threadIdx.x; idx < rows * (DV / 2); idx += blockDim.x) {
-    const int i = idx / (DV / 2);
-    const int d = 2 * (idx % (DV / 2));
+__global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
+  const int32_t* it = p.items + 8 * blockIdx.x;
+  if (it[1] != 0 || it[2] <= 1) return;
+  const int first = blockIdx.x, nspl = it[2];
+  const int col = blockIdx.y, W = gridDim.y, rows = p.rows_per_wg;
+  const int64_t out_row0 = int64_t(p.qsl[it[0]]) * p.Hq + int64_t(col) * rows;
+  for (int idx = threadIdx.x; idx < rows * (DV / 4); idx += blockDim.x) {
+    const int i = idx / (DV / 4);
+    const int d = 4 * (idx % (DV / 4));
     float M = -INFINITY;
     for (int j = 0; j < nspl; ++j) {
       const int64_t slot = int64_t(first + j) * W + col;
       M = fmaxf(M, p.ws_stats[(slot * rows + i) * 2]);
     }
-    float den = 0.f, o0 = 0.f, o1 = 0.f;
+    float den = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < nspl; ++j) {
       const int64_t slot = int64_t(first + j) * W + col;
-      const float f = exp2f(p.ws_stats[(slot * rows + i) * 2] - M);
+      const float mj = p.ws_stats[(slot * rows + i) * 2];
+      const float f = mj == -INFINITY ? 0.f : exp2f(mj - M);
       den += f * p.ws_stats[(slot * rows + i) * 2 + 1];
-      const float2 v = *reinterpret_cast<const float2*>(p.ws_o + (slot * rows + i) * DV + d);
-      o0 += f * v.x;
-      o1 += f * v.y;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(p.ws_o + (slot * rows + i) * DV + d);
+      acc += f * v;
     }
     const float inv = 1.f / den;
-    *reinterpret_cast<uint32_t*>(p.out + (out_row0 + i) * DV + d) = pack_bf16x2(o0 * inv, o1 * inv);
+    u32x2 pk;
+    pk[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+    pk[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+    *reinterpret_cast<u32x2*>(p.out + (out_row0 + i) * DV + d) = pk;
     if (d == 0 && p.lse) p.lse[out_row0 + i] = (M + log2f(den)) * kLn2;
   }
-  if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Publish this work-group's partial and report whether it arrived last.
-__device__ __forceinline__ bool arrive_last(uint32_t* counter, int nspl) {
-  __shared__ int s_last;
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = prev == uint32_t(nspl - 1);
+// Block-table entries of one work-group's key range are staged in LDS in
+// windows of kPageWin pages, so K/V gathers never wait on a dependent
+// block-table load (vector loads retire in order, which would otherwise turn
+// every gather into two serial memory round trips).
+constexpr int kPageWin = 512;
+
+// The running max of a row moves only when a chunk raises it by more than
+// this many log2 units; in between, probabilities are taken against the
+// stale max (so they stay below 2^8) and the accumulators are left alone.
+constexpr float kRescaleThreshold = 8.0f;
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
+
+// Online-softmax step of one 16-row block over one 32-key chunk.
+// s[b][r]: score of key kc0 + 16b + 4gq + r for this lane's row; keys at or
+// past `limit` are masked. Updates the row's max m (log2 units), the lane's
+// partial sum l and the accumulators o (rows 4gq + r), and returns the
+// chunk's probabilities as the bf16 A operand of the PV product.
+template <int NACC>
+__device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int limit, int gq, float scale_log2,
+                                               float& m, float& l, f32x4 (&o)[NACC]) {
+  float z[8];
+  float cmax = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int key = kc0 + chunk_key(e, gq);
+    z[e] = key < limit ? s[e >> 2][e & 3] * scale_log2 : -INFINITY;
+    cmax = fmaxf(cmax, z[e]);
   }
-  __syncthreads();
-  if (!s_last) return false;
-  __threadfence();
-  return true;
+  cmax = group_max(cmax);
+  const bool need = cmax > m + kRescaleThreshold;
+  if (wave_any(need)) {
+    const float m_new = need ? cmax : m;
+    const float alpha = fast_exp2(m - m_new);   // 1 if unchanged, 0 from -inf
+    l *= alpha;
+    m = m_new;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float ar = shfl_f(alpha, 4 * gq + r);
+#pragma unroll
+      for (int a = 0; a < NACC; ++a) o[a][r] *= ar;
+    }
+  }
+  const float m_use = m == -INFINITY ? 0.f : m;
+  u32x4 pop;
+  float psum = 0.f;
+#pragma unroll
+  for (int e2 = 0; e2 < 4; ++e2) {
+    const float p0 = fast_exp2(z[2 * e2] - m_use);
+    const float p1 = fast_exp2(z[2 * e2 + 1] - m_use);
+    psum += p0 + p1;
+    pop[e2] = pack_bf16x2(p0, p1);
+  }
+  l += psum;
+  return pop;
 }
 
 // ---------------------------------------------------------------------------
 // Decode, grouped-query heads.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void decode_gqa_kernel(AttnParams p) {
+template <int D>
+struct DecodeChunk {
+  static constexpr int DC = D / 32;
+  using VRow = typename std::conditional<D == 128, u32x4, u32x2>::type;
+  u32x4 k[2][DC];   // A operand rows: key 16b + n, dims 32c + 8gq .. +8
+  VRow v[8];        // value dims DPL*n .. of the lane's 8 keys
+};
+
+template <int D, int NW, int P>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void decode_gqa_kernel(AttnParams p) {
   static_assert(D == 64 || D == 128, "head dim");
   constexpr int DC = D / 32;   // 32-dim chunks of the QK^T contraction
   constexpr int DPL = D / 16;  // value dims each lane owns in PV
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
+  using Chunk = DecodeChunk<D>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
   const int item = blockIdx.x;
   const int g = blockIdx.y;
   const int W = gridDim.y;
   const int32_t* it = p.items + 8 * item;
-  const int seq = it[0], nspl = it[2], k0 = it[3], first = it[5], dseq = it[6];
+  const int seq = it[0], nspl = it[2], k0 = it[3];
   const int L = p.seq_lens[seq];
   const int kend = min(it[4], L);
   const int tok = p.qsl[seq];
   const int32_t* bt_row = p.bt + int64_t(seq) * p.bt_stride;
-  const int P = p.P;
   const int G = p.G;
-  const PagedCache kc = as_cache(p.kc), vc = as_cache(p.vc);
+  const uint16_t* kbase = p.kc.base + int64_t(g) * p.kc.sh + 8 * gq;
+  const uint16_t* vbase = p.vc.base + int64_t(g) * p.vc.sh + DPL * n;
+  const int64_t ksp = p.kc.sp, kss = p.kc.ss, vsp = p.vc.sp, vss = p.vc.ss;
+  __shared__ int s_pt[kPageWin];
 
   // Q as the B operand of S^T = K Q^T: column n = query head g*G + n.
   u32x4 qop[DC];
   {
     const bool ok = n < G;
-    const uint16_t* qr = p.q + (int64_t(tok) * p.Hq + g * G + (ok ? n : 0)) * D;
+    const uint16_t* qr = p.q + (int64_t(tok) * p.Hq + g * G + (ok ? n : 0)) * D + 8 * gq;
 #pragma unroll
-    for (int c = 0; c < DC; ++c) qop[c] = ok ? load16(qr + 32 * c + 8 * gq) : zero4();
+    for (int c = 0; c < DC; ++c) qop[c] = ok ? load16(qr + 32 * c) : zero4();
   }
 
   float m = -INFINITY, l = 0.f;
@@ -105,81 +176,61 @@ __global__ __launch_bounds__(NW * 64) void decode_gqa_kernel(AttnParams p) {
 #pragma unroll
   for (int a = 0; a < DPL; ++a) o[a] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nchunks = (kend - k0 + 31) >> 5;
-  for (int ci = w; ci < nchunks; ci += NW) {
-    const int kc0 = k0 + 32 * ci;
-    const int page0 = page_of(bt_row, kc0, P);
-    const int page1 = (kc0 + 16 < kend) ? page_of(bt_row, kc0 + 16, P) : page0;
+  for (int wk0 = k0; wk0 < kend; wk0 += kPageWin * P) {
+    const int wk1 = min(kend, wk0 + kPageWin * P);
+    const int pg0 = wk0 / P;
+    const int npg = (wk1 - 1) / P - pg0 + 1;
+    __syncthreads();
+    for (int i = tid; i < npg; i += NW * 64) s_pt[i] = bt_row[pg0 + i];
+    __syncthreads();
+    const int nch = (wk1 - wk0 + 31) >> 5;
 
-    // K rows as the A operand: row n of block b is key kc0 + 16b + n.
-    u32x4 kop[2][DC];
+    auto load = [&](Chunk& c, int ci) {
+      const int kc0 = wk0 + 32 * ci;
+      const bool any = ci < nch;
+      int page0 = 0, page1 = 0;
+      if (any) {
+        page0 = s_pt[kc0 / P - pg0];
+        page1 = (kc0 + 16 < wk1) ? s_pt[(kc0 + 16) / P - pg0] : page0;
+      }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int key = kc0 + 16 * b + n;
-      const bool ok = key < kend;
-      const uint16_t* kr = kc.row(b ? page1 : page0, key % P, g);
+      for (int b = 0; b < 2; ++b) {
+        const int key = kc0 + 16 * b + n;
+        const bool ok = any && key < wk1;
+        const uint16_t* kr = kbase + int64_t(b ? page1 : page0) * ksp + int64_t(key % P) * kss;
 #pragma unroll
-      for (int c = 0; c < DC; ++c) kop[b][c] = ok ? load16(kr + 32 * c + 8 * gq) : zero4();
-    }
-    // V rows of the lane's 8 keys, value dims DPL*n .. DPL*n + DPL - 1.
-    u32x4 vop[DPL];
-    if constexpr (D == 128) {
-      u32x4 rows[8];
+        for (int cc = 0; cc < DC; ++cc) c.k[b][cc] = ok ? load16(kr + 32 * cc) : zero4();
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int key = kc0 + chunk_key(e, gq);
-        rows[e] = key < kend ? load16(vc.row((e >> 2) ? page1 : page0, key % P, g) + DPL * n) : zero4();
+        const bool ok = any && key < wk1;
+        const uint16_t* vr = vbase + int64_t((e >> 2) ? page1 : page0) * vsp + int64_t(key % P) * vss;
+        if constexpr (D == 128) c.v[e] = ok ? load16(vr) : zero4();
+        else c.v[e] = ok ? load8(vr) : u32x2{0u, 0u};
       }
-      transpose8x8(rows, vop);
-    } else {
-      u32x2 rows[8];
+    };
+
+    Chunk cur, nxt;
+    load(cur, w);
+    for (int ci = w; ci < nch; ci += NW) {
+      load(nxt, ci + NW);   // next chunk's gathers stay in flight during this chunk's math
+      const int kc0 = wk0 + 32 * ci;
+      f32x4 s[2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int key = kc0 + chunk_key(e, gq);
-        rows[e] = key < kend ? load8(vc.row((e >> 2) ? page1 : page0, key % P, g) + DPL * n) : u32x2{0u, 0u};
+      for (int b = 0; b < 2; ++b) {
+        s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int cc = 0; cc < DC; ++cc) s[b] = mfma_16x16x32(cur.k[b][cc], qop[cc], s[b]);
       }
-      transpose8x4(rows, vop);
+      const u32x4 pop = softmax_chunk<DPL>(s, kc0, wk1, gq, p.scale_log2, m, l, o);
+      u32x4 vop[DPL];
+      if constexpr (D == 128) transpose8x8(cur.v, vop);
+      else transpose8x4(cur.v, vop);
+#pragma unroll
+      for (int a = 0; a < DPL; ++a) o[a] = mfma_16x16x32(pop, vop[a], o[a]);
+      cur = nxt;
     }
-
-    f32x4 s[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < DC; ++c) s[b] = mfma_16x16x32(kop[b][c], qop[c], s[b]);
-    }
-
-    // Online softmax for query row n over the chunk's keys (base 2).
-    float z[8];
-    float cmax = -INFINITY;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int key = kc0 + chunk_key(e, gq);
-      z[e] = key < kend ? s[e >> 2][e & 3] * p.scale_log2 : -INFINITY;
-      cmax = fmaxf(cmax, z[e]);
-    }
-    cmax = group_max(cmax);
-    const float m_new = fmaxf(m, cmax);
-    const float alpha = exp2f(m - m_new);
-    u32x4 pop;
-    float psum = 0.f;
-#pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) {
-      const float p0 = exp2f(z[2 * e2] - m_new);
-      const float p1 = exp2f(z[2 * e2 + 1] - m_new);
-      psum += p0 + p1;
-      pop[e2] = pack_bf16x2(p0, p1);
-    }
-    l = l * alpha + psum;
-    m = m_new;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float ar = shfl_f(alpha, 4 * gq + r);
-#pragma unroll
-      for (int a = 0; a < DPL; ++a) o[a][r] *= ar;
-    }
-#pragma unroll
-    for (int a = 0; a < DPL; ++a) o[a] = mfma_16x16x32(pop, vop[a], o[a]);
   }
 
   // Combine the waves' partial states through LDS.
@@ -200,7 +251,7 @@ __global__ __launch_bounds__(NW * 64) void decode_gqa_kernel(AttnParams p) {
   const bool single = nspl == 1;
   const int64_t out_row0 = int64_t(tok) * p.Hq + int64_t(g) * G;
   const int64_t slot = int64_t(item) * W + g;
-  for (int idx = threadIdx.x; idx < G * (D / 2); idx += NW * 64) {
+  for (int idx = tid; idx < G * (D / 2); idx += NW * 64) {
     const int i = idx / (D / 2), d = 2 * (idx % (D / 2));
     float M = s_m[0][i];
 #pragma unroll
@@ -208,7 +259,7 @@ __global__ __launch_bounds__(NW * 64) void decode_gqa_kernel(AttnParams p) {
     float den = 0.f, o0 = 0.f, o1 = 0.f;
 #pragma unroll
     for (int ww = 0; ww < NW; ++ww) {
-      const float f = exp2f(s_m[ww][i] - M);
+      const float f = s_m[ww][i] == -INFINITY ? 0.f : fast_exp2(s_m[ww][i] - M);
       den += f * s_l[ww][i];
       o0 += f * s_o[ww][i][d];
       o1 += f * s_o[ww][i][d + 1];
@@ -225,16 +276,24 @@ __global__ __launch_bounds__(NW * 64) void decode_gqa_kernel(AttnParams p) {
       }
     }
   }
-  if (single) return;
-  uint32_t* counter = p.counters + int64_t(dseq) * W + g;
-  if (!arrive_last(counter, nspl)) return;
-  merge_splits<D>(p, first, nspl, g, W, p.rows_per_wg, out_row0, counter);
 }
 
 // ---------------------------------------------------------------------------
-// Row-parallel attention: prefill (GQA and latent) and latent decode.
+// Row-parallel attention: prefill (grouped-query and latent) and latent decode.
+//
+// Each wave owns RB blocks of 16 query rows; the work-group stages key tiles
+// of BN keys, gathered through the block table, in double-buffered LDS that
+// every wave reads. Tile loads are issued two tiles ahead into registers.
+// Row layouts:
+//   kPrefillGrouped  work-group = (tile of RB*16 tokens, KV head, head chunk);
+//                    wave w = query head, rb = token block. One K/V tile
+//                    feeds every query head of the KV head.
+//   kPrefillPerHead  work-group = (tile of NW*RB*16 tokens, query head).
+//   kDecodeLatent    work-group = (decode item, group of NW*RB*16 heads).
 // ---------------------------------------------------------------------------
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, bool DECODE>
+enum RowMode { kPrefillGrouped = 0, kPrefillPerHead = 1, kDecodeLatent = 2 };
+
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS>
 struct RowParCfg {
   static constexpr int DC = DQK / 32;
   static constexpr int LDS_ROW = DQK + 8;                 // 16-byte pad per row
@@ -242,28 +301,29 @@ struct RowParCfg {
   static constexpr int CPR = DQK / 8;                     // 16-byte chunks per K row
   static constexpr int CPRV = VALIAS ? 0 : DV / 8;
   static constexpr int NT = NW * 64;
+  static constexpr int K_CHUNKS = BN * CPR;
   static constexpr int TILE_CHUNKS = BN * (CPR + CPRV);
-  static constexpr int NLD = TILE_CHUNKS / NT;
+  static constexpr int NLD = (TILE_CHUNKS + NT - 1) / NT;
   static constexpr int NACC = DV / 16;
   static constexpr int NVG = DV >= 128 ? DV / 128 : 1;   // value-dim groups of 8 per lane
   static constexpr int K_ELEMS = BN * LDS_ROW;
   static constexpr int V_ELEMS = VALIAS ? 0 : BN * LDS_ROW_V;
-  static constexpr size_t LDS_BYTES = size_t(2) * (K_ELEMS + V_ELEMS) * 2;
-  static_assert(TILE_CHUNKS % NT == 0, "tile chunks must divide evenly");
-  static_assert((BN * CPR) % NT == 0, "K chunks must divide evenly");
+  static constexpr size_t LDS_BYTES = size_t(2) * (K_ELEMS + V_ELEMS) * 2 + kPageWin * 4;
   static_assert(BN % 32 == 0, "key tile is a multiple of 32");
 };
 
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, bool DECODE>
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P>
 __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
-  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, DECODE>;
+  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS>;
+  static_assert(kPageWin * P >= 2 * BN + P, "page window must cover two key tiles");
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   uint16_t* ldsK = lds;
   uint16_t* ldsV = VALIAS ? lds : lds + 2 * C::K_ELEMS;
+  int* s_pt = reinterpret_cast<int*>(lds + 2 * (C::K_ELEMS + C::V_ELEMS));
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
   const int32_t* it = p.items + 8 * blockIdx.x;
   const int seq = it[0];
@@ -271,12 +331,11 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
   const int q0 = p.qsl[seq];
   const int nq = p.qsl[seq + 1] - q0;
   const int32_t* bt_row = p.bt + int64_t(seq) * p.bt_stride;
-  const int P = p.P;
-  const PagedCache kc = as_cache(p.kc), vc = as_cache(p.vc);
 
   int key_begin, key_end, head_kv, wave_limit;
+  bool wave_on = true;
   int row_tok[RB], row_head[RB], row_limit[RB];
-  if constexpr (DECODE) {
+  if constexpr (MODE == kDecodeLatent) {
     key_begin = it[3];
     key_end = min(it[4], L);
     const int hg = blockIdx.y;
@@ -288,7 +347,7 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       row_limit[rb] = key_end;
     }
     wave_limit = key_end;
-  } else {
+  } else if constexpr (MODE == kPrefillPerHead) {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
     key_end = it[4];
@@ -303,16 +362,38 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       row_limit[rb] = ok ? (L - nq + local + 1) : 1;
     }
     const int last = min(r1, r0 + (w + 1) * RB * 16) - 1;
-    wave_limit = (r0 + w * RB * 16 < r1) ? (L - nq + last + 1) : 0;
+    wave_on = r0 + w * RB * 16 < r1;
+    wave_limit = wave_on ? (L - nq + last + 1) : 0;
+  } else {
+    const int r0 = it[2], r1 = it[3];
+    key_begin = 0;
+    key_end = it[4];
+    const int chunks = (p.G + NW - 1) / NW;
+    head_kv = blockIdx.y / chunks;
+    const int hl = (blockIdx.y % chunks) * NW + w;     // query head within the group
+    wave_on = hl < p.G;
+    const int h = head_kv * p.G + (wave_on ? hl : 0);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int local = r0 + rb * 16 + n;
+      const bool ok = local < r1;
+      row_tok[rb] = q0 + (ok ? local : r0);
+      row_head[rb] = h;
+      row_limit[rb] = ok ? (L - nq + local + 1) : 1;
+    }
+    wave_limit = wave_on ? (L - nq + r1) : 0;
   }
+  const uint16_t* kbase = p.kc.base + int64_t(head_kv) * p.kc.sh;
+  const uint16_t* vbase = p.vc.base + int64_t(head_kv) * p.vc.sh;
+  const int64_t ksp = p.kc.sp, kss = p.kc.ss, vsp = p.vc.sp, vss = p.vc.ss;
 
   // Q as the B operand of S^T = K Q^T.
   u32x4 qop[RB][C::DC];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const uint16_t* qr = p.q + (int64_t(row_tok[rb]) * p.Hq + row_head[rb]) * DQK;
+    const uint16_t* qr = p.q + (int64_t(row_tok[rb]) * p.Hq + row_head[rb]) * DQK + 8 * gq;
 #pragma unroll
-    for (int c = 0; c < C::DC; ++c) qop[rb][c] = load16(qr + 32 * c + 8 * gq);
+    for (int c = 0; c < C::DC; ++c) qop[rb][c] = load16(qr + 32 * c);
   }
 
   float m[RB], l[RB];
@@ -326,53 +407,54 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
   }
 
   const int ntiles = (key_end - key_begin + BN - 1) / BN;
-  u32x4 stage[C::NLD];
-
-  // Gather one key tile (keys kb .. kb+BN-1) through the block table into registers.
-  auto load_tile = [&](int kb) {
-#pragma unroll
-    for (int i = 0; i < C::NLD; ++i) {
-      const int u = i * C::NT + tid;
-      if (u < BN * C::CPR) {
-        const int r = u / C::CPR, x = u % C::CPR;
-        const int key = kb + r;
-        stage[i] = key < key_end ? load16(kc.row(page_of(bt_row, key, P), key % P, head_kv) + 8 * x) : zero4();
-      } else {
-        const int u2 = u - BN * C::CPR;
-        const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
-        const int key = kb + r;
-        stage[i] = key < key_end ? load16(vc.row(page_of(bt_row, key, P), key % P, head_kv) + 8 * x) : zero4();
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < C::NLD; ++i) {
-      const int u = i * C::NT + tid;
-      if (u < BN * C::CPR) {
-        const int r = u / C::CPR, x = u % C::CPR;
-        *reinterpret_cast<u32x4*>(ldsK + buf * C::K_ELEMS + r * C::LDS_ROW + 8 * x) = stage[i];
-      } else {
-        const int u2 = u - BN * C::CPR;
-        const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
-        *reinterpret_cast<u32x4*>(ldsV + buf * C::V_ELEMS + r * C::LDS_ROW_V + 8 * x) = stage[i];
-      }
+  const int last_page = key_end > 0 ? (key_end - 1) / P : 0;
+  int pt_base = key_begin / P;
+  auto load_window = [&](int base) {
+    for (int i = tid; i < kPageWin; i += C::NT) {
+      const int pg = base + i;
+      s_pt[i] = pg <= last_page ? bt_row[pg] : 0;
     }
   };
 
-  if (ntiles > 0) {
-    load_tile(key_begin);
-    store_tile(0);
-  }
-  __syncthreads();
+  // Gather key tile kb .. kb+BN-1 through the staged block table into registers.
+  auto load_tile = [&](u32x4 (&st)[C::NLD], int kb) {
+#pragma unroll
+    for (int i = 0; i < C::NLD; ++i) {
+      const int u = i * C::NT + tid;
+      if (u < C::K_CHUNKS) {
+        const int r = u / C::CPR, x = u % C::CPR;
+        const int key = kb + r;
+        st[i] = key < key_end
+                    ? load16(kbase + int64_t(s_pt[key / P - pt_base]) * ksp + int64_t(key % P) * kss + 8 * x)
+                    : zero4();
+      } else if (C::CPRV > 0 && u < C::TILE_CHUNKS) {
+        const int u2 = u - C::K_CHUNKS;
+        const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
+        const int key = kb + r;
+        st[i] = key < key_end
+                    ? load16(vbase + int64_t(s_pt[key / P - pt_base]) * vsp + int64_t(key % P) * vss + 8 * x)
+                    : zero4();
+      }
+    }
+  };
+  auto store_tile = [&](const u32x4 (&st)[C::NLD], int buf) {
+#pragma unroll
+    for (int i = 0; i < C::NLD; ++i) {
+      const int u = i * C::NT + tid;
+      if (u < C::K_CHUNKS) {
+        const int r = u / C::CPR, x = u % C::CPR;
+        *reinterpret_cast<u32x4*>(ldsK + buf * C::K_ELEMS + r * C::LDS_ROW + 8 * x) = st[i];
+      } else if (C::CPRV > 0 && u < C::TILE_CHUNKS) {
+        const int u2 = u - C::K_CHUNKS;
+        const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
+        *reinterpret_cast<u32x4*>(ldsV + buf * C::V_ELEMS + r * C::LDS_ROW_V + 8 * x) = st[i];
+      }
+    }
+  };
 
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int kb = key_begin + kt * BN;
-    const int buf = kt & 1;
-    if (kt + 1 < ntiles) load_tile(kb + BN);
+  auto compute_tile = [&](int kb, int buf) {
     const uint16_t* Kt = ldsK + buf * C::K_ELEMS;
     const uint16_t* Vt = VALIAS ? Kt : ldsV + buf * C::V_ELEMS;
-
 #pragma unroll
     for (int ch = 0; ch < BN / 32; ++ch) {
       const int kc0 = kb + 32 * ch;
@@ -392,37 +474,9 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       }
       u32x4 pop[RB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        float z[8];
-        float cmax = -INFINITY;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int key = kc0 + chunk_key(e, gq);
-          z[e] = key < row_limit[rb] ? s[rb][e >> 2][e & 3] * p.scale_log2 : -INFINITY;
-          cmax = fmaxf(cmax, z[e]);
-        }
-        cmax = group_max(cmax);
-        const float m_new = fmaxf(m[rb], cmax);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m[rb] - m_use);
-        float psum = 0.f;
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          const float p0 = exp2f(z[2 * e2] - m_use);
-          const float p1 = exp2f(z[2 * e2 + 1] - m_use);
-          psum += p0 + p1;
-          pop[rb][e2] = pack_bf16x2(p0, p1);
-        }
-        l[rb] = l[rb] * alpha + psum;
-        m[rb] = m_new;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float ar = shfl_f(alpha, 4 * gq + r);
-#pragma unroll
-          for (int a = 0; a < C::NACC; ++a) o[rb][a][r] *= ar;
-        }
-      }
-      // PV: lane reads its 8 keys' value dims and transposes them in registers.
+      for (int rb = 0; rb < RB; ++rb)
+        pop[rb] = softmax_chunk<C::NACC>(s[rb], kc0, row_limit[rb], gq, p.scale_log2, m[rb], l[rb], o[rb]);
+      // PV: the lane reads its 8 keys' value dims and transposes them in registers.
 #pragma unroll
       for (int vg = 0; vg < C::NVG; ++vg) {
         if constexpr (DV >= 128) {
@@ -449,9 +503,36 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
         }
       }
     }
+  };
 
-    if (kt + 1 < ntiles) store_tile(buf ^ 1);
+  // One pipeline step: gather tile kt+2 into `ahead`, compute tile kt from LDS,
+  // then move tile kt+1 (gathered one step earlier into `ready`) into LDS.
+  auto step = [&](int kt, u32x4 (&ahead)[C::NLD], u32x4 (&ready)[C::NLD]) {
+    if (kt + 2 < ntiles) {
+      const int nb = key_begin + (kt + 2) * BN;
+      const int need_last = (min(nb + BN, key_end) - 1) / P;
+      if (need_last >= pt_base + kPageWin) {   // slide the block-table window (uniform)
+        pt_base = nb / P;
+        load_window(pt_base);
+        __syncthreads();
+      }
+      load_tile(ahead, nb);
+    }
+    compute_tile(key_begin + kt * BN, kt & 1);
+    if (kt + 1 < ntiles) store_tile(ready, (kt + 1) & 1);
     __syncthreads();
+  };
+
+  u32x4 stA[C::NLD], stB[C::NLD];
+  load_window(pt_base);
+  __syncthreads();
+  if (ntiles > 0) load_tile(stA, key_begin);
+  if (ntiles > 1) load_tile(stB, key_begin + BN);
+  if (ntiles > 0) store_tile(stA, 0);
+  __syncthreads();
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    step(kt, stA, stB);
+    if (kt + 1 < ntiles) step(kt + 1, stB, stA);
   }
 
   // Epilogue. Lane (n, gq) holds output rows 4*gq + r of each row block, at
@@ -474,27 +555,28 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
     }
   };
 
-  if constexpr (!DECODE) {
+  if constexpr (MODE != kDecodeLatent) {
+    if (!wave_on) return;
     const int r0 = it[2], r1 = it[3];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const float lt = group_sum(l[rb]);
+      const int blk = MODE == kPrefillPerHead ? (w * RB + rb) : rb;   // token block of this row block
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int rowi = (w * RB + rb) * 16 + 4 * gq + r;
         const float lr = shfl_f(lt, 4 * gq + r);
-        const int local = r0 + rowi;
+        const int local = r0 + blk * 16 + 4 * gq + r;
         if (local < r1) {
           const int64_t orow = int64_t(q0 + local) * p.Hq + row_head[rb];
           row_values(rb, r, 1.f / lr, p.out + orow * DV);
         }
       }
-      const int local = r0 + (w * RB + rb) * 16 + n;
+      const int local = r0 + blk * 16 + n;
       if (gq == 0 && local < r1 && p.lse)
         p.lse[int64_t(q0 + local) * p.Hq + row_head[rb]] = (m[rb] + log2f(lt)) * kLn2;
     }
   } else {
-    const int nspl = it[2], first = it[5], dseq = it[6];
+    const int nspl = it[2];
     const int hg = blockIdx.y;
     const int W = gridDim.y;
     const int rows = p.rows_per_wg;
@@ -541,10 +623,6 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
         }
       }
     }
-    if (nspl == 1) return;
-    uint32_t* counter = p.counters + int64_t(dseq) * W + hg;
-    if (!arrive_last(counter, nspl)) return;
-    merge_splits<DV>(p, first, nspl, hg, W, rows, out_row0, counter);
   }
 }
 
@@ -576,10 +654,10 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t words) {
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, bool DECODE>
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P>
 static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stream) {
-  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, DECODE>;
-  auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, DECODE>;
+  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS>;
+  auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, MODE, P>;
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, int(C::LDS_BYTES));
   if (attr != hipSuccess) return attr;
@@ -587,31 +665,69 @@ static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stre
   return hipGetLastError();
 }
 
-hipError_t launch_decode(const AttnParams& p, int dqk, hipStream_t stream) {
+template <int D, int P>
+static hipError_t launch_decode_gqa(const AttnParams& p, dim3 grid, hipStream_t stream) {
+  hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P>), grid, dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, dim3 grid, hipStream_t stream) {
+  const bool p16 = p.P == 16;
+  if (p.P != 16 && p.P != 64) return hipErrorInvalidValue;
+  switch (dqk) {
+    case 128: return p16 ? launch_decode_gqa<128, 16>(p, grid, stream) : launch_decode_gqa<128, 64>(p, grid, stream);
+    case 64: return p16 ? launch_decode_gqa<64, 16>(p, grid, stream) : launch_decode_gqa<64, 64>(p, grid, stream);
+    case 576:
+      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16>(p, grid, stream)
+                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64>(p, grid, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStream_t stream) {
   if (p.n_items == 0) return hipSuccess;
   const dim3 grid(p.n_items, p.grid_y);
+  hipError_t e = launch_decode_kernel(p, dqk, grid, stream);
+  if (e != hipSuccess || !has_splits) return e;
   switch (dqk) {
-    case 128:
-      hipLaunchKernelGGL((decode_gqa_kernel<128, 4>), grid, dim3(256), 0, stream, p);
-      return hipGetLastError();
-    case 64:
-      hipLaunchKernelGGL((decode_gqa_kernel<64, 4>), grid, dim3(256), 0, stream, p);
-      return hipGetLastError();
-    case 576:
-      return launch_rowpar<576, 512, 4, 1, 32, true, true>(p, grid, stream);
-    default:
-      return hipErrorInvalidValue;
+    case 128: hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, p); break;
+    case 64: hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, p); break;
+    case 576: hipLaunchKernelGGL(merge_kernel<512>, grid, dim3(256), 0, stream, p); break;
+    default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+// Grouped-query prefill: one wave per query head of a KV head (4 waves when
+// the group has at most 4 heads, else 8), bm/16 token blocks per wave.
+template <int D, int P>
+static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid, hipStream_t stream) {
+  const bool narrow = p.G <= 4;
+  // 32-key tiles for the widest variant keep its two staged tiles within the
+  // 256 registers that two waves per SIMD allow.
+  constexpr int BN2 = D == 128 ? 32 : 64;
+  if (bm == 32)
+    return narrow ? launch_rowpar<D, D, 4, 2, 64, false, kPrefillGrouped, P>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 2, BN2, false, kPrefillGrouped, P>(p, grid, stream);
+  if (bm == 16)
+    return narrow ? launch_rowpar<D, D, 4, 1, 64, false, kPrefillGrouped, P>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 1, 64, false, kPrefillGrouped, P>(p, grid, stream);
+  return hipErrorInvalidValue;
+}
+
+template <int P>
+static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 grid, hipStream_t stream) {
+  if (dqk == 128) return launch_prefill_grouped<128, P>(p, bm, grid, stream);
+  if (dqk == 64) return launch_prefill_grouped<64, P>(p, bm, grid, stream);
+  if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P>(p, grid, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_prefill(const AttnParams& p, int dqk, int bm, hipStream_t stream) {
   if (p.n_items == 0) return hipSuccess;
   const dim3 grid(p.n_items, p.grid_y);
-  if (dqk == 128 && bm == 128) return launch_rowpar<128, 128, 4, 2, 64, false, false>(p, grid, stream);
-  if (dqk == 128 && bm == 64) return launch_rowpar<128, 128, 4, 1, 64, false, false>(p, grid, stream);
-  if (dqk == 64 && bm == 128) return launch_rowpar<64, 64, 4, 2, 64, false, false>(p, grid, stream);
-  if (dqk == 64 && bm == 64) return launch_rowpar<64, 64, 4, 1, 64, false, false>(p, grid, stream);
-  if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, false>(p, grid, stream);
+  if (p.P == 16) return launch_prefill_p<16>(p, dqk, bm, grid, stream);
+  if (p.P == 64) return launch_prefill_p<64>(p, dqk, bm, grid, stream);
   return hipErrorInvalidValue;
 }
 

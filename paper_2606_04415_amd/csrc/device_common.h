@@ -88,13 +88,27 @@ __device__ __forceinline__ float shfl_xor_f(float v, int mask) { return __shfl_x
 __device__ __forceinline__ float shfl_f(float v, int src) { return __shfl(v, src, 64); }
 
 // Max / sum over the four lane groups g = 0..3 that share lane index n.
-__device__ __forceinline__ float group_max(float v) {
-  v = fmaxf(v, shfl_xor_f(v, 16));
-  return fmaxf(v, shfl_xor_f(v, 32));
+// v_permlane16_swap(x, x) returns rows (0,0,2,2) and (1,1,3,3) of x, and
+// v_permlane32_swap(x, x) returns rows (0,1,0,1) and (2,3,2,3): combining
+// each pair exchanges values with lane n^16, then lane n^32, on the VALU.
+__device__ __forceinline__ float swap16_combine_max(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto t = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
 }
+__device__ __forceinline__ float swap32_combine_max(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto t = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+}
+__device__ __forceinline__ float group_max(float v) { return swap32_combine_max(swap16_combine_max(v)); }
 __device__ __forceinline__ float group_sum(float v) {
-  v += shfl_xor_f(v, 16);
-  return v + shfl_xor_f(v, 32);
+  uint32_t u = __float_as_uint(v);
+  auto t = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+  u = __float_as_uint(v);
+  t = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
 }
 
 // Slot e (0..7) of a lane in group g within a 32-key chunk holds key

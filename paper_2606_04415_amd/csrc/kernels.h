@@ -22,7 +22,6 @@ struct AttnParams {
   float* lse;
   const int32_t* items;   // device pointer to the first item of this phase
   int32_t n_items;
-  uint32_t* counters;     // decode: one per (decode sequence, work-group column)
   float* ws_stats;        // decode: [item][W][rows][2] (max in log2 units, sum)
   float* ws_o;            // decode: [item][W][rows][d_v] unnormalised partial outputs
   int32_t Hq, Hkv, G;     // G = query heads per KV head
@@ -32,7 +31,7 @@ struct AttnParams {
   float scale_log2;       // sm_scale * log2(e)
 };
 
-hipError_t launch_decode(const AttnParams& p, int head_dim_qk, hipStream_t stream);
+hipError_t launch_decode(const AttnParams& p, int head_dim_qk, bool has_splits, hipStream_t stream);
 hipError_t launch_prefill(const AttnParams& p, int head_dim_qk, int bm, hipStream_t stream);
 hipError_t launch_gather(const CacheRef& kc, const CacheRef& vc, bool has_v, const int32_t* bt_row,
                          int32_t L, int32_t P, int32_t Hkv, int32_t dqk, int32_t dv,

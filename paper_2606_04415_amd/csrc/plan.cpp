@@ -93,13 +93,13 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
   const int64_t granule = o.split_granule ? o.split_granule : 64;
-  const int32_t bm = o.bm ? o.bm : (latent ? 64 : 128);
+  const int32_t bm = o.bm ? o.bm : (latent ? 64 : 32);
   if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
   if (o.cus_decode < -1 || o.cus_decode > cus_total)
     return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
-  if ((bm != 64 && bm != 128) || (latent && bm != 64))
-    return set_error(FLEX_ERR_UNSUPPORTED, "bm must be 64 or 128 (64 for the latent layout)");
+  if (latent ? bm != 64 : (bm != 16 && bm != 32))
+    return set_error(FLEX_ERR_UNSUPPORTED, "bm must be 16 or 32 (grouped-query) or 64 (latent layout)");
   if (max_pages_per_seq < 0) return set_error(FLEX_ERR_INVALID_ARG, "max_pages_per_seq < 0");
   if (num_seqs > 0 && qsl[0] != 0) return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc[0] != 0");
 
@@ -115,6 +115,10 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   }
 
   const int32_t W = latent ? sh.num_q_heads / kLatentRowsPerWG : sh.num_kv_heads;
+  // Prefill work-groups per tile: one per query head (latent layout), or one per
+  // KV head and group of up to 8 of its query heads (grouped-query layout).
+  const int32_t G = sh.num_q_heads / sh.num_kv_heads;
+  const int32_t pre_grid_y = latent ? sh.num_q_heads : sh.num_kv_heads * ((G + 7) / 8);
   const int32_t rows_per_wg = latent ? kLatentRowsPerWG : sh.num_q_heads / sh.num_kv_heads;
   std::vector<int32_t> dec, pre;
   for (int32_t s = 0; s < num_seqs; ++s) {
@@ -165,7 +169,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   for (int32_t s : dec) total_pages += cdiv(seq_lens[s], P);
   const int64_t pps = dec.empty() ? 0 : std::max(min_pps, cdiv(int64_t(W) * total_pages, cus_decode * wg_per_cu));
   std::vector<int32_t> dec_words;
-  int32_t n_dec_items = 0;
+  int32_t n_dec_items = 0, n_split_seqs = 0;
   for (size_t d = 0; d < dec.size(); ++d) {
     const int32_t s = dec[d];
     const int64_t Ps = cdiv(seq_lens[s], P);
@@ -175,6 +179,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
       nspl = cdiv(Ps, pps_s);
     }
     const int32_t first = n_dec_items;
+    if (nspl > 1) ++n_split_seqs;
     for (int64_t j = 0; j < nspl; ++j) {
       const int64_t k0 = j * pps_s * P;
       const int64_t k1 = std::min<int64_t>(seq_lens[s], (j + 1) * pps_s * P);
@@ -217,7 +222,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   w[H_N_DEC_SEQS] = int32_t(dec.size());
   w[H_N_PRE_SEQS] = int32_t(pre.size());
   w[H_DEC_WIDTH] = W;
-  w[H_PRE_GRID_Y] = sh.num_q_heads;
+  w[H_PRE_GRID_Y] = pre_grid_y;
   w[H_OFF_DEC] = kHeaderWords;
   w[H_OFF_PRE] = kHeaderWords + kItemWords * n_dec_items;
   w[H_PPS] = int32_t(pps);
@@ -231,12 +236,12 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     w.insert(w.end(), item, item + kItemWords);
   }
 
+  // Workspace: per (decode item, column) the rows' (max, sum) pairs, then the
+  // unnormalised partial outputs; needed only when some sequence is split.
   size_t ws = 0;
-  if (n_dec_items > 0) {
-    const size_t counters = size_t(cdiv(int64_t(dec.size()) * W * 4, 256) * 256);
+  if (n_split_seqs > 0) {
     const size_t stats = size_t(n_dec_items) * W * rows_per_wg * 2 * 4;
-    ws = counters + size_t(cdiv(int64_t(stats), 256) * 256) +
-         size_t(n_dec_items) * W * rows_per_wg * sh.head_dim_v * 4;
+    ws = size_t(cdiv(int64_t(stats), 256) * 256) + size_t(n_dec_items) * W * rows_per_wg * sh.head_dim_v * 4;
   }
   flex_attn_plan_info& info = plan->info;
   std::memset(&info, 0, sizeof(info));
@@ -245,8 +250,9 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   info.n_prefill_seqs = int32_t(pre.size());
   info.n_decode_items = n_dec_items;
   info.n_prefill_items = n_pre_items;
+  info.n_split_seqs = n_split_seqs;
   info.decode_wg_width = W;
-  info.prefill_grid_y = sh.num_q_heads;
+  info.prefill_grid_y = pre_grid_y;
   info.pages_per_split = int32_t(pps);
   info.cus_decode = int32_t(cus_decode);
   info.cus_prefill = int32_t(cus_prefill);

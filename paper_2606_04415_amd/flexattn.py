@@ -53,7 +53,8 @@ class PlanOpts(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("num_seqs", ctypes.c_int32), ("n_decode_seqs", ctypes.c_int32),
                 ("n_prefill_seqs", ctypes.c_int32), ("n_decode_items", ctypes.c_int32),
-                ("n_prefill_items", ctypes.c_int32), ("decode_wg_width", ctypes.c_int32),
+                ("n_prefill_items", ctypes.c_int32), ("n_split_seqs", ctypes.c_int32),
+                ("decode_wg_width", ctypes.c_int32),
                 ("prefill_grid_y", ctypes.c_int32), ("pages_per_split", ctypes.c_int32),
                 ("cus_decode", ctypes.c_int32), ("cus_prefill", ctypes.c_int32), ("bm", ctypes.c_int32),
                 ("plan_words", ctypes.c_int32), ("device_plan_bytes", ctypes.c_size_t),
@@ -337,7 +338,7 @@ class PagedAttention:
         self.plan = flex_attn_plan(shape, opts, h_query_start_loc, h_seq_lens, max_pages_per_seq)
         info = self.plan.info
         self.d_plan = torch.empty(max(256, info["device_plan_bytes"]), dtype=torch.uint8, device=device)
-        self.workspace = torch.zeros(max(256, info["workspace_bytes"]), dtype=torch.uint8, device=device)
+        self.workspace = torch.empty(max(256, info["workspace_bytes"]), dtype=torch.uint8, device=device)
         flex_attn_plan_upload(self.plan, self.d_plan)
 
     def args(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, lse=None) -> Args:

@@ -56,7 +56,7 @@ def compare(sh, opts, qsl, ls, maxp):
     assert st == ref.status
     if st == OP.OK:
         assert words == ref.blob
-        for k in ("n_decode_items", "n_prefill_items", "pages_per_split", "cus_decode", "cus_prefill",
+        for k in ("n_decode_items", "n_prefill_items", "n_split_seqs", "pages_per_split", "cus_decode", "cus_prefill",
                   "workspace_bytes", "device_plan_bytes", "plan_words", "decode_wg_width"):
             assert info[k] == ref.info[k], k
         assert info["decode_bytes"] == ref.info["decode_bytes"]
@@ -98,7 +98,7 @@ def test_plan_matches_rederivation_fuzz():
         maxp = max([1] + [-(-L // P) for L in ls]) + rng.randint(0, 3)
         opts = OP.Opts(cus_decode=rng.choice([0, 64, 192, -1]), max_splits=rng.choice([0, 1, 3]),
                        wg_per_cu=rng.choice([0, 2]), min_split_tokens=rng.choice([0, 16, 1000]),
-                       bm=rng.choice([0, 64]) if sh.head_dim_qk != 576 else 0,
+                       bm=rng.choice([0, 16]) if sh.head_dim_qk != 576 else 0,
                        cus_total=rng.choice([0, 256, 240]),
                        hbm_gbps=rng.choice([0.0, 5000.0]), decode_gbps_per_cu=rng.choice([0.0, 25.0]))
         compare(sh, opts, qsl, ls, maxp)
@@ -137,7 +137,8 @@ def test_opts_status_matches(opts):
 
 def test_run_calls_reject_bad_args_without_gpu():
     sh = F.make_shape(28, 4, 128, 128, 16, 0.088)
-    plan = F.flex_attn_plan(sh, None, [0, 1, 3], [40, 50], 4)
+    plan = F.flex_attn_plan(sh, F.make_opts(min_split_tokens=16), [0, 1, 3], [40, 50], 4)
+    assert plan.info["n_split_seqs"] == 1 and plan.info["workspace_bytes"] > 0
     a = F.Args()   # all NULL
     for fn in (F.lib().flex_attn_decode, F.lib().flex_attn_prefill):
         st = fn(plan.handle, ctypes.byref(a), None)

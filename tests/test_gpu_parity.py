@@ -69,11 +69,11 @@ def test_ragged_gqa_d64_page64_group16():
     full_check(b, F.make_opts(min_split_tokens=64), "ragged-d64")
 
 
-def test_gqa_bm64_tiles():
+def test_gqa_bm16_tiles():
     ns, ls = [77, 1, 150], [77, 500, 300]
     b = custom_batch(QW, ns, ls, seed=5)
-    log("GQA prefill with 64-row tiles")
-    full_check(b, F.make_opts(bm=64), "bm64")
+    log("GQA prefill with 16-row tiles")
+    full_check(b, F.make_opts(bm=16), "bm16")
 
 
 @pytest.mark.parametrize("hq", [64, 128])
