@@ -82,22 +82,23 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
 
 // Online-softmax step of one 16-row block over one 32-key chunk.
-// s[b][r]: score of key kc0 + 16b + 4gq + r for this lane's row; keys at or
-// past `limit` are masked. Updates the row's max m (log2 units), the lane's
-// partial sum l and the accumulators o (rows 4gq + r), and returns the
-// chunk's probabilities as the bf16 A operand of the PV product.
-template <int NACC>
+// s[b][r]: raw score q.k of key kc0 + 16b + 4gq + r for this lane's row. With
+// MASK, keys at or past `limit` are excluded; without, every key of the chunk
+// is visible to every row. The scale is folded into the exponent:
+// p = 2^(s * scale_log2 - m). Updates the row's max m (log2 units), the
+// lane's partial sum l and the accumulators o (rows 4gq + r), and returns
+// the probabilities as the bf16 A operand of the PV product.
+template <int NACC, bool MASK>
 __device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int limit, int gq, float scale_log2,
                                                float& m, float& l, f32x4 (&o)[NACC]) {
-  float z[8];
-  float cmax = -INFINITY;
+  float x[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const int key = kc0 + chunk_key(e, gq);
-    z[e] = key < limit ? s[e >> 2][e & 3] * scale_log2 : -INFINITY;
-    cmax = fmaxf(cmax, z[e]);
+    x[e] = s[e >> 2][e & 3];
+    if constexpr (MASK) x[e] = kc0 + chunk_key(e, gq) < limit ? x[e] : -INFINITY;
   }
-  cmax = group_max(cmax);
+  float cmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+  cmax = group_max(cmax) * scale_log2;
   const bool need = cmax > m + kRescaleThreshold;
   if (wave_any(need)) {
     const float m_new = need ? cmax : m;
@@ -111,18 +112,30 @@ __device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int
       for (int a = 0; a < NACC; ++a) o[a][r] *= ar;
     }
   }
-  const float m_use = m == -INFINITY ? 0.f : m;
+  const float neg_m = m == -INFINITY ? 0.f : -m;
   u32x4 pop;
   float psum = 0.f;
 #pragma unroll
   for (int e2 = 0; e2 < 4; ++e2) {
-    const float p0 = fast_exp2(z[2 * e2] - m_use);
-    const float p1 = fast_exp2(z[2 * e2 + 1] - m_use);
+    const float p0 = fast_exp2(fmaf(x[2 * e2], scale_log2, neg_m));
+    const float p1 = fast_exp2(fmaf(x[2 * e2 + 1], scale_log2, neg_m));
     psum += p0 + p1;
     pop[e2] = pack_bf16x2(p0, p1);
   }
   l += psum;
   return pop;
+}
+
+// Masked only when the chunk reaches past the smallest key limit of the wave's
+// rows. The 512-wide value layout keeps a single (masked) path: a second
+// inlined copy would push its 512-register budget into spills.
+template <int NACC>
+__device__ __forceinline__ u32x4 softmax_chunk_auto(const f32x4 (&s)[2], int kc0, int limit, int wave_min_limit,
+                                                    int gq, float scale_log2, float& m, float& l, f32x4 (&o)[NACC]) {
+  if constexpr (NACC <= 8) {
+    if (kc0 + 32 <= wave_min_limit) return softmax_chunk<NACC, false>(s, kc0, limit, gq, scale_log2, m, l, o);
+  }
+  return softmax_chunk<NACC, true>(s, kc0, limit, gq, scale_log2, m, l, o);
 }
 
 // ---------------------------------------------------------------------------
@@ -170,6 +183,7 @@ void decode_gqa_kernel(AttnParams p) {
 #pragma unroll
     for (int c = 0; c < DC; ++c) qop[c] = ok ? load16(qr + 32 * c) : zero4();
   }
+  wait_vmem_all();
 
   float m = -INFINITY, l = 0.f;
   f32x4 o[DPL];
@@ -185,51 +199,59 @@ void decode_gqa_kernel(AttnParams p) {
     __syncthreads();
     const int nch = (wk1 - wk0 + 31) >> 5;
 
+    // Every lane always issues its loads, so the number of loads in flight is
+    // fixed and the wait before a chunk's math covers exactly that chunk. Keys
+    // past the window read its last key's (finite) row instead; the softmax
+    // masks them to probability 0.
     auto load = [&](Chunk& c, int ci) {
       const int kc0 = wk0 + 32 * ci;
-      const bool any = ci < nch;
-      int page0 = 0, page1 = 0;
-      if (any) {
-        page0 = s_pt[kc0 / P - pg0];
-        page1 = (kc0 + 16 < wk1) ? s_pt[(kc0 + 16) / P - pg0] : page0;
-      }
+      const int klast = wk1 - 1;
+      const int page0 = s_pt[min(kc0, klast) / P - pg0];
+      const int page1 = s_pt[min(kc0 + 16, klast) / P - pg0];
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const int key = kc0 + 16 * b + n;
-        const bool ok = any && key < wk1;
-        const uint16_t* kr = kbase + int64_t(b ? page1 : page0) * ksp + int64_t(key % P) * kss;
+        const uint16_t* kr = kbase + int64_t(b ? page1 : page0) * ksp + int64_t(min(key, klast) % P) * kss;
 #pragma unroll
-        for (int cc = 0; cc < DC; ++cc) c.k[b][cc] = ok ? load16(kr + 32 * cc) : zero4();
+        for (int cc = 0; cc < DC; ++cc) c.k[b][cc] = load16(kr + 32 * cc);
       }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int key = kc0 + chunk_key(e, gq);
-        const bool ok = any && key < wk1;
-        const uint16_t* vr = vbase + int64_t((e >> 2) ? page1 : page0) * vsp + int64_t(key % P) * vss;
-        if constexpr (D == 128) c.v[e] = ok ? load16(vr) : zero4();
-        else c.v[e] = ok ? load8(vr) : u32x2{0u, 0u};
+        const uint16_t* vr = vbase + int64_t((e >> 2) ? page1 : page0) * vsp + int64_t(min(key, klast) % P) * vss;
+        if constexpr (D == 128) c.v[e] = load16(vr);
+        else c.v[e] = load8(vr);
       }
     };
 
-    Chunk cur, nxt;
-    load(cur, w);
-    for (int ci = w; ci < nch; ci += NW) {
-      load(nxt, ci + NW);   // next chunk's gathers stay in flight during this chunk's math
+    auto compute = [&](const Chunk& c, int ci) {
       const int kc0 = wk0 + 32 * ci;
       f32x4 s[2];
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int cc = 0; cc < DC; ++cc) s[b] = mfma_16x16x32(cur.k[b][cc], qop[cc], s[b]);
+        for (int cc = 0; cc < DC; ++cc) s[b] = mfma_16x16x32(c.k[b][cc], qop[cc], s[b]);
       }
-      const u32x4 pop = softmax_chunk<DPL>(s, kc0, wk1, gq, p.scale_log2, m, l, o);
+      const u32x4 pop = softmax_chunk_auto<DPL>(s, kc0, wk1, wk1, gq, p.scale_log2, m, l, o);
       u32x4 vop[DPL];
-      if constexpr (D == 128) transpose8x8(cur.v, vop);
-      else transpose8x4(cur.v, vop);
+      if constexpr (D == 128) transpose8x8(c.v, vop);
+      else transpose8x4(c.v, vop);
 #pragma unroll
       for (int a = 0; a < DPL; ++a) o[a] = mfma_16x16x32(pop, vop[a], o[a]);
-      cur = nxt;
+    };
+
+    // Two fixed chunk buffers, the loop unrolled by two: the next chunk's
+    // gathers stay in flight during this chunk's math (a register copy
+    // between iterations would force them to land first).
+    Chunk A, B;
+    load(A, w);
+    for (int ci = w; ci < nch; ci += 2 * NW) {
+      load(B, ci + NW);
+      compute(A, ci);
+      if (ci + NW >= nch) break;
+      load(A, ci + 2 * NW);
+      compute(B, ci + NW);
     }
   }
 
@@ -310,6 +332,7 @@ struct RowParCfg {
   static constexpr int V_ELEMS = VALIAS ? 0 : BN * LDS_ROW_V;
   static constexpr size_t LDS_BYTES = size_t(2) * (K_ELEMS + V_ELEMS) * 2 + kPageWin * 4;
   static_assert(BN % 32 == 0, "key tile is a multiple of 32");
+  static_assert(K_CHUNKS % NT == 0 && TILE_CHUNKS % NT == 0, "tile chunks must split evenly over threads");
 };
 
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P>
@@ -332,7 +355,7 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
   const int nq = p.qsl[seq + 1] - q0;
   const int32_t* bt_row = p.bt + int64_t(seq) * p.bt_stride;
 
-  int key_begin, key_end, head_kv, wave_limit;
+  int key_begin, key_end, head_kv, wave_limit, wave_min_limit;
   bool wave_on = true;
   int row_tok[RB], row_head[RB], row_limit[RB];
   if constexpr (MODE == kDecodeLatent) {
@@ -346,7 +369,7 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       row_head[rb] = hg * p.rows_per_wg + (w * RB + rb) * 16 + n;
       row_limit[rb] = key_end;
     }
-    wave_limit = key_end;
+    wave_limit = wave_min_limit = key_end;
   } else if constexpr (MODE == kPrefillPerHead) {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
@@ -364,6 +387,8 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
     const int last = min(r1, r0 + (w + 1) * RB * 16) - 1;
     wave_on = r0 + w * RB * 16 < r1;
     wave_limit = wave_on ? (L - nq + last + 1) : 0;
+    // invalid rows (past r1) see only key 0, so the smallest limit is 1 when the wave has any
+    wave_min_limit = (r0 + (w + 1) * RB * 16 <= r1) ? (L - nq + r0 + w * RB * 16 + 1) : 1;
   } else {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
@@ -382,6 +407,7 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       row_limit[rb] = ok ? (L - nq + local + 1) : 1;
     }
     wave_limit = wave_on ? (L - nq + r1) : 0;
+    wave_min_limit = (r0 + RB * 16 <= r1) ? (L - nq + r0 + 1) : 1;
   }
   const uint16_t* kbase = p.kc.base + int64_t(head_kv) * p.kc.sh;
   const uint16_t* vbase = p.vc.base + int64_t(head_kv) * p.vc.sh;
@@ -395,6 +421,7 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
 #pragma unroll
     for (int c = 0; c < C::DC; ++c) qop[rb][c] = load16(qr + 32 * c);
   }
+  wait_vmem_all();
 
   float m[RB], l[RB];
   f32x4 o[RB][C::NACC];
@@ -417,23 +444,23 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
   };
 
   // Gather key tile kb .. kb+BN-1 through the staged block table into registers.
+  // Loads are unconditional, so the count of loads in flight stays exact for
+  // the wait pass; keys past key_end read the last key's (finite) row instead,
+  // and every such key is masked to probability 0 for every row.
   auto load_tile = [&](u32x4 (&st)[C::NLD], int kb) {
+    const int klast = key_end - 1;
 #pragma unroll
     for (int i = 0; i < C::NLD; ++i) {
       const int u = i * C::NT + tid;
-      if (u < C::K_CHUNKS) {
+      if (i * C::NT < C::K_CHUNKS) {
         const int r = u / C::CPR, x = u % C::CPR;
-        const int key = kb + r;
-        st[i] = key < key_end
-                    ? load16(kbase + int64_t(s_pt[key / P - pt_base]) * ksp + int64_t(key % P) * kss + 8 * x)
-                    : zero4();
-      } else if (C::CPRV > 0 && u < C::TILE_CHUNKS) {
+        const int kc = min(kb + r, klast);
+        st[i] = load16(kbase + int64_t(s_pt[kc / P - pt_base]) * ksp + int64_t(kc % P) * kss + 8 * x);
+      } else {
         const int u2 = u - C::K_CHUNKS;
         const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
-        const int key = kb + r;
-        st[i] = key < key_end
-                    ? load16(vbase + int64_t(s_pt[key / P - pt_base]) * vsp + int64_t(key % P) * vss + 8 * x)
-                    : zero4();
+        const int kc = min(kb + r, klast);
+        st[i] = load16(vbase + int64_t(s_pt[kc / P - pt_base]) * vsp + int64_t(kc % P) * vss + 8 * x);
       }
     }
   };
@@ -441,10 +468,10 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
 #pragma unroll
     for (int i = 0; i < C::NLD; ++i) {
       const int u = i * C::NT + tid;
-      if (u < C::K_CHUNKS) {
+      if (i * C::NT < C::K_CHUNKS) {
         const int r = u / C::CPR, x = u % C::CPR;
         *reinterpret_cast<u32x4*>(ldsK + buf * C::K_ELEMS + r * C::LDS_ROW + 8 * x) = st[i];
-      } else if (C::CPRV > 0 && u < C::TILE_CHUNKS) {
+      } else {
         const int u2 = u - C::K_CHUNKS;
         const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
         *reinterpret_cast<u32x4*>(ldsV + buf * C::V_ELEMS + r * C::LDS_ROW_V + 8 * x) = st[i];
@@ -475,7 +502,8 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       u32x4 pop[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
-        pop[rb] = softmax_chunk<C::NACC>(s[rb], kc0, row_limit[rb], gq, p.scale_log2, m[rb], l[rb], o[rb]);
+        pop[rb] = softmax_chunk_auto<C::NACC>(s[rb], kc0, row_limit[rb], wave_min_limit, gq, p.scale_log2, m[rb],
+                                              l[rb], o[rb]);
       // PV: the lane reads its 8 keys' value dims and transposes them in registers.
 #pragma unroll
       for (int vg = 0; vg < C::NVG; ++vg) {
@@ -514,22 +542,22 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       if (need_last >= pt_base + kPageWin) {   // slide the block-table window (uniform)
         pt_base = nb / P;
         load_window(pt_base);
-        __syncthreads();
+        lds_barrier();
       }
       load_tile(ahead, nb);
     }
     compute_tile(key_begin + kt * BN, kt & 1);
     if (kt + 1 < ntiles) store_tile(ready, (kt + 1) & 1);
-    __syncthreads();
+    lds_barrier();
   };
 
   u32x4 stA[C::NLD], stB[C::NLD];
   load_window(pt_base);
-  __syncthreads();
+  lds_barrier();
   if (ntiles > 0) load_tile(stA, key_begin);
   if (ntiles > 1) load_tile(stB, key_begin + BN);
   if (ntiles > 0) store_tile(stA, 0);
-  __syncthreads();
+  lds_barrier();
   for (int kt = 0; kt < ntiles; kt += 2) {
     step(kt, stA, stB);
     if (kt + 1 < ntiles) step(kt + 1, stB, stA);

@@ -29,6 +29,29 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(const u32x4& a, const u32x4& b, c
 
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4] = 7, lgkmcnt [11:8] = 15).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+// Work-group barrier for LDS hand-offs that leaves vector-memory loads in
+// flight: this wave's LDS writes complete (lgkmcnt 0), then s_barrier. (The
+// fence inside __syncthreads also waits for every outstanding global load,
+// which would drain a prefetch pipeline at each tile.) The signal fences keep
+// the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt 63, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Let every outstanding vector-memory access land (placed after loads issued
+// before a pipelined loop, so loop-carried wait tracking starts clean).
+__device__ __forceinline__ void wait_vmem_all() { wait_vmem<0>(); }
+
 // Pack two floats into two bf16 (round to nearest even) in one dword, lo first.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = (__bf16)lo;
@@ -57,6 +80,11 @@ __device__ __forceinline__ u32x2 load8(const uint16_t* p) {
   return *reinterpret_cast<const u32x2*>(p);
 }
 
+// Two bf16 halves from two dwords: lo -> (x.lo, y.lo), hi -> (x.hi, y.hi)
+// (one v_perm_b32 each; selector bytes 0-3 pick from x, 4-7 from y).
+__device__ __forceinline__ uint32_t pair_lo(uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x05040100u); }
+__device__ __forceinline__ uint32_t pair_hi(uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x07060302u); }
+
 // 8 key rows x 8 dims (row r holds dims 0..7 of key r as 4 dwords) ->
 // 8 B-operands, operand c holding dim c of keys 0..7 (dword w = keys 2w, 2w+1).
 __device__ __forceinline__ void transpose8x8(const u32x4 (&rows)[8], u32x4 (&ops)[8]) {
@@ -66,7 +94,7 @@ __device__ __forceinline__ void transpose8x8(const u32x4 (&rows)[8], u32x4 (&ops
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const uint32_t x = rows[2 * w][dw], y = rows[2 * w + 1][dw];
-      ops[c][w] = (c & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+      ops[c][w] = (c & 1) ? pair_hi(x, y) : pair_lo(x, y);
     }
   }
 }
@@ -79,7 +107,7 @@ __device__ __forceinline__ void transpose8x4(const u32x2 (&rows)[8], u32x4 (&ops
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const uint32_t x = rows[2 * w][dw], y = rows[2 * w + 1][dw];
-      ops[c][w] = (c & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+      ops[c][w] = (c & 1) ? pair_hi(x, y) : pair_lo(x, y);
     }
   }
 }
