@@ -378,3 +378,24 @@ def test_planted_mistakes(mutant, monkeypatch):
             if not ok:
                 failed.append(name)
     assert failed, f"planted mistake {mutant} passed every pin"
+
+
+def test_attention_rows_matches_batch_oracle():
+    """The per-row oracle used for sampled checks at full size (it widens only
+    the pages a sequence uses and renumbers them) returns exactly the rows of
+    the pinned batch oracle."""
+    rng = np.random.default_rng(30)
+    Ls, ns = [45, 17, 70, 5], [1, 17, 30, 1]
+    q, ks, vs, kc, vc, bt = rand_problem(rng, Ls, ns, Hq=6, Hkv=2, d=8, P=4)
+    qsl = np.concatenate([[0], np.cumsum(ns)])
+    kw = dict(num_kv_heads=2, page_size=4)
+    full_o, full_l = A.paged_attention(q, kc, vc, bt, Ls, qsl, 0.3, **kw)
+    picks = [(0, 0), (1, 16), (1, 0), (2, 29), (2, 3), (3, 0)]
+    o, l = A.attention_rows(q, kc, vc, bt, Ls, qsl, 0.3, picks, **kw)
+    idx = [int(qsl[s]) + i for s, i in picks]
+    assert np.array_equal(o, full_o[idx]) and np.array_equal(l, full_l[idx])
+    # latent layout: V aliases the first columns of K
+    kc2 = kc[..., :8]
+    o1, l1 = A.paged_attention(q, kc2, None, bt, Ls, qsl, 0.3, v_aliases_k=True, head_dim_v=5, **kw)
+    o2, l2 = A.attention_rows(q, kc2, None, bt, Ls, qsl, 0.3, picks, v_aliases_k=True, head_dim_v=5, **kw)
+    assert np.array_equal(o2, o1[idx]) and np.array_equal(l2, l1[idx])
