@@ -32,6 +32,9 @@ def common_flags():
     return ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
             # keep the compiler from forming packed fp32 VALU instructions
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            # scores are finite; max() needs no NaN quieting (a NaN from a wrong
+            # page still reaches the output through the P x V product)
+            "-fno-honor-nans",
             "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-function"]
 
 

@@ -126,6 +126,52 @@ __device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int
   return pop;
 }
 
+// Same step with the row sums kept on the matrix core: `lsum` is an MFMA
+// accumulator (rows 4gq + r, every column holds the row's sum of the bf16
+// probabilities), updated by the caller with P x ones next to P x V, so the
+// denominator uses exactly the probabilities the numerator does. Rescaling
+// treats it like an output accumulator.
+template <int NACC, bool MASK>
+__device__ __forceinline__ u32x4 softmax_chunk_acc(const f32x4 (&s)[2], int kc0, int limit, int gq, float scale_log2,
+                                                   float& m, f32x4& lsum, f32x4 (&o)[NACC]) {
+  float x[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    x[e] = s[e >> 2][e & 3];
+    if constexpr (MASK) x[e] = kc0 + chunk_key(e, gq) < limit ? x[e] : -INFINITY;
+  }
+  float cmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+  cmax = group_max(cmax) * scale_log2;
+  const bool need = cmax > m + kRescaleThreshold;
+  if (wave_any(need)) {
+    const float m_new = need ? cmax : m;
+    const float alpha = fast_exp2(m - m_new);
+    m = m_new;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float ar = shfl_f(alpha, 4 * gq + r);
+      lsum[r] *= ar;
+#pragma unroll
+      for (int a = 0; a < NACC; ++a) o[a][r] *= ar;
+    }
+  }
+  const float neg_m = m == -INFINITY ? 0.f : -m;
+  u32x4 pop;
+#pragma unroll
+  for (int e2 = 0; e2 < 4; ++e2)
+    pop[e2] = pack_bf16x2(fast_exp2(fmaf(x[2 * e2], scale_log2, neg_m)),
+                          fast_exp2(fmaf(x[2 * e2 + 1], scale_log2, neg_m)));
+  return pop;
+}
+
+template <int NACC>
+__device__ __forceinline__ u32x4 softmax_chunk_acc_auto(const f32x4 (&s)[2], int kc0, int limit, int wave_min_limit,
+                                                        int gq, float scale_log2, float& m, f32x4& lsum,
+                                                        f32x4 (&o)[NACC]) {
+  if (kc0 + 32 <= wave_min_limit) return softmax_chunk_acc<NACC, false>(s, kc0, limit, gq, scale_log2, m, lsum, o);
+  return softmax_chunk_acc<NACC, true>(s, kc0, limit, gq, scale_log2, m, lsum, o);
+}
+
 // Masked only when the chunk reaches past the smallest key limit of the wave's
 // rows. The 512-wide value layout keeps a single (masked) path: a second
 // inlined copy would push its 512-register budget into spills.
@@ -303,46 +349,72 @@ void decode_gqa_kernel(AttnParams p) {
 // ---------------------------------------------------------------------------
 // Row-parallel attention: prefill (grouped-query and latent) and latent decode.
 //
-// Each wave owns RB blocks of 16 query rows; the work-group stages key tiles
-// of BN keys, gathered through the block table, in double-buffered LDS that
-// every wave reads. Tile loads are issued two tiles ahead into registers.
-// Row layouts:
+// Each wave owns RB blocks of 16 query rows. The work-group streams key tiles
+// of BN keys, gathered through the block table, straight from global memory
+// into a ring of NS LDS stages (global_load_lds_dwordx4: lane i of a wave
+// writes 16 bytes at stage + 16*i, so each instruction fills 1 KB); NS-1 tiles
+// are in flight while one is consumed, and one barrier per tile hands a stage
+// over. Waits on these loads are explicit (vmcnt counts only them inside the
+// loop). Row layouts:
 //   kPrefillGrouped  work-group = (tile of RB*16 tokens, KV head, head chunk);
-//                    wave w = query head, rb = token block. One K/V tile
-//                    feeds every query head of the KV head.
+//                    wave w = query head, rb = token block: one K/V tile in
+//                    LDS feeds every query head of the KV head.
 //   kPrefillPerHead  work-group = (tile of NW*RB*16 tokens, query head).
 //   kDecodeLatent    work-group = (decode item, group of NW*RB*16 heads).
+// LDS rows: grouped-query K/V rows are unpadded and XOR-swizzled by 16-byte
+// chunk so the MFMA operand reads are bank-conflict free; latent rows
+// (576 wide) are padded by one chunk instead.
 // ---------------------------------------------------------------------------
 enum RowMode { kPrefillGrouped = 0, kPrefillPerHead = 1, kDecodeLatent = 2 };
 
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS>
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) void* gbl_void_ptr;
+
+// 16-byte global -> LDS copy per lane; `lds_wave_base` is wave-uniform.
+__device__ __forceinline__ void dma16(const void* src, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((gbl_void_ptr)(src), (lds_void_ptr)(lds_wave_base), 16, 0, 0);
+}
+
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int NS>
 struct RowParCfg {
   static constexpr int DC = DQK / 32;
-  static constexpr int LDS_ROW = DQK + 8;                 // 16-byte pad per row
-  static constexpr int LDS_ROW_V = VALIAS ? LDS_ROW : DV + 8;
-  static constexpr int CPR = DQK / 8;                     // 16-byte chunks per K row
-  static constexpr int CPRV = VALIAS ? 0 : DV / 8;
+  static constexpr int CPR = DQK / 8;                      // 16-byte chunks of a K row
+  static constexpr int CPRV = VALIAS ? 0 : DV / 8;         // of a separate V row
+  static constexpr int ROWB = VALIAS ? CPR + 1 : CPR;      // LDS K row stride, chunks
+  static constexpr int K_SLOTS = BN * ROWB;
+  static constexpr int SLOTS = K_SLOTS + BN * CPRV;
+  static constexpr int TI_RAW = (SLOTS + 63) / 64;         // 1 KB loads per tile
+  static constexpr int TI = (TI_RAW + NW - 1) / NW * NW;
+  static constexpr int NI = TI / NW;                       // per wave per tile
+  static constexpr int STAGE = TI * 1024;
+  static constexpr int V_OFF = K_SLOTS * 16;
   static constexpr int NT = NW * 64;
-  static constexpr int K_CHUNKS = BN * CPR;
-  static constexpr int TILE_CHUNKS = BN * (CPR + CPRV);
-  static constexpr int NLD = (TILE_CHUNKS + NT - 1) / NT;
   static constexpr int NACC = DV / 16;
-  static constexpr int NVG = DV >= 128 ? DV / 128 : 1;   // value-dim groups of 8 per lane
-  static constexpr int K_ELEMS = BN * LDS_ROW;
-  static constexpr int V_ELEMS = VALIAS ? 0 : BN * LDS_ROW_V;
-  static constexpr size_t LDS_BYTES = size_t(2) * (K_ELEMS + V_ELEMS) * 2 + kPageWin * 4;
+  static constexpr size_t LDS_BYTES = size_t(NS) * STAGE + kPageWin * 4;
   static_assert(BN % 32 == 0, "key tile is a multiple of 32");
-  static_assert(K_CHUNKS % NT == 0 && TILE_CHUNKS % NT == 0, "tile chunks must split evenly over threads");
+  static_assert(VALIAS || K_SLOTS % 64 == 0, "separate K and V regions start on a load boundary");
+  static_assert((NS - 2) * NI < 64, "vmcnt range");
 };
 
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P>
+// Physical 16-byte chunk of logical chunk x in row r of an LDS tile.
+template <int DQK, bool VALIAS>
+__device__ __forceinline__ int swz_k(int x, int r) {
+  if constexpr (VALIAS) return x;
+  else if constexpr (DQK == 128) return x ^ (r & 15);        // 256-byte rows
+  else return x ^ ((r >> 1) & 7);                            // 128-byte rows
+}
+template <int DV>
+__device__ __forceinline__ int swz_v(int x, int r) {
+  if constexpr (DV == 128) return x ^ (2 * (r & 7));
+  else return x ^ (2 * ((r >> 1) & 3));
+}
+
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS>
 __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
-  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS>;
-  static_assert(kPageWin * P >= 2 * BN + P, "page window must cover two key tiles");
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  uint16_t* ldsK = lds;
-  uint16_t* ldsV = VALIAS ? lds : lds + 2 * C::K_ELEMS;
-  int* s_pt = reinterpret_cast<int*>(lds + 2 * (C::K_ELEMS + C::V_ELEMS));
+  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
+  static_assert(NS == 3 || NS == 4, "stages");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+  int* s_pt = reinterpret_cast<int*>(lds + NS * C::STAGE);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -387,7 +459,7 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
     const int last = min(r1, r0 + (w + 1) * RB * 16) - 1;
     wave_on = r0 + w * RB * 16 < r1;
     wave_limit = wave_on ? (L - nq + last + 1) : 0;
-    // invalid rows (past r1) see only key 0, so the smallest limit is 1 when the wave has any
+    // rows past r1 see only key 0, so a partial block forces the masked path
     wave_min_limit = (r0 + (w + 1) * RB * 16 <= r1) ? (L - nq + r0 + w * RB * 16 + 1) : 1;
   } else {
     const int r0 = it[2], r1 = it[3];
@@ -410,8 +482,9 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
     wave_min_limit = (r0 + RB * 16 <= r1) ? (L - nq + r0 + 1) : 1;
   }
   const uint16_t* kbase = p.kc.base + int64_t(head_kv) * p.kc.sh;
-  const uint16_t* vbase = p.vc.base + int64_t(head_kv) * p.vc.sh;
-  const int64_t ksp = p.kc.sp, kss = p.kc.ss, vsp = p.vc.sp, vss = p.vc.ss;
+  const uint16_t* vbase = (VALIAS ? p.kc.base : p.vc.base) + int64_t(head_kv) * (VALIAS ? p.kc.sh : p.vc.sh);
+  const int64_t ksp = p.kc.sp, kss = p.kc.ss;
+  const int64_t vsp = VALIAS ? p.kc.sp : p.vc.sp, vss = VALIAS ? p.kc.ss : p.vc.ss;
 
   // Q as the B operand of S^T = K Q^T.
   u32x4 qop[RB][C::DC];
@@ -421,67 +494,51 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
 #pragma unroll
     for (int c = 0; c < C::DC; ++c) qop[rb][c] = load16(qr + 32 * c);
   }
-  wait_vmem_all();
 
-  float m[RB], l[RB];
-  f32x4 o[RB][C::NACC];
+  float m[RB];
+  f32x4 o[RB][C::NACC], lsum[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     m[rb] = -INFINITY;
-    l[rb] = 0.f;
+    lsum[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int a = 0; a < C::NACC; ++a) o[rb][a] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 x 8
 
-  const int ntiles = (key_end - key_begin + BN - 1) / BN;
-  const int last_page = key_end > 0 ? (key_end - 1) / P : 0;
-  int pt_base = key_begin / P;
-  auto load_window = [&](int base) {
-    for (int i = tid; i < kPageWin; i += C::NT) {
-      const int pg = base + i;
-      s_pt[i] = pg <= last_page ? bt_row[pg] : 0;
-    }
-  };
-
-  // Gather key tile kb .. kb+BN-1 through the staged block table into registers.
-  // Loads are unconditional, so the count of loads in flight stays exact for
-  // the wait pass; keys past key_end read the last key's (finite) row instead,
-  // and every such key is masked to probability 0 for every row.
-  auto load_tile = [&](u32x4 (&st)[C::NLD], int kb) {
+  // Issue this wave's share of the loads of key tile kb into stage st. Every
+  // lane always issues (keys past key_end read the last key's row, padding
+  // slots read a dummy row); those keys are masked to probability 0.
+  auto issue = [&](int kb, int st, int pt_base) {
+    uint8_t* sbase = lds + st * C::STAGE;
     const int klast = key_end - 1;
 #pragma unroll
-    for (int i = 0; i < C::NLD; ++i) {
-      const int u = i * C::NT + tid;
-      if (i * C::NT < C::K_CHUNKS) {
-        const int r = u / C::CPR, x = u % C::CPR;
-        const int kc = min(kb + r, klast);
-        st[i] = load16(kbase + int64_t(s_pt[kc / P - pt_base]) * ksp + int64_t(kc % P) * kss + 8 * x);
-      } else {
-        const int u2 = u - C::K_CHUNKS;
-        const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
-        const int kc = min(kb + r, klast);
-        st[i] = load16(vbase + int64_t(s_pt[kc / P - pt_base]) * vsp + int64_t(kc % P) * vss + 8 * x);
+    for (int j = 0; j < C::NI; ++j) {
+      const int blk = w * C::NI + j;
+      const int s = blk * 64 + lane;
+      int row = 0, x = 0;
+      bool isv = false;
+      if (s < C::K_SLOTS) {
+        row = s / C::ROWB;
+        const int pc = s % C::ROWB;
+        x = pc < C::CPR ? swz_k<DQK, VALIAS>(pc, row) : 0;
+      } else if (s < C::SLOTS) {
+        isv = true;
+        const int s2 = s - C::K_SLOTS;
+        row = s2 / (C::CPRV > 0 ? C::CPRV : 1);
+        x = swz_v<DV>(s2 % (C::CPRV > 0 ? C::CPRV : 1), row);
       }
-    }
-  };
-  auto store_tile = [&](const u32x4 (&st)[C::NLD], int buf) {
-#pragma unroll
-    for (int i = 0; i < C::NLD; ++i) {
-      const int u = i * C::NT + tid;
-      if (i * C::NT < C::K_CHUNKS) {
-        const int r = u / C::CPR, x = u % C::CPR;
-        *reinterpret_cast<u32x4*>(ldsK + buf * C::K_ELEMS + r * C::LDS_ROW + 8 * x) = st[i];
-      } else {
-        const int u2 = u - C::K_CHUNKS;
-        const int r = u2 / (C::CPRV > 0 ? C::CPRV : 1), x = u2 % (C::CPRV > 0 ? C::CPRV : 1);
-        *reinterpret_cast<u32x4*>(ldsV + buf * C::V_ELEMS + r * C::LDS_ROW_V + 8 * x) = st[i];
-      }
+      const int key = min(kb + row, klast);
+      const int64_t page = s_pt[key / P - pt_base];
+      const uint16_t* src = isv ? vbase + page * vsp + int64_t(key % P) * vss
+                                : kbase + page * ksp + int64_t(key % P) * kss;
+      dma16(src + 8 * x, sbase + blk * 1024);
     }
   };
 
-  auto compute_tile = [&](int kb, int buf) {
-    const uint16_t* Kt = ldsK + buf * C::K_ELEMS;
-    const uint16_t* Vt = VALIAS ? Kt : ldsV + buf * C::V_ELEMS;
+  auto compute_tile = [&](int kb, int st) {
+    const uint8_t* Kst = lds + st * C::STAGE;
+    const uint8_t* Vst = VALIAS ? Kst : Kst + C::V_OFF;
 #pragma unroll
     for (int ch = 0; ch < BN / 32; ++ch) {
       const int kc0 = kb + 32 * ch;
@@ -489,119 +546,120 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       f32x4 s[RB][2];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      auto kaddr = [&](int b, int c) {
+        const int row = 32 * ch + 16 * b + n;
+        return Kst + row * C::ROWB * 16 + 16 * swz_k<DQK, VALIAS>(4 * c + gq, row);
+      };
+      if constexpr (C::DC <= 4) {
+        // All K operands of the chunk first, then 2*RB independent accumulator
+        // chains interleaved, so neither LDS latency nor MFMA dependencies stall.
+        u32x4 kop[2][C::DC];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const uint16_t* kr = Kt + (32 * ch + 16 * b + n) * C::LDS_ROW + 8 * gq;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int c = 0; c < C::DC; ++c) {
-          const u32x4 kop = *reinterpret_cast<const u32x4*>(kr + 32 * c);
+          for (int c = 0; c < C::DC; ++c) kop[b][c] = *reinterpret_cast<const u32x4*>(kaddr(b, c));
 #pragma unroll
-          for (int rb = 0; rb < RB; ++rb) s[rb][b] = mfma_16x16x32(kop, qop[rb][c], s[rb][b]);
-        }
+        for (int c = 0; c < C::DC; ++c)
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) s[rb][b] = mfma_16x16x32(kop[b][c], qop[rb][c], s[rb][b]);
+      } else {
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int c = 0; c < C::DC; ++c) {
+            const u32x4 kop = *reinterpret_cast<const u32x4*>(kaddr(b, c));
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) s[rb][b] = mfma_16x16x32(kop, qop[rb][c], s[rb][b]);
+          }
       }
       u32x4 pop[RB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        pop[rb] = softmax_chunk_auto<C::NACC>(s[rb], kc0, row_limit[rb], wave_min_limit, gq, p.scale_log2, m[rb],
-                                              l[rb], o[rb]);
-      // PV: the lane reads its 8 keys' value dims and transposes them in registers.
+      for (int rb = 0; rb < RB; ++rb) {
+        pop[rb] = softmax_chunk_acc_auto<C::NACC>(s[rb], kc0, row_limit[rb], wave_min_limit, gq, p.scale_log2,
+                                                  m[rb], lsum[rb], o[rb]);
+        lsum[rb] = mfma_16x16x32(pop[rb], ones, lsum[rb]);
+      }
+      // PV: transposing LDS reads give each lane its 8 keys of value column
+      // 16*cv + n (rows 4*gq + e and 16 + 4*gq + e of the chunk).
+      const int rowa = 32 * ch + 4 * gq + (n >> 2), rowb = rowa + 16;
+      const int cb = 8 * (n & 3);   // byte offset of the lane's 4 columns within a 32-byte column block
 #pragma unroll
-      for (int vg = 0; vg < C::NVG; ++vg) {
-        if constexpr (DV >= 128) {
-          u32x4 rows[8], vop[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            rows[e] = *reinterpret_cast<const u32x4*>(Vt + (32 * ch + chunk_key(e, gq)) * C::LDS_ROW_V + 128 * vg + 8 * n);
-          transpose8x8(rows, vop);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int c = 0; c < 8; ++c) o[rb][8 * vg + c] = mfma_16x16x32(pop[rb], vop[c], o[rb][8 * vg + c]);
+      for (int cv = 0; cv < C::NACC; ++cv) {
+        const uint8_t *va, *vb;
+        if constexpr (VALIAS) {
+          va = Vst + rowa * C::ROWB * 16 + 32 * cv + cb;
+          vb = Vst + rowb * C::ROWB * 16 + 32 * cv + cb;
         } else {
-          u32x2 rows[8];
-          u32x4 vop[4];
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            rows[e] = *reinterpret_cast<const u32x2*>(Vt + (32 * ch + chunk_key(e, gq)) * C::LDS_ROW_V + 4 * n);
-          transpose8x4(rows, vop);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) o[rb][c] = mfma_16x16x32(pop[rb], vop[c], o[rb][c]);
+          const int x = 2 * cv + (cb >> 4), off = cb & 15;
+          va = Vst + rowa * C::CPRV * 16 + 16 * swz_v<DV>(x, rowa) + off;
+          vb = Vst + rowb * C::CPRV * 16 + 16 * swz_v<DV>(x, rowb) + off;
         }
+        const u32x2 lo = lds_read_tr16(reinterpret_cast<const uint16_t*>(va));
+        const u32x2 hi = lds_read_tr16(reinterpret_cast<const uint16_t*>(vb));
+        const u32x4 vop = {lo[0], lo[1], hi[0], hi[1]};
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) o[rb][cv] = mfma_16x16x32(pop[rb], vop, o[rb][cv]);
       }
     }
   };
 
-  // One pipeline step: gather tile kt+2 into `ahead`, compute tile kt from LDS,
-  // then move tile kt+1 (gathered one step earlier into `ready`) into LDS.
-  auto step = [&](int kt, u32x4 (&ahead)[C::NLD], u32x4 (&ready)[C::NLD]) {
-    if (kt + 2 < ntiles) {
-      const int nb = key_begin + (kt + 2) * BN;
-      const int need_last = (min(nb + BN, key_end) - 1) / P;
-      if (need_last >= pt_base + kPageWin) {   // slide the block-table window (uniform)
-        pt_base = nb / P;
-        load_window(pt_base);
-        lds_barrier();
-      }
-      load_tile(ahead, nb);
-    }
-    compute_tile(key_begin + kt * BN, kt & 1);
-    if (kt + 1 < ntiles) store_tile(ready, (kt + 1) & 1);
+  // Q must land before the loop: inside it vmcnt counts only the tile loads.
+  wait_vmem_all();
+
+  // Windows of kPageWin block-table entries; the tile pipeline drains at the
+  // end of each window (one window covers the whole range in the usual case).
+  constexpr int WIN_KEYS = kPageWin * P;
+  static_assert(WIN_KEYS % BN == 0, "windows hold whole tiles");
+  const int last_page = key_end > 0 ? (key_end - 1) / P : 0;
+  for (int wk0 = key_begin; wk0 < key_end; wk0 += WIN_KEYS) {
+    const int wk1 = min(key_end, wk0 + WIN_KEYS);
+    const int pt_base = wk0 / P;
     lds_barrier();
-  };
-
-  u32x4 stA[C::NLD], stB[C::NLD];
-  load_window(pt_base);
-  lds_barrier();
-  if (ntiles > 0) load_tile(stA, key_begin);
-  if (ntiles > 1) load_tile(stB, key_begin + BN);
-  if (ntiles > 0) store_tile(stA, 0);
-  lds_barrier();
-  for (int kt = 0; kt < ntiles; kt += 2) {
-    step(kt, stA, stB);
-    if (kt + 1 < ntiles) step(kt + 1, stB, stA);
+    for (int i = tid; i < kPageWin; i += C::NT) {
+      const int pg = pt_base + i;
+      s_pt[i] = pg <= last_page ? bt_row[pg] : 0;
+    }
+    wait_vmem_all();
+    lds_barrier();
+    const int ntiles = (wk1 - wk0 + BN - 1) / BN;
+#pragma unroll
+    for (int t = 0; t < NS - 1; ++t)
+      if (t < ntiles) issue(wk0 + t * BN, t, pt_base);
+    for (int kt = 0; kt < ntiles; ++kt) {
+      const int ahead = min(NS - 2, ntiles - 1 - kt);   // tiles issued after tile kt
+      if (NS == 4 && ahead >= 2) wait_vmem<(NS - 2) * C::NI>();
+      else if (ahead >= 1) wait_vmem<C::NI>();
+      else wait_vmem<0>();
+      lds_barrier();   // tile kt is in LDS for every wave; stage (kt - 1) % NS is free
+      if (kt + NS - 1 < ntiles) issue(wk0 + (kt + NS - 1) * BN, (kt + NS - 1) % NS, pt_base);
+      compute_tile(wk0 + kt * BN, kt % NS);
+    }
   }
 
-  // Epilogue. Lane (n, gq) holds output rows 4*gq + r of each row block, at
-  // value dims 128*vg + 8*n + c (DV >= 128) or 4*n + c (DV = 64).
-  auto row_values = [&](int rb, int r, float scale, uint16_t* dst_row) {
-    if constexpr (DV >= 128) {
-#pragma unroll
-      for (int vg = 0; vg < C::NVG; ++vg) {
-        u32x4 pk;
-#pragma unroll
-        for (int c2 = 0; c2 < 4; ++c2)
-          pk[c2] = pack_bf16x2(o[rb][8 * vg + 2 * c2][r] * scale, o[rb][8 * vg + 2 * c2 + 1][r] * scale);
-        *reinterpret_cast<u32x4*>(dst_row + 128 * vg + 8 * n) = pk;
-      }
-    } else {
-      u32x2 pk;
-      pk[0] = pack_bf16x2(o[rb][0][r] * scale, o[rb][1][r] * scale);
-      pk[1] = pack_bf16x2(o[rb][2][r] * scale, o[rb][3][r] * scale);
-      *reinterpret_cast<u32x2*>(dst_row + 4 * n) = pk;
-    }
-  };
-
+  // Epilogue. Lane (n, gq) holds rows 4*gq + r of each row block at value
+  // columns 16*cv + n, and each row's probability sum in lsum[r].
   if constexpr (MODE != kDecodeLatent) {
     if (!wave_on) return;
     const int r0 = it[2], r1 = it[3];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const float lt = group_sum(l[rb]);
-      const int blk = MODE == kPrefillPerHead ? (w * RB + rb) : rb;   // token block of this row block
+      const int blk = MODE == kPrefillPerHead ? (w * RB + rb) : rb;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float lr = shfl_f(lt, 4 * gq + r);
         const int local = r0 + blk * 16 + 4 * gq + r;
+        const float mr = shfl_f(m[rb], 4 * gq + r);
         if (local < r1) {
-          const int64_t orow = int64_t(q0 + local) * p.Hq + row_head[rb];
-          row_values(rb, r, 1.f / lr, p.out + orow * DV);
+          const float lr = lsum[rb][r];
+          const float inv = 1.f / lr;
+          uint16_t* dst = p.out + (int64_t(q0 + local) * p.Hq + row_head[rb]) * DV + n;
+#pragma unroll
+          for (int cv = 0; cv < C::NACC; ++cv)
+            dst[16 * cv] = __builtin_bit_cast(uint16_t, (__bf16)(o[rb][cv][r] * inv));
+          if (n == 0 && p.lse) p.lse[int64_t(q0 + local) * p.Hq + row_head[rb]] = (mr + log2f(lr)) * kLn2;
         }
       }
-      const int local = r0 + blk * 16 + n;
-      if (gq == 0 && local < r1 && p.lse)
-        p.lse[int64_t(q0 + local) * p.Hq + row_head[rb]] = (m[rb] + log2f(lt)) * kLn2;
     }
   } else {
     const int nspl = it[2];
@@ -612,42 +670,26 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
     const int64_t slot = int64_t(blockIdx.x) * W + hg;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const float lt = group_sum(l[rb]);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int rowi = (w * RB + rb) * 16 + 4 * gq + r;
-        const float lr = shfl_f(lt, 4 * gq + r);
+        const float mr = shfl_f(m[rb], 4 * gq + r);
+        const float lr = lsum[rb][r];
         if (nspl == 1) {
-          row_values(rb, r, 1.f / lr, p.out + (out_row0 + rowi) * DV);
+          const float inv = 1.f / lr;
+          uint16_t* dst = p.out + (out_row0 + rowi) * DV + n;
+#pragma unroll
+          for (int cv = 0; cv < C::NACC; ++cv)
+            dst[16 * cv] = __builtin_bit_cast(uint16_t, (__bf16)(o[rb][cv][r] * inv));
+          if (n == 0 && p.lse) p.lse[out_row0 + rowi] = (mr + log2f(lr)) * kLn2;
         } else {
-          float* dst = p.ws_o + (slot * rows + rowi) * DV;
-          if constexpr (DV >= 128) {
+          float* dst = p.ws_o + (slot * rows + rowi) * DV + n;
 #pragma unroll
-            for (int vg = 0; vg < C::NVG; ++vg) {
-              f32x4 a0, a1;
-#pragma unroll
-              for (int c = 0; c < 4; ++c) {
-                a0[c] = o[rb][8 * vg + c][r];
-                a1[c] = o[rb][8 * vg + 4 + c][r];
-              }
-              *reinterpret_cast<f32x4*>(dst + 128 * vg + 8 * n) = a0;
-              *reinterpret_cast<f32x4*>(dst + 128 * vg + 8 * n + 4) = a1;
-            }
-          } else {
-            f32x4 a0;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) a0[c] = o[rb][c][r];
-            *reinterpret_cast<f32x4*>(dst + 4 * n) = a0;
+          for (int cv = 0; cv < C::NACC; ++cv) dst[16 * cv] = o[rb][cv][r];
+          if (n == 0) {
+            p.ws_stats[(slot * rows + rowi) * 2] = mr;
+            p.ws_stats[(slot * rows + rowi) * 2 + 1] = lr;
           }
-        }
-      }
-      const int rown = (w * RB + rb) * 16 + n;
-      if (gq == 0) {
-        if (nspl == 1) {
-          if (p.lse) p.lse[out_row0 + rown] = (m[rb] + log2f(lt)) * kLn2;
-        } else {
-          p.ws_stats[(slot * rows + rown) * 2] = m[rb];
-          p.ws_stats[(slot * rows + rown) * 2 + 1] = lt;
         }
       }
     }
@@ -682,10 +724,10 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t words) {
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P>
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS>
 static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stream) {
-  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS>;
-  auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, MODE, P>;
+  using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
+  auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, MODE, P, NS>;
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, int(C::LDS_BYTES));
   if (attr != hipSuccess) return attr;
@@ -706,8 +748,8 @@ static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, dim3 grid, 
     case 128: return p16 ? launch_decode_gqa<128, 16>(p, grid, stream) : launch_decode_gqa<128, 64>(p, grid, stream);
     case 64: return p16 ? launch_decode_gqa<64, 16>(p, grid, stream) : launch_decode_gqa<64, 64>(p, grid, stream);
     case 576:
-      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16>(p, grid, stream)
-                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64>(p, grid, stream);
+      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16, 3>(p, grid, stream)
+                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64, 3>(p, grid, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -730,16 +772,14 @@ hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStrea
 // the group has at most 4 heads, else 8), bm/16 token blocks per wave.
 template <int D, int P>
 static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid, hipStream_t stream) {
+  constexpr int BN = D == 128 ? 32 : 64;
   const bool narrow = p.G <= 4;
-  // 32-key tiles for the widest variant keep its two staged tiles within the
-  // 256 registers that two waves per SIMD allow.
-  constexpr int BN2 = D == 128 ? 32 : 64;
   if (bm == 32)
-    return narrow ? launch_rowpar<D, D, 4, 2, 64, false, kPrefillGrouped, P>(p, grid, stream)
-                  : launch_rowpar<D, D, 8, 2, BN2, false, kPrefillGrouped, P>(p, grid, stream);
+    return narrow ? launch_rowpar<D, D, 4, 2, BN, false, kPrefillGrouped, P, 4>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 2, BN, false, kPrefillGrouped, P, 4>(p, grid, stream);
   if (bm == 16)
-    return narrow ? launch_rowpar<D, D, 4, 1, 64, false, kPrefillGrouped, P>(p, grid, stream)
-                  : launch_rowpar<D, D, 8, 1, 64, false, kPrefillGrouped, P>(p, grid, stream);
+    return narrow ? launch_rowpar<D, D, 4, 1, BN, false, kPrefillGrouped, P, 4>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, 4>(p, grid, stream);
   return hipErrorInvalidValue;
 }
 
@@ -747,7 +787,7 @@ template <int P>
 static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 grid, hipStream_t stream) {
   if (dqk == 128) return launch_prefill_grouped<128, P>(p, bm, grid, stream);
   if (dqk == 64) return launch_prefill_grouped<64, P>(p, bm, grid, stream);
-  if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P>(p, grid, stream);
+  if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   return hipErrorInvalidValue;
 }
 

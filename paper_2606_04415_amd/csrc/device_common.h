@@ -80,6 +80,18 @@ __device__ __forceinline__ u32x2 load8(const uint16_t* p) {
   return *reinterpret_cast<const u32x2*>(p);
 }
 
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane j supplies the LDS
+// address of 4 consecutive bf16; lane i receives element i%4 of the rows that
+// lanes i/4, 4 + i/4, 8 + i/4 and 12 + i/4 addressed. With lane j pointing
+// at row R(j/4), column c + 4*(j%4), lane i gets column c + i of rows
+// R(0..3): a B operand read straight from a row-major (key-major) tile.
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t* lds_addr) {
+  typedef __attribute__((address_space(3))) v4i16* lds_v4i16_ptr;
+  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(lds_addr));
+  return __builtin_bit_cast(u32x2, v);
+}
+
 // Two bf16 halves from two dwords: lo -> (x.lo, y.lo), hi -> (x.hi, y.hi)
 // (one v_perm_b32 each; selector bytes 0-3 pick from x, 4-7 from y).
 __device__ __forceinline__ uint32_t pair_lo(uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x05040100u); }
