@@ -6,14 +6,14 @@
 //                     32-key chunks of the item's key range in turn, streaming
 //                     K and V straight from HBM into registers.
 // rowpar_kernel       prefill phase (all layouts) and decode of the 576/512
-//                     latent layout: each wave owns 16 (or 32) query rows; the
-//                     work-group stages key tiles, gathered through the block
-//                     table, in double-buffered LDS shared by all waves.
-//
-// Both end in the flash-decoding merge when a decode sequence is split:
-// every split writes (max, sum, unnormalised output) to the workspace and the
-// last work-group of the (sequence, column) to arrive combines them in split
-// order, so results are bit-identical run to run (no float atomics).
+//                     latent layout: each wave owns 16 or 32 query rows; the
+//                     work-group streams key tiles, gathered through the block
+//                     table, into a ring of LDS stages shared by all waves.
+// merge_kernel        flash-decoding combine of a split decode sequence: every
+//                     split writes (max, sum, unnormalised output) to the
+//                     workspace; a second launch combines them in split order,
+//                     so results are bit-identical run to run (no float
+//                     atomics).
 #include <math.h>
 
 #include <type_traits>
@@ -124,52 +124,6 @@ __device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int
   }
   l += psum;
   return pop;
-}
-
-// Same step with the row sums kept on the matrix core: `lsum` is an MFMA
-// accumulator (rows 4gq + r, every column holds the row's sum of the bf16
-// probabilities), updated by the caller with P x ones next to P x V, so the
-// denominator uses exactly the probabilities the numerator does. Rescaling
-// treats it like an output accumulator.
-template <int NACC, bool MASK>
-__device__ __forceinline__ u32x4 softmax_chunk_acc(const f32x4 (&s)[2], int kc0, int limit, int gq, float scale_log2,
-                                                   float& m, f32x4& lsum, f32x4 (&o)[NACC]) {
-  float x[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    x[e] = s[e >> 2][e & 3];
-    if constexpr (MASK) x[e] = kc0 + chunk_key(e, gq) < limit ? x[e] : -INFINITY;
-  }
-  float cmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-  cmax = group_max(cmax) * scale_log2;
-  const bool need = cmax > m + kRescaleThreshold;
-  if (wave_any(need)) {
-    const float m_new = need ? cmax : m;
-    const float alpha = fast_exp2(m - m_new);
-    m = m_new;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float ar = shfl_f(alpha, 4 * gq + r);
-      lsum[r] *= ar;
-#pragma unroll
-      for (int a = 0; a < NACC; ++a) o[a][r] *= ar;
-    }
-  }
-  const float neg_m = m == -INFINITY ? 0.f : -m;
-  u32x4 pop;
-#pragma unroll
-  for (int e2 = 0; e2 < 4; ++e2)
-    pop[e2] = pack_bf16x2(fast_exp2(fmaf(x[2 * e2], scale_log2, neg_m)),
-                          fast_exp2(fmaf(x[2 * e2 + 1], scale_log2, neg_m)));
-  return pop;
-}
-
-template <int NACC>
-__device__ __forceinline__ u32x4 softmax_chunk_acc_auto(const f32x4 (&s)[2], int kc0, int limit, int wave_min_limit,
-                                                        int gq, float scale_log2, float& m, f32x4& lsum,
-                                                        f32x4 (&o)[NACC]) {
-  if (kc0 + 32 <= wave_min_limit) return softmax_chunk_acc<NACC, false>(s, kc0, limit, gq, scale_log2, m, lsum, o);
-  return softmax_chunk_acc<NACC, true>(s, kc0, limit, gq, scale_log2, m, lsum, o);
 }
 
 // Masked only when the chunk reaches past the smallest key limit of the wave's
@@ -352,10 +306,10 @@ void decode_gqa_kernel(AttnParams p) {
 // Each wave owns RB blocks of 16 query rows. The work-group streams key tiles
 // of BN keys, gathered through the block table, straight from global memory
 // into a ring of NS LDS stages (global_load_lds_dwordx4: lane i of a wave
-// writes 16 bytes at stage + 16*i, so each instruction fills 1 KB); NS-1 tiles
-// are in flight while one is consumed, and one barrier per tile hands a stage
-// over. Waits on these loads are explicit (vmcnt counts only them inside the
-// loop). Row layouts:
+// writes 16 bytes at stage + 16*i, so each instruction fills 1 KB); up to
+// NS-2 tiles are in flight beyond the one being consumed, and one barrier per
+// tile hands a stage over. Waits on these loads are explicit (vmcnt counts
+// only them inside the loop). Row layouts:
 //   kPrefillGrouped  work-group = (tile of RB*16 tokens, KV head, head chunk);
 //                    wave w = query head, rb = token block: one K/V tile in
 //                    LDS feeds every query head of the KV head.
@@ -367,12 +321,18 @@ void decode_gqa_kernel(AttnParams p) {
 // ---------------------------------------------------------------------------
 enum RowMode { kPrefillGrouped = 0, kPrefillPerHead = 1, kDecodeLatent = 2 };
 
-typedef __attribute__((address_space(3))) void* lds_void_ptr;
-typedef __attribute__((address_space(1))) void* gbl_void_ptr;
+typedef __attribute__((address_space(3))) uint8_t* lds_byte_ptr;
 
-// 16-byte global -> LDS copy per lane; `lds_wave_base` is wave-uniform.
+// 16-byte global -> LDS copy per lane: lane i writes lds_wave_base + 16 i
+// (the LDS address goes in M0 and must be wave-uniform). Written as inline
+// assembly so the compiler's wait insertion does not see an LDS write in
+// flight: it would otherwise drain every outstanding tile load (vmcnt(0))
+// before LDS reads it cannot prove disjoint, such as the transposing reads.
+// Completion is awaited explicitly (wait_vmem) before the barrier that hands
+// a stage to the readers.
 __device__ __forceinline__ void dma16(const void* src, void* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((gbl_void_ptr)(src), (lds_void_ptr)(lds_wave_base), 16, 0, 0);
+  const uint32_t m0 = uint32_t(reinterpret_cast<uintptr_t>((lds_byte_ptr)(lds_wave_base)));
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(__builtin_amdgcn_readfirstlane(m0)) : "memory");
 }
 
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int NS>
@@ -409,10 +369,33 @@ __device__ __forceinline__ int swz_v(int x, int r) {
   else return x ^ (2 * ((r >> 1) & 3));
 }
 
+// vmcnt wait that leaves the loads of the last `ahead` tiles in flight
+// (NI load instructions per tile per wave, at most MAXA tiles ahead).
+template <int NI, int MAXA>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  static_assert(MAXA * NI < 64, "vmcnt range");
+  if constexpr (MAXA >= 4) {
+    if (ahead >= 4) { wait_vmem<4 * NI>(); return; }
+  }
+  if constexpr (MAXA >= 3) {
+    if (ahead == 3) { wait_vmem<3 * NI>(); return; }
+  }
+  if constexpr (MAXA >= 2) {
+    if (ahead == 2) { wait_vmem<2 * NI>(); return; }
+  }
+  if constexpr (MAXA >= 1) {
+    if (ahead == 1) { wait_vmem<NI>(); return; }
+  }
+  wait_vmem<0>();
+}
+
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS>
-__global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW == 8 ? 2 : 1)))
+void rowpar_kernel(AttnParams p) {
   using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
-  static_assert(NS == 3 || NS == 4, "stages");
+  static_assert(NS >= 2 && NS <= 6, "stages");
+  static_assert(BN % 32 == 0, "whole 32-key chunks per tile");
+  static_assert(P % BN == 0 || BN % P == 0, "pages and tiles nest");
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
   int* s_pt = reinterpret_cast<int*>(lds + NS * C::STAGE);
 
@@ -427,7 +410,12 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
   const int nq = p.qsl[seq + 1] - q0;
   const int32_t* bt_row = p.bt + int64_t(seq) * p.bt_stride;
 
-  int key_begin, key_end, head_kv, wave_limit, wave_min_limit;
+  // Per row: query token and head, and the key limit (keys >= limit are
+  // masked). Rows past the tile's end repeat its first row, so they stay
+  // finite and never force masking; their results are not written.
+  // wave_limit: end of the keys any row of the wave sees; wave_full: keys
+  // below it are visible to every row of the wave.
+  int key_begin, key_end, head_kv, wave_limit, wave_full;
   bool wave_on = true;
   int row_tok[RB], row_head[RB], row_limit[RB];
   if constexpr (MODE == kDecodeLatent) {
@@ -441,26 +429,25 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
       row_head[rb] = hg * p.rows_per_wg + (w * RB + rb) * 16 + n;
       row_limit[rb] = key_end;
     }
-    wave_limit = wave_min_limit = key_end;
+    wave_limit = wave_full = key_end;
   } else if constexpr (MODE == kPrefillPerHead) {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
     key_end = it[4];
     const int h = blockIdx.y;
     head_kv = h / p.G;
+    const int wr0 = r0 + w * RB * 16;   // first row of the wave
+    wave_on = wr0 < r1;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int local = r0 + (w * RB + rb) * 16 + n;
-      const bool ok = local < r1;
-      row_tok[rb] = q0 + (ok ? local : r0);
+      const int local = wr0 + rb * 16 + n;
+      const int lr = local < r1 ? local : wr0;
+      row_tok[rb] = q0 + (wave_on ? lr : r0);
       row_head[rb] = h;
-      row_limit[rb] = ok ? (L - nq + local + 1) : 1;
+      row_limit[rb] = L - nq + lr + 1;
     }
-    const int last = min(r1, r0 + (w + 1) * RB * 16) - 1;
-    wave_on = r0 + w * RB * 16 < r1;
-    wave_limit = wave_on ? (L - nq + last + 1) : 0;
-    // rows past r1 see only key 0, so a partial block forces the masked path
-    wave_min_limit = (r0 + (w + 1) * RB * 16 <= r1) ? (L - nq + r0 + w * RB * 16 + 1) : 1;
+    wave_limit = wave_on ? L - nq + min(r1, wr0 + RB * 16) : 0;
+    wave_full = L - nq + wr0 + 1;
   } else {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
@@ -473,18 +460,14 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int local = r0 + rb * 16 + n;
-      const bool ok = local < r1;
-      row_tok[rb] = q0 + (ok ? local : r0);
+      const int lr = local < r1 ? local : r0;
+      row_tok[rb] = q0 + lr;
       row_head[rb] = h;
-      row_limit[rb] = ok ? (L - nq + local + 1) : 1;
+      row_limit[rb] = L - nq + lr + 1;
     }
-    wave_limit = wave_on ? (L - nq + r1) : 0;
-    wave_min_limit = (r0 + RB * 16 <= r1) ? (L - nq + r0 + 1) : 1;
+    wave_limit = wave_on ? L - nq + r1 : 0;
+    wave_full = L - nq + r0 + 1;
   }
-  const uint16_t* kbase = p.kc.base + int64_t(head_kv) * p.kc.sh;
-  const uint16_t* vbase = (VALIAS ? p.kc.base : p.vc.base) + int64_t(head_kv) * (VALIAS ? p.kc.sh : p.vc.sh);
-  const int64_t ksp = p.kc.sp, kss = p.kc.ss;
-  const int64_t vsp = VALIAS ? p.kc.sp : p.vc.sp, vss = VALIAS ? p.kc.ss : p.vc.ss;
 
   // Q as the B operand of S^T = K Q^T.
   u32x4 qop[RB][C::DC];
@@ -506,102 +489,231 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
   }
   const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 x 8
 
-  // Issue this wave's share of the loads of key tile kb into stage st. Every
-  // lane always issues (keys past key_end read the last key's row, padding
-  // slots read a dummy row); those keys are masked to probability 0.
-  auto issue = [&](int kb, int st, int pt_base) {
-    uint8_t* sbase = lds + st * C::STAGE;
-    const int klast = key_end - 1;
-#pragma unroll
-    for (int j = 0; j < C::NI; ++j) {
-      const int blk = w * C::NI + j;
-      const int s = blk * 64 + lane;
-      int row = 0, x = 0;
-      bool isv = false;
+  // Gather addressing. Load instruction j of this wave fills 1 KB of a stage:
+  // lane slot s = 64 * (w * NI + j) + lane is one 16-byte chunk of a K row
+  // (s < K_SLOTS) or of a V row. Byte offsets split into a per-lane part fixed
+  // for the whole launch and a per-tile part: a tile starts on a multiple of
+  // BN keys, so in a tile that lies below key_end the slot of row r within its
+  // page is r % P (pages of at most BN keys) or kb % P + r (larger pages).
+  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(head_kv) * p.kc.sh);
+  const uint8_t* vbase =
+      reinterpret_cast<const uint8_t*>((VALIAS ? p.kc.base : p.vc.base) + int64_t(head_kv) * (VALIAS ? p.kc.sh : p.vc.sh));
+  const uint32_t ksp = uint32_t(p.kc.sp) * 2u, kss = uint32_t(p.kc.ss) * 2u;
+  const uint32_t vsp = uint32_t(VALIAS ? p.kc.sp : p.vc.sp) * 2u, vss = uint32_t(VALIAS ? p.kc.ss : p.vc.ss) * 2u;
+  // Row and byte offset within the row of the chunk lane slot s loads.
+  auto slot_of = [&](int j, int& row, uint32_t& xoff) {
+    const int blk = w * C::NI + j;
+    const int s = blk * 64 + lane;
+    int x = 0;
+    row = 0;
+    if (VALIAS || blk * 64 < C::K_SLOTS) {   // wave-uniform
       if (s < C::K_SLOTS) {
         row = s / C::ROWB;
         const int pc = s % C::ROWB;
         x = pc < C::CPR ? swz_k<DQK, VALIAS>(pc, row) : 0;
-      } else if (s < C::SLOTS) {
-        isv = true;
-        const int s2 = s - C::K_SLOTS;
-        row = s2 / (C::CPRV > 0 ? C::CPRV : 1);
-        x = swz_v<DV>(s2 % (C::CPRV > 0 ? C::CPRV : 1), row);
       }
-      const int key = min(kb + row, klast);
-      const int64_t page = s_pt[key / P - pt_base];
-      const uint16_t* src = isv ? vbase + page * vsp + int64_t(key % P) * vss
-                                : kbase + page * ksp + int64_t(key % P) * kss;
-      dma16(src + 8 * x, sbase + blk * 1024);
+    } else if (s < C::SLOTS) {
+      const int s2 = s - C::K_SLOTS;
+      row = s2 / (C::CPRV > 0 ? C::CPRV : 1);
+      x = swz_v<DV>(s2 % (C::CPRV > 0 ? C::CPRV : 1), row);
+    }
+    xoff = 16u * uint32_t(x);
+  };
+  // Page of a slot within its tile (pages of at most BN keys): per lane for
+  // the padded latent rows; for unpadded rows one load instruction covers
+  // 64 / CPR whole rows of one page, so it is wave-uniform.
+  auto tile_page = [&](int j, int row) {
+    if constexpr (P > BN) return 0;
+    if constexpr (VALIAS) return row / P;
+    const int blk = w * C::NI + j;
+    const int row0 = blk * 64 < C::K_SLOTS ? blk * 64 / C::CPR : (blk * 64 - C::K_SLOTS) / (C::CPRV > 0 ? C::CPRV : 1);
+    return __builtin_amdgcn_readfirstlane(row0 / P);
+  };
+  static_assert(VALIAS || (64 % C::CPR == 0 && P % (64 / C::CPR) == 0), "a load instruction stays in one page");
+  uint32_t ld_lane_off[C::NI];
+#pragma unroll
+  for (int j = 0; j < C::NI; ++j) {
+    const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
+    int row;
+    uint32_t xoff;
+    slot_of(j, row, xoff);
+    ld_lane_off[j] = (P <= BN ? uint32_t(row % P) : uint32_t(row)) * (isv ? vss : kss) + xoff;
+  }
+
+  // Issue this wave's loads of the key tile starting at kb into stage st.
+  // Keys past key_end read the last key's row (masked later); padding slots
+  // read a dummy row.
+  auto issue = [&](int kb, int st, int pt_base) {
+    uint8_t* sbase = lds + st * C::STAGE;
+    const bool whole = kb + BN <= key_end;
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
+      const uint8_t* base = isv ? vbase : kbase;
+      const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
+      int pidx;
+      uint32_t off;
+      if (whole) {
+        int row = 0;
+        if constexpr (VALIAS && P <= BN) {
+          uint32_t xoff;
+          slot_of(j, row, xoff);
+        }
+        pidx = kb / P - pt_base + tile_page(j, row);
+        off = P <= BN ? ld_lane_off[j] : ld_lane_off[j] + uint32_t(kb % P) * ss;
+      } else {
+        int row;
+        uint32_t xoff;
+        slot_of(j, row, xoff);
+        const uint32_t key = uint32_t(min(kb + row, key_end - 1));
+        pidx = int(key / P) - pt_base;
+        off = (key % P) * ss + xoff;
+      }
+      const uint32_t page = uint32_t(s_pt[pidx]);
+      dma16(base + (uint64_t(page) * sp + off), sbase + (w * C::NI + j) * 1024);
     }
   };
 
-  auto compute_tile = [&](int kb, int st) {
-    const uint8_t* Kst = lds + st * C::STAGE;
-    const uint8_t* Vst = VALIAS ? Kst : Kst + C::V_OFF;
+  // Per-lane LDS byte offsets of the MFMA operand reads within a stage. The
+  // row swizzles depend only on the row modulo 16 (K) or 8 (V), so they are
+  // the same for every 32-key chunk and 16-key block of a tile: chunk, block
+  // and stage enter as immediate offsets.
+  constexpr int CH = BN / 32;                      // 32-key chunks per tile
+  constexpr int KROW = C::ROWB * 16;               // LDS bytes per K row
+  constexpr int VROW = VALIAS ? KROW : C::CPRV * 16;
+  constexpr int NKO = VALIAS ? 1 : C::DC, NVO = VALIAS ? 1 : C::NACC;
+  const int rowa0 = 4 * gq + (n >> 2);             // V row of the lane's first 4 keys
+  const int cb = 8 * (n & 3);                      // byte offset of its 4 columns in a 32-byte block
+  uint32_t k_off[NKO], v_off[NVO];
+  if constexpr (VALIAS) {
+    k_off[0] = uint32_t(n * KROW + 16 * gq);
+    v_off[0] = uint32_t(rowa0 * VROW + cb);
+  } else {
 #pragma unroll
-    for (int ch = 0; ch < BN / 32; ++ch) {
-      const int kc0 = kb + 32 * ch;
-      if (kc0 >= wave_limit) break;
-      f32x4 s[RB][2];
+    for (int c = 0; c < C::DC; ++c) k_off[c] = uint32_t(n * KROW + 16 * swz_k<DQK, VALIAS>(4 * c + gq, n));
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-      auto kaddr = [&](int b, int c) {
-        const int row = 32 * ch + 16 * b + n;
-        return Kst + row * C::ROWB * 16 + 16 * swz_k<DQK, VALIAS>(4 * c + gq, row);
-      };
+    for (int cv = 0; cv < C::NACC; ++cv) {
+      const int x = 2 * cv + (cb >> 4);
+      v_off[cv] = uint32_t(C::V_OFF + rowa0 * VROW + 16 * swz_v<DV>(x, rowa0) + (cb & 15));
+    }
+  }
+  // Stage base (wave-uniform) + per-lane offset + an immediate; pointer
+  // arithmetic so the constant part folds into the instruction's offset.
+  auto kread = [&](const uint8_t* stage, int ch, int b, int c) {
+    const uint8_t* base = stage + (VALIAS ? k_off[0] : k_off[c]);
+    return *reinterpret_cast<const u32x4*>(base + ((32 * ch + 16 * b) * KROW + (VALIAS ? 64 * c : 0)));
+  };
+  auto vread = [&](const uint8_t* stage, int ch, int half, int cv) {
+    const uint8_t* base = stage + (VALIAS ? v_off[0] : v_off[cv]);
+    return lds_read_tr16(
+        reinterpret_cast<const uint16_t*>(base + ((32 * ch + 16 * half) * VROW + (VALIAS ? 32 * cv : 0))));
+  };
+
+  // One key tile: S^T = K Q^T per 32-key chunk, masking (only when the tile
+  // crosses a row limit), the tile max of each row, lazy rescale, then
+  // probabilities and O += P V, l += P 1 per chunk. (One instance per loop:
+  // a masked and an unmasked copy in one loop body would be merged by the
+  // compiler at a large register cost.)
+  auto compute_tile = [&](bool masked, int st, int kc0) {
+    const uint8_t* stage = lds + __builtin_amdgcn_readfirstlane(st * C::STAGE);
+    f32x4 s[RB][2 * CH];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 2 * CH; ++i) s[rb][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ch = 0; ch < CH; ++ch) {
       if constexpr (C::DC <= 4) {
-        // All K operands of the chunk first, then 2*RB independent accumulator
-        // chains interleaved, so neither LDS latency nor MFMA dependencies stall.
         u32x4 kop[2][C::DC];
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
-          for (int c = 0; c < C::DC; ++c) kop[b][c] = *reinterpret_cast<const u32x4*>(kaddr(b, c));
+          for (int c = 0; c < C::DC; ++c) kop[b][c] = kread(stage, ch, b, c);
 #pragma unroll
         for (int c = 0; c < C::DC; ++c)
 #pragma unroll
           for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) s[rb][b] = mfma_16x16x32(kop[b][c], qop[rb][c], s[rb][b]);
+            for (int rb = 0; rb < RB; ++rb) s[rb][2 * ch + b] = mfma_16x16x32(kop[b][c], qop[rb][c], s[rb][2 * ch + b]);
       } else {
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int c = 0; c < C::DC; ++c) {
-            const u32x4 kop = *reinterpret_cast<const u32x4*>(kaddr(b, c));
+            const u32x4 kop = kread(stage, ch, b, c);
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) s[rb][b] = mfma_16x16x32(kop, qop[rb][c], s[rb][b]);
+            for (int rb = 0; rb < RB; ++rb) s[rb][2 * ch + b] = mfma_16x16x32(kop, qop[rb][c], s[rb][2 * ch + b]);
           }
       }
+      // Keep each chunk's operand reads next to its products: hoisting every
+      // read of the tile to the top would cost a register per value.
+      __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // s[rb][2ch + b][r] is the score of key kc0 + 32ch + 16b + 4gq + r for row n.
+    float cmax[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      if (masked) {
+#pragma unroll
+        for (int i = 0; i < 2 * CH; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            s[rb][i][r] = kc0 + 16 * i + 4 * gq + r < row_limit[rb] ? s[rb][i][r] : -INFINITY;
+      }
+      float mx = fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3]));
+#pragma unroll
+      for (int i = 1; i < 2 * CH; ++i)
+        mx = fmaxf(mx, fmaxf(fmaxf(s[rb][i][0], s[rb][i][1]), fmaxf(s[rb][i][2], s[rb][i][3])));
+      cmax[rb] = group_max(mx) * p.scale_log2;
+    }
+
+    // Lazy rescale: a row's max moves only when the tile max exceeds it by
+    // more than the threshold; then its accumulators and sum scale by 2^(m-m').
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const bool need = cmax[rb] > m[rb] + kRescaleThreshold;
+      if (wave_any(need)) {
+        const float m_new = need ? cmax[rb] : m[rb];
+        const float alpha = fast_exp2(m[rb] - m_new);   // 1 if unchanged, 0 from -inf
+        m[rb] = m_new;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float ar = shfl_f(alpha, 4 * gq + r);
+          lsum[rb][r] *= ar;
+#pragma unroll
+          for (int a = 0; a < C::NACC; ++a) o[rb][a][r] *= ar;
+        }
+      }
+    }
+
+#pragma unroll
+    for (int ch = 0; ch < CH; ++ch) {
+      // Probabilities 2^(s * scale_log2 - m) as the bf16 A operand of P x V.
       u32x4 pop[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        pop[rb] = softmax_chunk_acc_auto<C::NACC>(s[rb], kc0, row_limit[rb], wave_min_limit, gq, p.scale_log2,
-                                                  m[rb], lsum[rb], o[rb]);
+        const float neg_m = m[rb] == -INFINITY ? 0.f : -m[rb];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const f32x4& sb = s[rb][2 * ch + (e2 >> 1)];
+          const int r = 2 * (e2 & 1);
+          pop[rb][e2] = pack_bf16x2(fast_exp2(fmaf(sb[r], p.scale_log2, neg_m)),
+                                    fast_exp2(fmaf(sb[r + 1], p.scale_log2, neg_m)));
+        }
         lsum[rb] = mfma_16x16x32(pop[rb], ones, lsum[rb]);
       }
-      // PV: transposing LDS reads give each lane its 8 keys of value column
-      // 16*cv + n (rows 4*gq + e and 16 + 4*gq + e of the chunk).
-      const int rowa = 32 * ch + 4 * gq + (n >> 2), rowb = rowa + 16;
-      const int cb = 8 * (n & 3);   // byte offset of the lane's 4 columns within a 32-byte column block
+      // Transposing LDS reads give each lane its 8 keys of value column
+      // 16cv + n (keys 4gq + e and 16 + 4gq + e of the chunk).
 #pragma unroll
       for (int cv = 0; cv < C::NACC; ++cv) {
-        const uint8_t *va, *vb;
-        if constexpr (VALIAS) {
-          va = Vst + rowa * C::ROWB * 16 + 32 * cv + cb;
-          vb = Vst + rowb * C::ROWB * 16 + 32 * cv + cb;
-        } else {
-          const int x = 2 * cv + (cb >> 4), off = cb & 15;
-          va = Vst + rowa * C::CPRV * 16 + 16 * swz_v<DV>(x, rowa) + off;
-          vb = Vst + rowb * C::CPRV * 16 + 16 * swz_v<DV>(x, rowb) + off;
-        }
-        const u32x2 lo = lds_read_tr16(reinterpret_cast<const uint16_t*>(va));
-        const u32x2 hi = lds_read_tr16(reinterpret_cast<const uint16_t*>(vb));
+        const u32x2 lo = vread(stage, ch, 0, cv);
+        const u32x2 hi = vread(stage, ch, 1, cv);
         const u32x4 vop = {lo[0], lo[1], hi[0], hi[1]};
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) o[rb][cv] = mfma_16x16x32(pop[rb], vop, o[rb][cv]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -610,6 +722,10 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
 
   // Windows of kPageWin block-table entries; the tile pipeline drains at the
   // end of each window (one window covers the whole range in the usual case).
+  // Iteration kt waits for tile kt, passes one barrier (every wave is done
+  // with tile kt - 1, so its stage takes tile kt + NS - 1) and computes.
+  // Tiles that no row of the wave masks and that still have a tile to issue
+  // after them run in a loop with fixed wait counts and no masking.
   constexpr int WIN_KEYS = kPageWin * P;
   static_assert(WIN_KEYS % BN == 0, "windows hold whole tiles");
   const int last_page = key_end > 0 ? (key_end - 1) / P : 0;
@@ -627,14 +743,22 @@ __global__ __launch_bounds__(NW * 64) void rowpar_kernel(AttnParams p) {
 #pragma unroll
     for (int t = 0; t < NS - 1; ++t)
       if (t < ntiles) issue(wk0 + t * BN, t, pt_base);
-    for (int kt = 0; kt < ntiles; ++kt) {
-      const int ahead = min(NS - 2, ntiles - 1 - kt);   // tiles issued after tile kt
-      if (NS == 4 && ahead >= 2) wait_vmem<(NS - 2) * C::NI>();
-      else if (ahead >= 1) wait_vmem<C::NI>();
-      else wait_vmem<0>();
-      lds_barrier();   // tile kt is in LDS for every wave; stage (kt - 1) % NS is free
+
+    const int n_steady = wave_on ? max(0, min(max(0, wave_full - wk0) / BN, ntiles - (NS - 1))) : 0;
+    int kt = 0;
+    for (; kt < n_steady; ++kt) {
+      wait_vmem<(NS - 2) * C::NI>();
+      lds_barrier();
+      issue(wk0 + (kt + NS - 1) * BN, (kt + NS - 1) % NS, pt_base);
+      compute_tile(false, kt % NS, wk0 + kt * BN);
+    }
+    for (; kt < ntiles; ++kt) {
+      const int kc = wk0 + kt * BN;
+      wait_tiles<C::NI, NS - 2>(min(NS - 2, ntiles - 1 - kt));
+      lds_barrier();
       if (kt + NS - 1 < ntiles) issue(wk0 + (kt + NS - 1) * BN, (kt + NS - 1) % NS, pt_base);
-      compute_tile(wk0 + kt * BN, kt % NS);
+      if (!wave_on || kc >= wave_limit) continue;   // past this wave's rows: loads and barriers only
+      compute_tile(kc + BN > wave_full, kt % NS, kc);
     }
   }
 
@@ -772,14 +896,15 @@ hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStrea
 // the group has at most 4 heads, else 8), bm/16 token blocks per wave.
 template <int D, int P>
 static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid, hipStream_t stream) {
-  constexpr int BN = D == 128 ? 32 : 64;
+  constexpr int BN = 64;
+  constexpr int NS = D == 128 ? 3 : 4;
   const bool narrow = p.G <= 4;
   if (bm == 32)
-    return narrow ? launch_rowpar<D, D, 4, 2, BN, false, kPrefillGrouped, P, 4>(p, grid, stream)
-                  : launch_rowpar<D, D, 8, 2, BN, false, kPrefillGrouped, P, 4>(p, grid, stream);
+    return narrow ? launch_rowpar<D, D, 4, 2, BN, false, kPrefillGrouped, P, NS>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 2, BN, false, kPrefillGrouped, P, NS>(p, grid, stream);
   if (bm == 16)
-    return narrow ? launch_rowpar<D, D, 4, 1, BN, false, kPrefillGrouped, P, 4>(p, grid, stream)
-                  : launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, 4>(p, grid, stream);
+    return narrow ? launch_rowpar<D, D, 4, 1, BN, false, kPrefillGrouped, P, NS>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, NS>(p, grid, stream);
   return hipErrorInvalidValue;
 }
 

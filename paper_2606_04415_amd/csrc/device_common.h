@@ -53,10 +53,10 @@ __device__ __forceinline__ void lds_barrier() {
 __device__ __forceinline__ void wait_vmem_all() { wait_vmem<0>(); }
 
 // Pack two floats into two bf16 (round to nearest even) in one dword, lo first.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo;
-  const __bf16 b = (__bf16)hi;
-  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Element offset of (page, slot, head) in a paged cache with element strides.

@@ -5,7 +5,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/flexattn.h"
+#include "flexattn.h"
 
 namespace flexattn {
 
