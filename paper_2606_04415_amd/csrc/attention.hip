@@ -310,9 +310,10 @@ void decode_gqa_kernel(AttnParams p) {
 // NS-2 tiles are in flight beyond the one being consumed, and one barrier per
 // tile hands a stage over. Waits on these loads are explicit (vmcnt counts
 // only them inside the loop). Row layouts:
-//   kPrefillGrouped  work-group = (tile of RB*16 tokens, KV head, head chunk);
-//                    wave w = query head, rb = token block: one K/V tile in
-//                    LDS feeds every query head of the KV head.
+//   kPrefillGrouped  work-group = (tile of TB*RB*16 tokens, KV head, head
+//                    chunk); wave w = query head w / TB, token blocks
+//                    (w % TB) * RB + rb: one K/V tile in LDS feeds every
+//                    query head of the KV head.
 //   kPrefillPerHead  work-group = (tile of NW*RB*16 tokens, query head).
 //   kDecodeLatent    work-group = (decode item, group of NW*RB*16 heads).
 // LDS rows: grouped-query K/V rows are unpadded and XOR-swizzled by 16-byte
@@ -389,8 +390,8 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   wait_vmem<0>();
 }
 
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW == 8 ? 2 : 1)))
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)))
 void rowpar_kernel(AttnParams p) {
   using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
   static_assert(NS >= 2 && NS <= 6, "stages");
@@ -452,21 +453,24 @@ void rowpar_kernel(AttnParams p) {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
     key_end = it[4];
-    const int chunks = (p.G + NW - 1) / NW;
+    constexpr int HPW = NW / TB;                       // query heads per work-group
+    const int chunks = (p.G + HPW - 1) / HPW;
     head_kv = blockIdx.y / chunks;
-    const int hl = (blockIdx.y % chunks) * NW + w;     // query head within the group
-    wave_on = hl < p.G;
-    const int h = head_kv * p.G + (wave_on ? hl : 0);
+    const int hl = (blockIdx.y % chunks) * HPW + w / TB;   // query head within the group
+    const int wr0 = r0 + (w % TB) * RB * 16;               // first row of the wave
+    wave_on = hl < p.G && wr0 < r1;
+    const int h = head_kv * p.G + (hl < p.G ? hl : 0);
+    const int rfirst = wr0 < r1 ? wr0 : r0;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int local = r0 + rb * 16 + n;
-      const int lr = local < r1 ? local : r0;
+      const int local = rfirst + rb * 16 + n;
+      const int lr = local < r1 ? local : rfirst;
       row_tok[rb] = q0 + lr;
       row_head[rb] = h;
       row_limit[rb] = L - nq + lr + 1;
     }
-    wave_limit = wave_on ? L - nq + r1 : 0;
-    wave_full = L - nq + r0 + 1;
+    wave_limit = wave_on ? L - nq + min(r1, wr0 + RB * 16) : 0;
+    wave_full = L - nq + rfirst + 1;
   }
 
   // Q as the B operand of S^T = K Q^T.
@@ -769,7 +773,7 @@ void rowpar_kernel(AttnParams p) {
     const int r0 = it[2], r1 = it[3];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int blk = MODE == kPrefillPerHead ? (w * RB + rb) : rb;
+      const int blk = MODE == kPrefillPerHead ? (w * RB + rb) : ((w % TB) * RB + rb);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int local = r0 + blk * 16 + 4 * gq + r;
@@ -848,10 +852,10 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t words) {
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
-template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS>
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB = 1>
 static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stream) {
   using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
-  auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, MODE, P, NS>;
+  auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, MODE, P, NS, TB>;
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, int(C::LDS_BYTES));
   if (attr != hipSuccess) return attr;
@@ -900,8 +904,8 @@ static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid,
   constexpr int NS = D == 128 ? 3 : 4;
   const bool narrow = p.G <= 4;
   if (bm == 32)
-    return narrow ? launch_rowpar<D, D, 4, 2, BN, false, kPrefillGrouped, P, NS>(p, grid, stream)
-                  : launch_rowpar<D, D, 8, 2, BN, false, kPrefillGrouped, P, NS>(p, grid, stream);
+    return narrow ? launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, NS, 2>(p, grid, stream)
+                  : launch_rowpar<D, D, 16, 1, BN, false, kPrefillGrouped, P, NS, 2>(p, grid, stream);
   if (bm == 16)
     return narrow ? launch_rowpar<D, D, 4, 1, BN, false, kPrefillGrouped, P, NS>(p, grid, stream)
                   : launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, NS>(p, grid, stream);
