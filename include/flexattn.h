@@ -116,6 +116,9 @@ typedef struct flex_attn_plan_info {
  *           page*k_stride[0] + slot*k_stride[1] + kv_head*k_stride[2] + d.
  *  v_cache  same with v_stride and d < d_v; ignored (may be NULL) when the
  *           shape has v_aliases_k.
+ *           For both caches the page stride and page_size * slot stride must
+ *           each stay below 2^31 bytes (kernels address within a page with
+ *           32-bit offsets); larger strides are FLEX_ERR_INVALID_ARG.
  *  block_table int32 [B, >= max_pages_per_seq], row stride block_table_stride;
  *           entries 0 .. ceil(L_s / P) - 1 of row s must lie in [0, num_pages).
  *  seq_lens int32 [B], query_start_loc int32 [B+1]: the same values the plan

@@ -18,8 +18,10 @@ the contract is:
   pps = max(min_pps, ceil(W * sum_s P_s / (cus_decode * wg_per_cu)));
   n_s = ceil(P_s / pps); if n_s > max_splits then pps_s = ceil(P_s / max_splits),
   n_s = ceil(P_s / pps_s), else pps_s = pps; split j covers keys
-  [j * pps_s * P, min(L_s, (j + 1) * pps_s * P)). Items: decode sequences in
-  batch order, splits ascending.
+  [j * pps_s * P, min(L_s, (j + 1) * pps_s * P)). Workspace slots number the
+  splits in batch order (splits of a sequence consecutive); items are listed
+  in launch order: key count descending, ties by slot. Item words:
+  [s, j, n_s, k0, k1, slot of split 0, decode ordinal, slot].
 * prefill tiles of BM rows (BM 32 by default for grouped-query heads, 64 for
   the latent layout): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
   ordered by key_end descending, then sequence, then tile. Each tile is served
@@ -39,7 +41,7 @@ from typing import List, Optional, Sequence
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
 MAGIC = 0x46504C58
-VERSION = 1
+VERSION = 2
 HEADER = 16
 ITEM = 8
 
@@ -182,12 +184,13 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         if nspl > max_splits:
             pps_s = cdiv(Ps, max_splits)
             nspl = cdiv(Ps, pps_s)
-        first = len(dec_items)
+        slot0 = len(dec_items)
         n_split += nspl > 1
         for j in range(nspl):
             k0 = j * pps_s * P
             k1 = min(seq_lens[s], (j + 1) * pps_s * P)
-            dec_items.append([s, j, nspl, k0, k1, first, d, 0])
+            dec_items.append([s, j, nspl, k0, k1, slot0, d, slot0 + j])
+    dec_items.sort(key=lambda it: (-(it[4] - it[3]), it[7]))
 
     # --- prefill tiles, longest key range first
     tiles = []

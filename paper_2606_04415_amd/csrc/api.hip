@@ -63,6 +63,11 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
     if (a->k_stride[i] <= 0 || vs[i] <= 0 || (a->k_stride[i] * 2) % 16 || (vs[i] * 2) % 16)
       return set_error(FLEX_ERR_INVALID_ARG, "cache strides must be positive multiples of 16 bytes");
   }
+  // Within a page the kernels use 32-bit byte offsets.
+  const int64_t lim = int64_t(1) << 31;
+  if (a->k_stride[0] * 2 >= lim || vs[0] * 2 >= lim || a->k_stride[1] * 2 * sh.page_size >= lim ||
+      vs[1] * 2 * sh.page_size >= lim)
+    return set_error(FLEX_ERR_INVALID_ARG, "cache page stride or page_size * slot stride reaches 2^31 bytes");
   if (a->k_stride[2] < sh.head_dim_qk || vs[2] < (sh.v_aliases_k ? sh.head_dim_qk : sh.head_dim_v))
     return set_error(FLEX_ERR_INVALID_ARG, "cache head stride smaller than the head dimension");
   if (a->num_pages <= 0) return set_error(FLEX_ERR_INVALID_ARG, "num_pages must be positive");

@@ -36,7 +36,7 @@ template <int DV>
 __global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
   const int32_t* it = p.items + 8 * blockIdx.x;
   if (it[1] != 0 || it[2] <= 1) return;
-  const int first = blockIdx.x, nspl = it[2];
+  const int slot0 = it[5], nspl = it[2];   // workspace slots slot0 .. slot0 + nspl - 1
   const int col = blockIdx.y, W = gridDim.y, rows = p.rows_per_wg;
   const int64_t out_row0 = int64_t(p.qsl[it[0]]) * p.Hq + int64_t(col) * rows;
   for (int idx = threadIdx.x; idx < rows * (DV / 4); idx += blockDim.x) {
@@ -44,13 +44,13 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
     const int d = 4 * (idx % (DV / 4));
     float M = -INFINITY;
     for (int j = 0; j < nspl; ++j) {
-      const int64_t slot = int64_t(first + j) * W + col;
+      const int64_t slot = int64_t(slot0 + j) * W + col;
       M = fmaxf(M, p.ws_stats[(slot * rows + i) * 2]);
     }
     float den = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < nspl; ++j) {
-      const int64_t slot = int64_t(first + j) * W + col;
+      const int64_t slot = int64_t(slot0 + j) * W + col;
       const float mj = p.ws_stats[(slot * rows + i) * 2];
       const float f = mj == -INFINITY ? 0.f : exp2f(mj - M);
       den += f * p.ws_stats[(slot * rows + i) * 2 + 1];
@@ -170,9 +170,14 @@ void decode_gqa_kernel(AttnParams p) {
   const int tok = p.qsl[seq];
   const int32_t* bt_row = p.bt + int64_t(seq) * p.bt_stride;
   const int G = p.G;
-  const uint16_t* kbase = p.kc.base + int64_t(g) * p.kc.sh + 8 * gq;
-  const uint16_t* vbase = p.vc.base + int64_t(g) * p.vc.sh + DPL * n;
-  const int64_t ksp = p.kc.sp, kss = p.kc.ss, vsp = p.vc.sp, vss = p.vc.ss;
+  // Byte strides (the host checks that a page's slots span less than 2^31
+  // bytes) and per-lane byte offsets of a chunk's loads from the page bases.
+  const uint8_t* kbase_b = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(g) * p.kc.sh);
+  const uint8_t* vbase_b = reinterpret_cast<const uint8_t*>(p.vc.base + int64_t(g) * p.vc.sh);
+  const uint32_t ksp_b = uint32_t(p.kc.sp) * 2u, kss_b = uint32_t(p.kc.ss) * 2u;
+  const uint32_t vsp_b = uint32_t(p.vc.sp) * 2u, vss_b = uint32_t(p.vc.ss) * 2u;
+  const uint32_t k_lane = uint32_t(n) * kss_b + 16u * gq;
+  const uint32_t v_lane = uint32_t(4 * gq) * vss_b + 2u * DPL * n;
   __shared__ int s_pt[kPageWin];
 
   // Q as the B operand of S^T = K Q^T: column n = query head g*G + n.
@@ -201,26 +206,40 @@ void decode_gqa_kernel(AttnParams p) {
 
     // Every lane always issues its loads, so the number of loads in flight is
     // fixed and the wait before a chunk's math covers exactly that chunk. Keys
-    // past the window read its last key's (finite) row instead; the softmax
-    // masks them to probability 0.
+    // past the window read zeros; the softmax masks them to probability 0.
     auto load = [&](Chunk& c, int ci) {
       const int kc0 = wk0 + 32 * ci;
       const int klast = wk1 - 1;
-      const int page0 = s_pt[min(kc0, klast) / P - pg0];
-      const int page1 = s_pt[min(kc0 + 16, klast) / P - pg0];
+      // Page bases and valid ranges of the chunk's two 16-key halves
+      // (wave-uniform): a buffer resource per half whose record count ends at
+      // the last key of the range, so loads past it read zeros and never
+      // touch memory; offsets within a half are per-lane constants.
+      __amdgpu_buffer_rsrc_t kr[2], vr[2];
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        const int key = kc0 + 16 * b + n;
-        const uint16_t* kr = kbase + int64_t(b ? page1 : page0) * ksp + int64_t(min(key, klast) % P) * kss;
-#pragma unroll
-        for (int cc = 0; cc < DC; ++cc) c.k[b][cc] = load16(kr + 32 * cc);
+        const int key = kc0 + 16 * b;
+        // (readfirstlane keeps the record counts in scalar registers: a
+        // resource the compiler sees in vector registers becomes a loop.)
+        const uint32_t nvalid = uint32_t(__builtin_amdgcn_readfirstlane(min(max(wk1 - key, 0), 16)));
+        const uint32_t pg = uint32_t(__builtin_amdgcn_readfirstlane(s_pt[min(key, klast) / P - pg0]));
+        const uint32_t slot = uint32_t(key % P);
+        kr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(kbase_b + (uint64_t(pg) * ksp_b + slot * kss_b)),
+                                                  0, __builtin_amdgcn_readfirstlane(int(nvalid * kss_b)), kBufferFlags);
+        vr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(vbase_b + (uint64_t(pg) * vsp_b + slot * vss_b)),
+                                                  0, __builtin_amdgcn_readfirstlane(int(nvalid * vss_b)), kBufferFlags);
       }
 #pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int cc = 0; cc < DC; ++cc)
+          c.k[b][cc] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr[b], int(k_lane + 64u * cc), 0, 0));
+#pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int key = kc0 + chunk_key(e, gq);
-        const uint16_t* vr = vbase + int64_t((e >> 2) ? page1 : page0) * vsp + int64_t(min(key, klast) % P) * vss;
-        if constexpr (D == 128) c.v[e] = load16(vr);
-        else c.v[e] = load8(vr);
+        const int off = int(v_lane + uint32_t(e & 3) * vss_b);
+        if constexpr (D == 128)
+          c.v[e] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr[e >> 2], off, 0, 0));
+        else
+          c.v[e] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(vr[e >> 2], off, 0, 0));
       }
     };
 
@@ -272,7 +291,7 @@ void decode_gqa_kernel(AttnParams p) {
 
   const bool single = nspl == 1;
   const int64_t out_row0 = int64_t(tok) * p.Hq + int64_t(g) * G;
-  const int64_t slot = int64_t(item) * W + g;
+  const int64_t slot = int64_t(it[7]) * W + g;   // this split's workspace slot
   for (int idx = tid; idx < G * (D / 2); idx += NW * 64) {
     const int i = idx / (D / 2), d = 2 * (idx % (D / 2));
     float M = s_m[0][i];
@@ -795,7 +814,7 @@ void rowpar_kernel(AttnParams p) {
     const int W = gridDim.y;
     const int rows = p.rows_per_wg;
     const int64_t out_row0 = int64_t(q0) * p.Hq + int64_t(hg) * rows;
-    const int64_t slot = int64_t(blockIdx.x) * W + hg;
+    const int64_t slot = int64_t(it[7]) * W + hg;   // this split's workspace slot
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
 #pragma unroll

@@ -59,6 +59,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
+// Word 3 of a raw (unswizzled, stride 0) buffer resource on gfx9: 32-bit
+// data format, so out-of-range dword loads return zero.
+constexpr int kBufferFlags = 0x00020000;
+
 // Element offset of (page, slot, head) in a paged cache with element strides.
 struct PagedCache {
   const uint16_t* base;

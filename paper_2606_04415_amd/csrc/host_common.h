@@ -12,7 +12,7 @@ namespace flexattn {
 // Plan word layout: a 16-word header, then 8 words per decode item, then 8
 // words per prefill item.
 constexpr int32_t kPlanMagic = 0x46504C58;
-constexpr int32_t kPlanVersion = 1;
+constexpr int32_t kPlanVersion = 2;
 constexpr int kHeaderWords = 16;
 constexpr int kItemWords = 8;
 
@@ -22,8 +22,10 @@ enum HeaderField {
   H_CUS_PRE, H_BM, H_TOTAL_WORDS
 };
 
-// Decode item words: seq, split, n_splits, key_begin, key_end, first item of
-// the sequence, decode-sequence ordinal, unused.
+// Decode item words: seq, split, n_splits, key_begin, key_end, workspace slot
+// of the sequence's split 0, decode-sequence ordinal, this item's workspace
+// slot. Items are in launch order (longest key range first); slots are in
+// batch order, so split j of a sequence sits at slot 0 + j.
 // Prefill item words: seq, tile, row_begin, row_end, key_end, unused x3.
 
 // Rows (query heads) one decode work-group owns in the 576/512 layout.

@@ -168,7 +168,12 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   int64_t total_pages = 0;
   for (int32_t s : dec) total_pages += cdiv(seq_lens[s], P);
   const int64_t pps = dec.empty() ? 0 : std::max(min_pps, cdiv(int64_t(W) * total_pages, cus_decode * wg_per_cu));
-  std::vector<int32_t> dec_words;
+  // Workspace slots follow batch order (the splits of a sequence are
+  // consecutive); the launch order puts the longest key ranges first, so the
+  // hardware dispatcher schedules them longest-processing-time first and the
+  // short ones fill the tail.
+  struct DecItem { int32_t w[kItemWords]; };
+  std::vector<DecItem> dec_items;
   int32_t n_dec_items = 0, n_split_seqs = 0;
   for (size_t d = 0; d < dec.size(); ++d) {
     const int32_t s = dec[d];
@@ -178,17 +183,21 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
       pps_s = cdiv(Ps, max_splits);
       nspl = cdiv(Ps, pps_s);
     }
-    const int32_t first = n_dec_items;
+    const int32_t slot0 = n_dec_items;
     if (nspl > 1) ++n_split_seqs;
     for (int64_t j = 0; j < nspl; ++j) {
       const int64_t k0 = j * pps_s * P;
       const int64_t k1 = std::min<int64_t>(seq_lens[s], (j + 1) * pps_s * P);
-      const int32_t item[kItemWords] = {s, int32_t(j), int32_t(nspl), int32_t(k0), int32_t(k1),
-                                        first, int32_t(d), 0};
-      dec_words.insert(dec_words.end(), item, item + kItemWords);
+      dec_items.push_back({{s, int32_t(j), int32_t(nspl), int32_t(k0), int32_t(k1), slot0, int32_t(d),
+                            slot0 + int32_t(j)}});
       ++n_dec_items;
     }
   }
+  std::stable_sort(dec_items.begin(), dec_items.end(), [](const DecItem& a, const DecItem& b) {
+    return a.w[4] - a.w[3] > b.w[4] - b.w[3];
+  });
+  std::vector<int32_t> dec_words;
+  for (const DecItem& it : dec_items) dec_words.insert(dec_words.end(), it.w, it.w + kItemWords);
 
   // Prefill tiles of bm rows, the longest causal key range first.
   struct Tile { int32_t s, t, r0, r1, kend; };

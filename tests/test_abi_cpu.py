@@ -155,6 +155,13 @@ def test_run_calls_reject_bad_args_without_gpu():
     a.v_stride = (ctypes.c_int64 * 3)(16 * 4 * 128, 4 * 128, 128)
     a.num_pages = 10
     a.block_table_stride = 4
+    # page-local offsets are 32-bit: a page stride or slot span of 2^31 bytes is refused
+    a.k_stride = (ctypes.c_int64 * 3)(1 << 30, 4 * 128, 128)
+    assert F.lib().flex_attn_decode(plan.handle, ctypes.byref(a), None) == F.FLEX_ERR_INVALID_ARG
+    assert "2^31" in F.last_error()
+    a.k_stride = (ctypes.c_int64 * 3)(16 * 4 * 128, 1 << 26, 128)
+    assert F.lib().flex_attn_decode(plan.handle, ctypes.byref(a), None) == F.FLEX_ERR_INVALID_ARG
+    a.k_stride = (ctypes.c_int64 * 3)(16 * 4 * 128, 4 * 128, 128)
     a.d_plan_bytes = 8
     assert F.lib().flex_attn_decode(plan.handle, ctypes.byref(a), None) == F.FLEX_ERR_WORKSPACE
     a.d_plan_bytes = plan.info["device_plan_bytes"]

@@ -2,8 +2,9 @@
 
 These pin the integer plan contract by properties that hold for any batch:
 decode splits tile [0, L) exactly with page-aligned, non-empty ranges and at
-most max_splits pieces; prefill tiles tile [0, n) with the right causal key
-end; the tile list is ordered longest-first; counts agree with the header.
+most max_splits pieces, in consecutive workspace slots, launched longest
+first; prefill tiles tile [0, n) with the right causal key end; the tile list
+is ordered longest-first; counts agree with the header.
 """
 import random
 
@@ -53,21 +54,26 @@ def check_invariants(sh, opts, qsl, ls, maxp):
     dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1]
     pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= 2]
     assert b[5] == len(dec) and b[6] == len(pre)
-    # decode: each decode sequence's splits tile [0, L)
+    # decode: launch order is key count descending (ties: workspace slot);
+    # slots number the splits in batch order, a sequence's splits consecutive
+    sizes = [(it[4] - it[3], it[7]) for it in dec_items]
+    assert sizes == sorted(sizes, key=lambda x: (-x[0], x[1]))
+    assert sorted(it[7] for it in dec_items) == list(range(nd))
     by_seq = {}
-    for idx, it in enumerate(dec_items):
-        by_seq.setdefault(it[0], []).append((idx, it))
+    for it in sorted(dec_items, key=lambda it: it[7]):
+        by_seq.setdefault(it[0], []).append(it)
     assert sorted(by_seq) == dec
-    order = [it[0] for it in dec_items]
-    assert order == sorted(order)                   # batch order
+    slot_order = [it[0] for it in sorted(dec_items, key=lambda it: it[7])]
+    assert slot_order == sorted(slot_order)         # batch order
+    # each decode sequence's splits tile [0, L)
     for d, s in enumerate(dec):
         items = by_seq[s]
         nspl = len(items)
         assert 1 <= nspl <= max_splits
         pos = 0
-        for j, (idx, it) in enumerate(items):
-            seq, jj, n_s, k0, k1, first, dseq, _ = it
-            assert (jj, n_s, first, dseq) == (j, nspl, items[0][0], d)
+        for j, it in enumerate(items):
+            seq, jj, n_s, k0, k1, slot0, dseq, slot = it
+            assert (jj, n_s, slot0, dseq, slot) == (j, nspl, items[0][7], d, items[0][7] + j)
             assert k0 == pos and k1 > k0 and k0 % P == 0
             pos = k1
         assert pos == ls[s]
