@@ -80,9 +80,10 @@ typedef struct flex_attn_plan_opts {
   int32_t cus_total;          /* [256] */
   int32_t cus_decode;         /* [0 = all CUs] */
   int32_t bm;                 /* prefill rows per tile: 16 or 32 [32]; 64 for 576/512 */
-  int32_t min_split_tokens;   /* smallest decode split, in keys [256] */
-  int32_t max_splits;         /* most splits per decode sequence [32] */
-  int32_t wg_per_cu;          /* decode work-groups aimed at per CU [4] */
+  int32_t min_split_tokens;   /* shortest balanced decode range, in keys [256] */
+  int32_t max_splits;         /* accepted and ignored (must be >= 0) */
+  int32_t wg_per_cu;          /* decode work-groups aimed at per CU
+                                 [1 grouped-query, 4 for 576/512] */
   int32_t split_granule;      /* co-run split granularity in CUs [64] */
   double hbm_gbps;            /* cost model: device HBM bandwidth [8000] */
   double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws [60] */
@@ -94,12 +95,13 @@ typedef struct flex_attn_plan_info {
   int32_t num_seqs;
   int32_t n_decode_seqs;     /* sequences with one new token */
   int32_t n_prefill_seqs;    /* sequences with two or more new tokens */
-  int32_t n_decode_items;    /* (sequence, split) work items */
+  int32_t n_decode_items;    /* decode pieces: (sequence, key range) work items */
   int32_t n_prefill_items;   /* (sequence, row tile) work items */
-  int32_t n_split_seqs;      /* decode sequences split into more than one item */
-  int32_t decode_wg_width;   /* work-groups per decode item (grid y) */
+  int32_t n_split_seqs;      /* decode sequences cut into more than one piece */
+  int32_t decode_wg_width;   /* work-groups per decode range or piece (grid y) */
+  int32_t n_decode_ranges;   /* balanced page ranges the decode pieces form */
   int32_t prefill_grid_y;    /* work-groups per prefill tile (grid y) */
-  int32_t pages_per_split;
+  int32_t pages_per_split;   /* pages per decode range (rounded up) */
   int32_t cus_decode;
   int32_t cus_prefill;
   int32_t bm;

@@ -13,15 +13,24 @@ each phase. The partition itself is not in the paper (it defines no kernel);
 the contract is:
 
 * classification: n = 1 -> decode, n >= 2 -> prefill, n = 0 -> nothing.
-* decode split-K: P_s = ceil(L_s / P); W = work-groups per decode item
-  (Hkv for grouped-query attention, Hq / 64 for the 576/512 latent layout);
-  pps = max(min_pps, ceil(W * sum_s P_s / (cus_decode * wg_per_cu)));
-  n_s = ceil(P_s / pps); if n_s > max_splits then pps_s = ceil(P_s / max_splits),
-  n_s = ceil(P_s / pps_s), else pps_s = pps; split j covers keys
-  [j * pps_s * P, min(L_s, (j + 1) * pps_s * P)). Workspace slots number the
-  splits in batch order (splits of a sequence consecutive); items are listed
-  in launch order: key count descending, ties by slot. Item words:
-  [s, j, n_s, k0, k1, slot of split 0, decode ordinal, slot].
+* decode partition (balanced split-K): P_s = ceil(L_s / P); the pages of
+  all decode sequences, concatenated in batch order, form a list of
+  T = sum_s P_s pages; W = work-groups per key range (grouped-query
+  attention: one per group of up to 8 KV heads, W = ceil(Hkv / 8), so a
+  work-group reads whole slot rows; the 576/512 latent layout: Hq / 64). The
+  list is cut into
+  R = max(1, min(floor(cus_decode * wg_per_cu / W), floor(T / min_pps)),
+  ceil(T / 8192)) ranges, range r = pages [floor(r T / R), floor((r + 1) T / R)),
+  min_pps = ceil(min_split_tokens / P). A piece is the non-empty overlap of a
+  range with one sequence, keys [k0, k1) = [first page * P,
+  min(L_s, end page * P)); pieces are listed by range, i.e. in batch order
+  with keys ascending, and the list index is the piece's workspace slot.
+  Item words: [s, j, n_s, k0, k1, slot of piece 0 of s, qsl[s], slot], j the
+  piece's rank within its sequence and n_s the sequence's piece count. A range
+  table of R + 1 words gives the first piece of each range (the last word is
+  the piece count), and a launch order of the pieces for one-work-group-per-
+  piece launches lists them by key count descending, ties by slot.
+  max_splits is accepted and ignored.
 * prefill tiles of BM rows (BM 32 by default for grouped-query heads, 64 for
   the latent layout): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
   ordered by key_end descending, then sequence, then tile. Each tile is served
@@ -30,8 +39,8 @@ the contract is:
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
 
-Blob layout (int32): 16-word header, 8 words per decode item, 8 per prefill
-item; see ``build_plan``.
+Blob layout (int32): 20-word header, 8 words per decode item, the range
+table, the piece launch order, 8 words per prefill item; see ``build_plan``.
 """
 from __future__ import annotations
 
@@ -41,8 +50,8 @@ from typing import List, Optional, Sequence
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
 MAGIC = 0x46504C58
-VERSION = 2
-HEADER = 16
+VERSION = 3
+HEADER = 20
 ITEM = 8
 
 
@@ -68,7 +77,7 @@ class Opts:
     bm: int = 0                  # 0 -> 32 (64 for the 576/512 layout)
     min_split_tokens: int = 0    # 0 -> 256
     max_splits: int = 0          # 0 -> 32
-    wg_per_cu: int = 0           # 0 -> 4
+    wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 4 (576/512 latent layout)
     split_granule: int = 0       # 0 -> 64
     hbm_gbps: float = 0.0        # 0 -> 8000
     decode_gbps_per_cu: float = 0.0   # 0 -> 60
@@ -83,6 +92,7 @@ class PlanResult:
 
 
 MLA_ROWS_PER_WG = 64
+MAX_RANGE_PAGES = 8192
 
 
 def _supported(sh: Shape) -> bool:
@@ -113,7 +123,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         return PlanResult(ERR_UNSUPPORTED)
     # --- option checks / defaults
     cus_total = o.cus_total or 256
-    wg_per_cu = o.wg_per_cu or 4
+    wg_per_cu = o.wg_per_cu or (4 if sh.head_dim_qk == 576 else 1)
     max_splits = o.max_splits or 32
     min_tokens = o.min_split_tokens or 256
     granule = o.split_granule or 64
@@ -139,8 +149,9 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     if B > 0 and qsl[B] > 2**31 - 1:
         return PlanResult(ERR_INVALID_ARG)
 
-    W = (sh.num_q_heads // MLA_ROWS_PER_WG) if mla else sh.num_kv_heads
-    rows_per_wg = MLA_ROWS_PER_WG if mla else sh.num_q_heads // sh.num_kv_heads
+    heads_per_wg = min(sh.num_kv_heads, 8)
+    W = (sh.num_q_heads // MLA_ROWS_PER_WG) if mla else cdiv(sh.num_kv_heads, heads_per_wg)
+    rows_per_wg = MLA_ROWS_PER_WG if mla else heads_per_wg * (sh.num_q_heads // sh.num_kv_heads)
     dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1]
     pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= 2]
 
@@ -171,26 +182,34 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         cus_decode = best if best is not None else cus_total
     cus_prefill = cus_total - cus_decode if (dec and pre and cus_decode < cus_total) else cus_total
 
-    # --- decode split-K partition
+    # --- decode partition: balanced page ranges over the concatenated decode sequences
     min_pps = cdiv(min_tokens, P)
-    total_pages = sum(cdiv(seq_lens[s], P) for s in dec)
-    pps = max(min_pps, cdiv(W * total_pages, cus_decode * wg_per_cu)) if dec else 0
+    pages = [cdiv(seq_lens[s], P) for s in dec]
+    T = sum(pages)
+    R = max(1, min((cus_decode * wg_per_cu) // W, T // min_pps), cdiv(T, MAX_RANGE_PAGES)) if dec else 0
+    bounds = [(r * T) // R for r in range(R + 1)] if dec else [0]
+    start = [0]
+    for n_p in pages:
+        start.append(start[-1] + n_p)       # first global page of each decode sequence
+    pieces, ranges = [], []
+    for r in range(R):
+        ranges.append(len(pieces))
+        for d, s in enumerate(dec):
+            lo, hi = max(bounds[r], start[d]), min(bounds[r + 1], start[d + 1])
+            if lo < hi:
+                k0 = (lo - start[d]) * P
+                k1 = min(seq_lens[s], (hi - start[d]) * P)
+                pieces.append([s, d, k0, k1])
+    ranges.append(len(pieces))
     dec_items = []
     n_split = 0
     for d, s in enumerate(dec):
-        Ps = cdiv(seq_lens[s], P)
-        nspl = cdiv(Ps, pps)
-        pps_s = pps
-        if nspl > max_splits:
-            pps_s = cdiv(Ps, max_splits)
-            nspl = cdiv(Ps, pps_s)
-        slot0 = len(dec_items)
-        n_split += nspl > 1
-        for j in range(nspl):
-            k0 = j * pps_s * P
-            k1 = min(seq_lens[s], (j + 1) * pps_s * P)
-            dec_items.append([s, j, nspl, k0, k1, slot0, d, slot0 + j])
-    dec_items.sort(key=lambda it: (-(it[4] - it[3]), it[7]))
+        mine = [i for i, pc in enumerate(pieces) if pc[1] == d]
+        n_split += len(mine) > 1
+        for j, i in enumerate(mine):
+            dec_items.append((i, [s, j, len(mine), pieces[i][2], pieces[i][3], mine[0], qsl[s], i]))
+    dec_items = [it for _, it in sorted(dec_items, key=lambda x: x[0])]
+    ppr = cdiv(T, R) if R else 0
 
     # --- prefill tiles, longest key range first
     tiles = []
@@ -202,12 +221,16 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     tiles.sort(key=lambda it: (-it[4], it[0], it[1]))
 
     nd_, np_ = len(dec_items), len(tiles)
-    total = HEADER + ITEM * (nd_ + np_)
+    order = sorted(range(nd_), key=lambda i: (-(dec_items[i][4] - dec_items[i][3]), i))
+    off_ranges = HEADER + ITEM * nd_
+    off_order = off_ranges + len(ranges)
+    off_pre = off_order + nd_
+    total = off_pre + ITEM * np_
     G = sh.num_q_heads // sh.num_kv_heads
     pre_height = sh.num_q_heads if mla else sh.num_kv_heads * cdiv(G, 8)
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
-           HEADER, HEADER + ITEM * nd_, pps, cus_decode, cus_prefill, bm, total]
-    blob = hdr + [x for it in dec_items for x in it] + [x for it in tiles for x in it]
+           HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, 0]
+    blob = hdr + [x for it in dec_items for x in it] + ranges + order + [x for it in tiles for x in it]
     # workspace: (max, sum) per decode item, column and row, then the partial outputs;
     # only needed when some decode sequence is split
     if n_split == 0:
@@ -217,7 +240,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         ws = cdiv(stats, 256) * 256 + nd_ * W * rows_per_wg * sh.head_dim_v * 4
     info = dict(num_seqs=B, n_decode_seqs=len(dec), n_prefill_seqs=len(pre),
                 n_decode_items=nd_, n_prefill_items=np_, n_split_seqs=n_split, decode_wg_width=W,
-                prefill_grid_y=pre_height, pages_per_split=pps,
+                n_decode_ranges=R, prefill_grid_y=pre_height, pages_per_split=ppr,
                 cus_decode=cus_decode, cus_prefill=cus_prefill, bm=bm,
                 plan_words=total, device_plan_bytes=cdiv(total * 4, 256) * 256,
                 workspace_bytes=ws, decode_bytes=dec_bytes, prefill_flops=pre_flops)

@@ -25,37 +25,51 @@ namespace flexattn {
 
 __device__ __forceinline__ PagedCache as_cache(const CacheRef& c) { return PagedCache{c.base, c.sp, c.ss, c.sh}; }
 
-// Split-K merge (flash-decoding combine), one work-group per (decode item,
-// column); only the first split of a split sequence does work. Runs as its own
-// launch after the decode kernel, so every partial is visible without
-// device-scope fences. Splits are combined in ascending order, so results are
-// bit-identical run to run:
-//   M = max_j m_j,  out = sum_j 2^{m_j - M} O_j / sum_j 2^{m_j - M} l_j,
+// Split-K merge (flash-decoding combine), one work-group per (decode piece,
+// column); only piece 0 of a split sequence does work. Runs as its own launch
+// after the decode kernel, so every partial is visible without device-scope
+// fences. Each thread owns 4 value columns of one row and folds the pieces in
+// ascending order, 8 at a time with all their loads in flight, keeping a
+// running maximum M: results are bit-identical run to run. The result is
+//   out = sum_j 2^{m_j - M} O_j / sum_j 2^{m_j - M} l_j,
 //   lse = (M + log2 sum_j 2^{m_j - M} l_j) * ln 2     (m_j in log2 units).
 template <int DV>
 __global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
+  constexpr int KB = 8;   // pieces folded per step
   const int32_t* it = p.items + 8 * blockIdx.x;
   if (it[1] != 0 || it[2] <= 1) return;
   const int slot0 = it[5], nspl = it[2];   // workspace slots slot0 .. slot0 + nspl - 1
   const int col = blockIdx.y, W = gridDim.y, rows = p.rows_per_wg;
-  const int64_t out_row0 = int64_t(p.qsl[it[0]]) * p.Hq + int64_t(col) * rows;
+  const int64_t out_row0 = int64_t(it[6]) * p.Hq + int64_t(col) * rows;
   for (int idx = threadIdx.x; idx < rows * (DV / 4); idx += blockDim.x) {
     const int i = idx / (DV / 4);
     const int d = 4 * (idx % (DV / 4));
-    float M = -INFINITY;
-    for (int j = 0; j < nspl; ++j) {
-      const int64_t slot = int64_t(slot0 + j) * W + col;
-      M = fmaxf(M, p.ws_stats[(slot * rows + i) * 2]);
-    }
-    float den = 0.f;
+    float M = -INFINITY, den = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < nspl; ++j) {
-      const int64_t slot = int64_t(slot0 + j) * W + col;
-      const float mj = p.ws_stats[(slot * rows + i) * 2];
-      const float f = mj == -INFINITY ? 0.f : exp2f(mj - M);
-      den += f * p.ws_stats[(slot * rows + i) * 2 + 1];
-      const f32x4 v = *reinterpret_cast<const f32x4*>(p.ws_o + (slot * rows + i) * DV + d);
-      acc += f * v;
+    for (int j0 = 0; j0 < nspl; j0 += KB) {
+      float mj[KB], lj[KB];
+      f32x4 vj[KB];
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        const int j = min(j0 + k, nspl - 1);
+        const int64_t r = (int64_t(slot0 + j) * W + col) * rows + i;
+        mj[k] = j0 + k < nspl ? p.ws_stats[r * 2] : -INFINITY;
+        lj[k] = p.ws_stats[r * 2 + 1];
+        vj[k] = *reinterpret_cast<const f32x4*>(p.ws_o + r * DV + d);
+      }
+      float Mn = M;
+#pragma unroll
+      for (int k = 0; k < KB; ++k) Mn = fmaxf(Mn, mj[k]);
+      const float sc = M == -INFINITY ? 0.f : exp2f(M - Mn);
+      den *= sc;
+      acc *= sc;
+      M = Mn;
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        const float f = mj[k] == -INFINITY ? 0.f : exp2f(mj[k] - M);
+        den += f * lj[k];
+        acc += f * vj[k];
+      }
     }
     const float inv = 1.f / den;
     u32x2 pk;
@@ -82,20 +96,21 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
 
 // Online-softmax step of one 16-row block over one 32-key chunk.
-// s[b][r]: raw score q.k of key kc0 + 16b + 4gq + r for this lane's row. With
-// MASK, keys at or past `limit` are excluded; without, every key of the chunk
-// is visible to every row. The scale is folded into the exponent:
-// p = 2^(s * scale_log2 - m). Updates the row's max m (log2 units), the
-// lane's partial sum l and the accumulators o (rows 4gq + r), and returns
-// the probabilities as the bf16 A operand of the PV product.
-template <int NACC, bool MASK>
-__device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int limit, int gq, float scale_log2,
-                                               float& m, float& l, f32x4 (&o)[NACC]) {
+// s[b][r]: raw score q.k of key kc0 + 16b + 4gq + r for this lane's row; with
+// `masked`, keys at or past `limit` are excluded (one code path: a second
+// inlined copy for the unmasked case costs registers). The scale is folded
+// into the exponent: p = 2^(s * scale_log2 - m). Updates the row's max m
+// (log2 units, lazily), the lane's partial sum l and the accumulators o
+// (rows 4gq + r), and returns the probabilities as the bf16 A operand of P V.
+template <int NACC>
+__device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], bool masked, int kc0, int limit, int gq,
+                                               float scale_log2, float& m, float& l, f32x4 (&o)[NACC]) {
   float x[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    x[e] = s[e >> 2][e & 3];
-    if constexpr (MASK) x[e] = kc0 + chunk_key(e, gq) < limit ? x[e] : -INFINITY;
+  for (int e = 0; e < 8; ++e) x[e] = s[e >> 2][e & 3];
+  if (masked) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = kc0 + chunk_key(e, gq) < limit ? x[e] : -INFINITY;
   }
   float cmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
   cmax = group_max(cmax) * scale_log2;
@@ -126,20 +141,21 @@ __device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], int kc0, int
   return pop;
 }
 
-// Masked only when the chunk reaches past the smallest key limit of the wave's
-// rows. The 512-wide value layout keeps a single (masked) path: a second
-// inlined copy would push its 512-register budget into spills.
-template <int NACC>
-__device__ __forceinline__ u32x4 softmax_chunk_auto(const f32x4 (&s)[2], int kc0, int limit, int wave_min_limit,
-                                                    int gq, float scale_log2, float& m, float& l, f32x4 (&o)[NACC]) {
-  if constexpr (NACC <= 8) {
-    if (kc0 + 32 <= wave_min_limit) return softmax_chunk<NACC, false>(s, kc0, limit, gq, scale_log2, m, l, o);
-  }
-  return softmax_chunk<NACC, true>(s, kc0, limit, gq, scale_log2, m, l, o);
-}
-
 // ---------------------------------------------------------------------------
 // Decode, grouped-query heads.
+//
+// Work-group (range r, column c) owns one balanced page range of the decode
+// batch, the pieces (sequence, key range) the plan lists for it, and HW =
+// rows_per_wg / G KV heads starting at c * HW. Every wave serves one of those
+// heads (WPH = NW / HW waves per head, taking chunks u, u + WPH, ... of each
+// piece): the work-group reads whole slot rows, so its traffic spreads over
+// all memory channels instead of the subset a single head's fixed row offset
+// maps to. At start it copies the block-table entries of the whole range into
+// LDS; the waves then walk the range as one stream of 32-key chunks with the
+// next chunk's K/V loads in flight while one is computed, across piece
+// boundaries. When a wave leaves a piece it writes that piece's output (whole
+// sequence) or partial (split sequence), combining through LDS first when a
+// head has several waves.
 // ---------------------------------------------------------------------------
 template <int D>
 struct DecodeChunk {
@@ -149,7 +165,15 @@ struct DecodeChunk {
   VRow v[8];        // value dims DPL*n .. of the lane's 8 keys
 };
 
-template <int D, int NW, int P>
+// Position in a wave's chunk stream: piece i (plan item), chunk ci of it, and
+// the piece's first entry in the LDS page window. Wave-uniform.
+struct DecodeCursor {
+  int i, ci, seq, k0, k1, poff;
+};
+
+__device__ __forceinline__ int pages_in(int k0, int k1, int P) { return (k1 - 1) / P - k0 / P + 1; }
+
+template <int D, int NW, int P, bool COMBINE>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void decode_gqa_kernel(AttnParams p) {
   static_assert(D == 64 || D == 128, "head dim");
@@ -160,163 +184,258 @@ void decode_gqa_kernel(AttnParams p) {
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
-  const int item = blockIdx.x;
-  const int g = blockIdx.y;
-  const int W = gridDim.y;
-  const int32_t* it = p.items + 8 * item;
-  const int seq = it[0], nspl = it[2], k0 = it[3];
-  const int L = p.seq_lens[seq];
-  const int kend = min(it[4], L);
-  const int tok = p.qsl[seq];
-  const int32_t* bt_row = p.bt + int64_t(seq) * p.bt_stride;
   const int G = p.G;
+  const int HW = p.rows_per_wg / G;        // KV heads of this work-group
+  const int WPH = max(1, NW / HW);         // waves per head
+  const int hh = w / WPH, u = w % WPH;     // this wave's head within the group, rank among its waves
+  const int g = blockIdx.y * HW + hh;      // this wave's KV head
+  const bool active = hh < HW && g < p.Hkv;
+  const int i_begin = p.ranges[blockIdx.x], i_end = p.ranges[blockIdx.x + 1];
   // Byte strides (the host checks that a page's slots span less than 2^31
   // bytes) and per-lane byte offsets of a chunk's loads from the page bases.
-  const uint8_t* kbase_b = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(g) * p.kc.sh);
-  const uint8_t* vbase_b = reinterpret_cast<const uint8_t*>(p.vc.base + int64_t(g) * p.vc.sh);
+  const uint8_t* kbase_b = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(active ? g : 0) * p.kc.sh);
+  const uint8_t* vbase_b = reinterpret_cast<const uint8_t*>(p.vc.base + int64_t(active ? g : 0) * p.vc.sh);
   const uint32_t ksp_b = uint32_t(p.kc.sp) * 2u, kss_b = uint32_t(p.kc.ss) * 2u;
   const uint32_t vsp_b = uint32_t(p.vc.sp) * 2u, vss_b = uint32_t(p.vc.ss) * 2u;
   const uint32_t k_lane = uint32_t(n) * kss_b + 16u * gq;
   const uint32_t v_lane = uint32_t(4 * gq) * vss_b + 2u * DPL * n;
-  __shared__ int s_pt[kPageWin];
+  extern __shared__ int s_pt[];   // block-table entries of the range
+  __shared__ float s_m[NW][16];
+  __shared__ float s_l[NW][16];
+  __shared__ float s_o[COMBINE ? NW : 1][16][D];   // wave combine (several waves per head)
 
-  // Q as the B operand of S^T = K Q^T: column n = query head g*G + n.
-  u32x4 qop[DC];
+  // The range's block-table entries, piece after piece.
   {
+    int poff = 0;
+    for (int i = i_begin; i < i_end; ++i) {
+      const int32_t* it = p.items + 8 * i;
+      const int k0 = it[3], k1 = it[4];
+      const int32_t* bt_row = p.bt + int64_t(it[0]) * p.bt_stride + k0 / P;
+      const int npg = pages_in(k0, k1, P);
+      for (int t = tid; t < npg; t += NW * 64) s_pt[poff + t] = bt_row[t];
+      poff += npg;
+    }
+  }
+
+  // First piece at or after i (window offset poff) in which this wave has a chunk.
+  auto open = [&](DecodeCursor& c, int i, int poff) {
+    for (; active && i < i_end; ++i) {
+      const int32_t* it = p.items + 8 * i;
+      const int k0 = it[3], k1 = it[4];
+      if (u * 32 < k1 - k0) {
+        c = DecodeCursor{i, u, it[0], k0, k1, poff};
+        return;
+      }
+      poff += pages_in(k0, k1, P);
+    }
+    c.i = i_end;
+  };
+  auto advance = [&](DecodeCursor& c) {
+    c.ci += WPH;
+    if (c.k0 + 32 * c.ci >= c.k1) open(c, c.i + 1, c.poff + pages_in(c.k0, c.k1, P));
+  };
+
+  // K/V loads of one chunk through buffer resources built per 16-key half
+  // from scalar page bases; the record count ends at the piece's last key,
+  // so loads past it read zeros and never touch memory.
+  auto load = [&](Chunk& c, const DecodeCursor& cur) {
+    const int kc0 = cur.k0 + 32 * cur.ci;
+    __amdgpu_buffer_rsrc_t kr[2], vr[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int key = kc0 + 16 * b;
+      // (readfirstlane keeps resources in scalar registers: one the compiler
+      // sees in vector registers becomes a loop.)
+      const uint32_t nvalid = uint32_t(__builtin_amdgcn_readfirstlane(min(max(cur.k1 - key, 0), 16)));
+      const int pidx = cur.poff + min(key, cur.k1 - 1) / P - cur.k0 / P;
+      const uint32_t pg = uint32_t(__builtin_amdgcn_readfirstlane(s_pt[pidx]));
+      const uint32_t slot = uint32_t(key % P);
+      kr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(kbase_b + (uint64_t(pg) * ksp_b + slot * kss_b)),
+                                                0, __builtin_amdgcn_readfirstlane(int(nvalid * kss_b)), kBufferFlags);
+      vr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(vbase_b + (uint64_t(pg) * vsp_b + slot * vss_b)),
+                                                0, __builtin_amdgcn_readfirstlane(int(nvalid * vss_b)), kBufferFlags);
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int cc = 0; cc < DC; ++cc)
+        c.k[b][cc] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr[b], int(k_lane + 64u * cc), 0, 0));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int off = int(v_lane + uint32_t(e & 3) * vss_b);
+      if constexpr (D == 128)
+        c.v[e] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr[e >> 2], off, 0, 0));
+      else
+        c.v[e] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(vr[e >> 2], off, 0, 0));
+    }
+  };
+
+  // Q as the B operand of S^T = K Q^T: column n = query head g*G + n of the
+  // piece's token.
+  u32x4 qop[DC];
+  int q_piece = -1;
+  auto load_q = [&](int i) {
+    const int tok = p.items[8 * i + 6];
     const bool ok = n < G;
     const uint16_t* qr = p.q + (int64_t(tok) * p.Hq + g * G + (ok ? n : 0)) * D + 8 * gq;
 #pragma unroll
     for (int c = 0; c < DC; ++c) qop[c] = ok ? load16(qr + 32 * c) : zero4();
-  }
-  wait_vmem_all();
+    q_piece = i;
+  };
 
   float m = -INFINITY, l = 0.f;
   f32x4 o[DPL];
 #pragma unroll
   for (int a = 0; a < DPL; ++a) o[a] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int wk0 = k0; wk0 < kend; wk0 += kPageWin * P) {
-    const int wk1 = min(kend, wk0 + kPageWin * P);
-    const int pg0 = wk0 / P;
-    const int npg = (wk1 - 1) / P - pg0 + 1;
-    __syncthreads();
-    for (int i = tid; i < npg; i += NW * 64) s_pt[i] = bt_row[pg0 + i];
-    __syncthreads();
-    const int nch = (wk1 - wk0 + 31) >> 5;
-
-    // Every lane always issues its loads, so the number of loads in flight is
-    // fixed and the wait before a chunk's math covers exactly that chunk. Keys
-    // past the window read zeros; the softmax masks them to probability 0.
-    auto load = [&](Chunk& c, int ci) {
-      const int kc0 = wk0 + 32 * ci;
-      const int klast = wk1 - 1;
-      // Page bases and valid ranges of the chunk's two 16-key halves
-      // (wave-uniform): a buffer resource per half whose record count ends at
-      // the last key of the range, so loads past it read zeros and never
-      // touch memory; offsets within a half are per-lane constants.
-      __amdgpu_buffer_rsrc_t kr[2], vr[2];
+  auto compute = [&](const Chunk& c, const DecodeCursor& cur) {
+    const int kc0 = cur.k0 + 32 * cur.ci;
+    f32x4 s[2];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int key = kc0 + 16 * b;
-        // (readfirstlane keeps the record counts in scalar registers: a
-        // resource the compiler sees in vector registers becomes a loop.)
-        const uint32_t nvalid = uint32_t(__builtin_amdgcn_readfirstlane(min(max(wk1 - key, 0), 16)));
-        const uint32_t pg = uint32_t(__builtin_amdgcn_readfirstlane(s_pt[min(key, klast) / P - pg0]));
-        const uint32_t slot = uint32_t(key % P);
-        kr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(kbase_b + (uint64_t(pg) * ksp_b + slot * kss_b)),
-                                                  0, __builtin_amdgcn_readfirstlane(int(nvalid * kss_b)), kBufferFlags);
-        vr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(vbase_b + (uint64_t(pg) * vsp_b + slot * vss_b)),
-                                                  0, __builtin_amdgcn_readfirstlane(int(nvalid * vss_b)), kBufferFlags);
-      }
+    for (int b = 0; b < 2; ++b) {
+      s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int cc = 0; cc < DC; ++cc)
-          c.k[b][cc] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr[b], int(k_lane + 64u * cc), 0, 0));
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int off = int(v_lane + uint32_t(e & 3) * vss_b);
-        if constexpr (D == 128)
-          c.v[e] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr[e >> 2], off, 0, 0));
-        else
-          c.v[e] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(vr[e >> 2], off, 0, 0));
-      }
-    };
-
-    auto compute = [&](const Chunk& c, int ci) {
-      const int kc0 = wk0 + 32 * ci;
-      f32x4 s[2];
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int cc = 0; cc < DC; ++cc) s[b] = mfma_16x16x32(c.k[b][cc], qop[cc], s[b]);
-      }
-      const u32x4 pop = softmax_chunk_auto<DPL>(s, kc0, wk1, wk1, gq, p.scale_log2, m, l, o);
-      u32x4 vop[DPL];
-      if constexpr (D == 128) transpose8x8(c.v, vop);
-      else transpose8x4(c.v, vop);
-#pragma unroll
-      for (int a = 0; a < DPL; ++a) o[a] = mfma_16x16x32(pop, vop[a], o[a]);
-    };
-
-    // Two fixed chunk buffers, the loop unrolled by two: the next chunk's
-    // gathers stay in flight during this chunk's math (a register copy
-    // between iterations would force them to land first).
-    Chunk A, B;
-    load(A, w);
-    for (int ci = w; ci < nch; ci += 2 * NW) {
-      load(B, ci + NW);
-      compute(A, ci);
-      if (ci + NW >= nch) break;
-      load(A, ci + 2 * NW);
-      compute(B, ci + NW);
+      for (int cc = 0; cc < DC; ++cc) s[b] = mfma_16x16x32(c.k[b][cc], qop[cc], s[b]);
     }
-  }
+    const u32x4 pop = softmax_chunk<DPL>(s, kc0 + 32 > cur.k1, kc0, cur.k1, gq, p.scale_log2, m, l, o);
+    u32x4 vop[DPL];
+    if constexpr (D == 128) transpose8x8(c.v, vop);
+    else transpose8x4(c.v, vop);
+#pragma unroll
+    for (int a = 0; a < DPL; ++a) o[a] = mfma_16x16x32(pop, vop[a], o[a]);
+  };
 
-  // Combine the waves' partial states through LDS.
-  const float ltot = group_sum(l);
-  __shared__ float s_m[NW][16];
-  __shared__ float s_l[NW][16];
-  __shared__ float s_o[NW][16][D];
-  if (gq == 0) {
-    s_m[w][n] = m;
-    s_l[w][n] = ltot;
-  }
+  // Write piece i's result for this wave's head: the output of a whole
+  // sequence (normalised, bf16) or the partial of a split one (fp32 numerator,
+  // max and sum per row, into the piece's workspace slot); reset the state.
+  // Lane (n, gq) holds rows 4gq + r of the accumulators at value dims
+  // DPL*n .. DPL*n + DPL - 1.
+  auto finish = [&](int i) {
+    const int32_t* it = p.items + 8 * i;
+    const int nspl = it[2];
+    const int tok = it[6];
+    const int64_t slot = int64_t(it[7]) * gridDim.y + blockIdx.y;   // this piece's workspace slot
+    const float ltot = group_sum(l);
+    if constexpr (!COMBINE) {   // one wave per head
+      if (active) {
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 4; ++r) {
+          const int row = 4 * gq + r;
+          const float mr = shfl_f(m, row), lr = shfl_f(ltot, row);
+          if (row < G) {
+            if (nspl == 1) {
+              const float inv = 1.f / lr;
+              uint16_t* dst = p.out + (int64_t(tok) * p.Hq + g * G + row) * D + DPL * n;
+              if constexpr (DPL == 8) {
+                u32x4 pk;
 #pragma unroll
-    for (int a = 0; a < DPL; ++a) s_o[w][4 * gq + r][DPL * n + a] = o[a][r];
-  __syncthreads();
-
-  const bool single = nspl == 1;
-  const int64_t out_row0 = int64_t(tok) * p.Hq + int64_t(g) * G;
-  const int64_t slot = int64_t(it[7]) * W + g;   // this split's workspace slot
-  for (int idx = tid; idx < G * (D / 2); idx += NW * 64) {
-    const int i = idx / (D / 2), d = 2 * (idx % (D / 2));
-    float M = s_m[0][i];
+                for (int a = 0; a < 4; ++a) pk[a] = pack_bf16x2(o[2 * a][r] * inv, o[2 * a + 1][r] * inv);
+                *reinterpret_cast<u32x4*>(dst) = pk;
+              } else {
+                u32x2 pk;
 #pragma unroll
-    for (int ww = 1; ww < NW; ++ww) M = fmaxf(M, s_m[ww][i]);
-    float den = 0.f, o0 = 0.f, o1 = 0.f;
+                for (int a = 0; a < 2; ++a) pk[a] = pack_bf16x2(o[2 * a][r] * inv, o[2 * a + 1][r] * inv);
+                *reinterpret_cast<u32x2*>(dst) = pk;
+              }
+              if (n == 0 && p.lse) p.lse[int64_t(tok) * p.Hq + g * G + row] = (mr + log2f(lr)) * kLn2;
+            } else {
+              const int64_t srow = slot * p.rows_per_wg + hh * G + row;
+              float* dst = p.ws_o + srow * D + DPL * n;
 #pragma unroll
-    for (int ww = 0; ww < NW; ++ww) {
-      const float f = s_m[ww][i] == -INFINITY ? 0.f : fast_exp2(s_m[ww][i] - M);
-      den += f * s_l[ww][i];
-      o0 += f * s_o[ww][i][d];
-      o1 += f * s_o[ww][i][d + 1];
-    }
-    if (single) {
-      const float inv = 1.f / den;
-      *reinterpret_cast<uint32_t*>(p.out + (out_row0 + i) * D + d) = pack_bf16x2(o0 * inv, o1 * inv);
-      if (d == 0 && p.lse) p.lse[out_row0 + i] = (M + log2f(den)) * kLn2;
+              for (int a4 = 0; a4 < DPL / 4; ++a4)
+                *reinterpret_cast<f32x4*>(dst + 4 * a4) =
+                    f32x4{o[4 * a4][r], o[4 * a4 + 1][r], o[4 * a4 + 2][r], o[4 * a4 + 3][r]};
+              if (n == 0) {
+                p.ws_stats[srow * 2] = mr;
+                p.ws_stats[srow * 2 + 1] = lr;
+              }
+            }
+          }
+        }
+      }
     } else {
-      *reinterpret_cast<float2*>(p.ws_o + (slot * p.rows_per_wg + i) * D + d) = make_float2(o0, o1);
-      if (d == 0) {
-        p.ws_stats[(slot * p.rows_per_wg + i) * 2] = M;
-        p.ws_stats[(slot * p.rows_per_wg + i) * 2 + 1] = den;
+      // Several waves per head: combine their states through LDS.
+      lds_barrier();   // the previous piece's combine is done reading
+      if (gq == 0) {
+        s_m[w][n] = m;
+        s_l[w][n] = ltot;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int a = 0; a < DPL; ++a) s_o[w][4 * gq + r][DPL * n + a] = o[a][r];
+      lds_barrier();
+      for (int idx = tid; idx < HW * G * (D / 2); idx += NW * 64) {
+        const int h = idx / (G * (D / 2));
+        const int row = (idx / (D / 2)) % G, d = 2 * (idx % (D / 2));
+        const int gh = blockIdx.y * HW + h;
+        if (gh >= p.Hkv) continue;
+        const int w0 = h * WPH;
+        float M = s_m[w0][row];
+        for (int ww = 1; ww < WPH; ++ww) M = fmaxf(M, s_m[w0 + ww][row]);
+        float den = 0.f, o0 = 0.f, o1 = 0.f;
+        for (int ww = 0; ww < WPH; ++ww) {
+          const float f = s_m[w0 + ww][row] == -INFINITY ? 0.f : fast_exp2(s_m[w0 + ww][row] - M);
+          den += f * s_l[w0 + ww][row];
+          o0 += f * s_o[w0 + ww][row][d];
+          o1 += f * s_o[w0 + ww][row][d + 1];
+        }
+        if (nspl == 1) {
+          const float inv = 1.f / den;
+          *reinterpret_cast<uint32_t*>(p.out + (int64_t(tok) * p.Hq + gh * G + row) * D + d) =
+              pack_bf16x2(o0 * inv, o1 * inv);
+          if (d == 0 && p.lse) p.lse[int64_t(tok) * p.Hq + gh * G + row] = (M + log2f(den)) * kLn2;
+        } else {
+          const int64_t srow = slot * p.rows_per_wg + h * G + row;
+          *reinterpret_cast<float2*>(p.ws_o + srow * D + d) = make_float2(o0, o1);
+          if (d == 0) {
+            p.ws_stats[srow * 2] = M;
+            p.ws_stats[srow * 2 + 1] = den;
+          }
+        }
       }
     }
+    m = -INFINITY;
+    l = 0.f;
+#pragma unroll
+    for (int a = 0; a < DPL; ++a) o[a] = f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  // Finish every piece before i, then make sure Q is piece i's. A wave
+  // finishes every piece of the range in order (several waves per head meet
+  // in each combine).
+  int fin = i_begin;
+  auto enter = [&](int i) {
+    for (; fin < i; ++fin) finish(fin);
+    if (q_piece != i) load_q(i);
+  };
+
+  DecodeCursor c;
+  open(c, i_begin, 0);
+  if (c.i < i_end) load_q(c.i);
+  wait_vmem_all();
+  lds_barrier();   // the page window is complete
+
+  // Two fixed chunk buffers, the loop unrolled by two: the next chunk's loads
+  // stay in flight during this chunk's math (a register copy between
+  // iterations would force them to land first).
+  Chunk A, B;
+  if (c.i < i_end) load(A, c);
+  while (c.i < i_end) {
+    DecodeCursor c2 = c;
+    advance(c2);
+    if (c2.i < i_end) load(B, c2);
+    enter(c.i);
+    compute(A, c);
+    if (c2.i >= i_end) break;
+    DecodeCursor c3 = c2;
+    advance(c3);
+    if (c3.i < i_end) load(A, c3);
+    enter(c2.i);
+    compute(B, c2);
+    c = c3;
   }
+  for (; fin < i_end; ++fin) finish(fin);
 }
 
 // ---------------------------------------------------------------------------
@@ -423,7 +542,8 @@ void rowpar_kernel(AttnParams p) {
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
-  const int32_t* it = p.items + 8 * blockIdx.x;
+  // Decode pieces launch longest first; prefill tiles are listed that way.
+  const int32_t* it = p.items + 8 * (MODE == kDecodeLatent ? p.order[blockIdx.x] : int(blockIdx.x));
   const int seq = it[0];
   const int L = p.seq_lens[seq];
   const int q0 = p.qsl[seq];
@@ -883,20 +1003,33 @@ static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stre
 }
 
 template <int D, int P>
-static hipError_t launch_decode_gqa(const AttnParams& p, dim3 grid, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P>), grid, dim3(256), 0, stream, p);
+static hipError_t launch_decode_gqa(const AttnParams& p, hipStream_t stream) {
+  // One work-group per (balanced range, KV head); the range's block-table
+  // entries take dynamic LDS.
+  // Four waves when the work-group serves at most four KV heads, else eight
+  // (one per head).
+  const dim3 grid(p.n_ranges, p.grid_y);
+  const size_t window = size_t(p.range_pages) * 4;
+  const int hw = p.rows_per_wg / p.G;
+  if (hw <= 2)   // several waves per head, combined through LDS
+    hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P, true>), grid, dim3(256), window, stream, p);
+  else if (hw <= 4)
+    hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P, false>), grid, dim3(256), window, stream, p);
+  else
+    hipLaunchKernelGGL((decode_gqa_kernel<D, 8, P, false>), grid, dim3(512), window, stream, p);
   return hipGetLastError();
 }
 
-static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, dim3 grid, hipStream_t stream) {
+static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t stream) {
   const bool p16 = p.P == 16;
   if (p.P != 16 && p.P != 64) return hipErrorInvalidValue;
+  const dim3 pieces(p.n_items, p.grid_y);
   switch (dqk) {
-    case 128: return p16 ? launch_decode_gqa<128, 16>(p, grid, stream) : launch_decode_gqa<128, 64>(p, grid, stream);
-    case 64: return p16 ? launch_decode_gqa<64, 16>(p, grid, stream) : launch_decode_gqa<64, 64>(p, grid, stream);
-    case 576:
-      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16, 3>(p, grid, stream)
-                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64, 3>(p, grid, stream);
+    case 128: return p16 ? launch_decode_gqa<128, 16>(p, stream) : launch_decode_gqa<128, 64>(p, stream);
+    case 64: return p16 ? launch_decode_gqa<64, 16>(p, stream) : launch_decode_gqa<64, 64>(p, stream);
+    case 576:   // one work-group per (piece, group of 64 heads)
+      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16, 3>(p, pieces, stream)
+                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64, 3>(p, pieces, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -904,7 +1037,7 @@ static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, dim3 grid, 
 hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStream_t stream) {
   if (p.n_items == 0) return hipSuccess;
   const dim3 grid(p.n_items, p.grid_y);
-  hipError_t e = launch_decode_kernel(p, dqk, grid, stream);
+  hipError_t e = launch_decode_kernel(p, dqk, stream);
   if (e != hipSuccess || !has_splits) return e;
   switch (dqk) {
     case 128: hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, p); break;

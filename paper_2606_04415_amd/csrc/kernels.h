@@ -22,6 +22,10 @@ struct AttnParams {
   float* lse;
   const int32_t* items;   // device pointer to the first item of this phase
   int32_t n_items;
+  const int32_t* ranges;  // decode: first piece of each balanced range (+ the piece count)
+  const int32_t* order;   // decode: pieces longest first, for one work-group per piece
+  int32_t n_ranges;
+  int32_t range_pages;    // decode: most pages a range holds
   float* ws_stats;        // decode: [item][W][rows][2] (max in log2 units, sum)
   float* ws_o;            // decode: [item][W][rows][d_v] unnormalised partial outputs
   int32_t Hq, Hkv, G;     // G = query heads per KV head

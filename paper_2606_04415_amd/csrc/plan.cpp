@@ -89,7 +89,9 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   if (opts) o = *opts;
   const bool latent = sh.head_dim_qk == 576;
   const int64_t cus_total = o.cus_total ? o.cus_total : 256;
-  const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : 4;
+  // Grouped-query decode: one work-group per CU walking a long range measured
+  // fastest; latent decode launches one work-group per piece, so more pieces.
+  const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : (sh.head_dim_qk == 576 ? 4 : 1);
   const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
   const int64_t granule = o.split_granule ? o.split_granule : 64;
@@ -114,12 +116,16 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
       return set_error(FLEX_ERR_INVALID_ARG, "sequence " + std::to_string(s) + ": L > max_pages_per_seq * page_size");
   }
 
-  const int32_t W = latent ? sh.num_q_heads / kLatentRowsPerWG : sh.num_kv_heads;
+  // Decode work-groups per key range: one per group of up to 8 KV heads for
+  // grouped-query attention (a work-group then reads whole slot rows, which
+  // spreads its stream over every memory channel), Hq / 64 for the latent layout.
+  const int32_t heads_per_wg = std::min(sh.num_kv_heads, kDecodeHeadsPerWG);
+  const int32_t W = latent ? sh.num_q_heads / kLatentRowsPerWG : int32_t(cdiv(sh.num_kv_heads, heads_per_wg));
   // Prefill work-groups per tile: one per query head (latent layout), or one per
   // KV head and group of up to 8 of its query heads (grouped-query layout).
   const int32_t G = sh.num_q_heads / sh.num_kv_heads;
   const int32_t pre_grid_y = latent ? sh.num_q_heads : sh.num_kv_heads * ((G + 7) / 8);
-  const int32_t rows_per_wg = latent ? kLatentRowsPerWG : sh.num_q_heads / sh.num_kv_heads;
+  const int32_t rows_per_wg = latent ? kLatentRowsPerWG : heads_per_wg * (sh.num_q_heads / sh.num_kv_heads);
   std::vector<int32_t> dec, pre;
   for (int32_t s = 0; s < num_seqs; ++s) {
     const int32_t n = qsl[s + 1] - qsl[s];
@@ -162,42 +168,55 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t cus_prefill =
       (!dec.empty() && !pre.empty() && cus_decode < cus_total) ? cus_total - cus_decode : cus_total;
 
-  // Decode split-K partition: page-aligned key ranges sized so that the
-  // decode grid holds about wg_per_cu work-groups per decode CU.
+  // Decode partition (balanced split-K): the pages of all decode sequences,
+  // concatenated in batch order, are cut into R near-equal ranges, one
+  // work-group column each, aiming at wg_per_cu resident work-groups per
+  // decode CU. A piece is the overlap of a range with one sequence; pieces
+  // are listed by range (batch order, keys ascending) and the list index is
+  // the piece's workspace slot, so a sequence's pieces are consecutive.
   const int64_t min_pps = cdiv(min_tokens, P);
-  int64_t total_pages = 0;
-  for (int32_t s : dec) total_pages += cdiv(seq_lens[s], P);
-  const int64_t pps = dec.empty() ? 0 : std::max(min_pps, cdiv(int64_t(W) * total_pages, cus_decode * wg_per_cu));
-  // Workspace slots follow batch order (the splits of a sequence are
-  // consecutive); the launch order puts the longest key ranges first, so the
-  // hardware dispatcher schedules them longest-processing-time first and the
-  // short ones fill the tail.
-  struct DecItem { int32_t w[kItemWords]; };
-  std::vector<DecItem> dec_items;
-  int32_t n_dec_items = 0, n_split_seqs = 0;
-  for (size_t d = 0; d < dec.size(); ++d) {
-    const int32_t s = dec[d];
-    const int64_t Ps = cdiv(seq_lens[s], P);
-    int64_t nspl = cdiv(Ps, pps), pps_s = pps;
-    if (nspl > max_splits) {
-      pps_s = cdiv(Ps, max_splits);
-      nspl = cdiv(Ps, pps_s);
-    }
-    const int32_t slot0 = n_dec_items;
-    if (nspl > 1) ++n_split_seqs;
-    for (int64_t j = 0; j < nspl; ++j) {
-      const int64_t k0 = j * pps_s * P;
-      const int64_t k1 = std::min<int64_t>(seq_lens[s], (j + 1) * pps_s * P);
-      dec_items.push_back({{s, int32_t(j), int32_t(nspl), int32_t(k0), int32_t(k1), slot0, int32_t(d),
-                            slot0 + int32_t(j)}});
-      ++n_dec_items;
+  std::vector<int64_t> start(dec.size() + 1, 0);   // first global page of each decode sequence
+  for (size_t d = 0; d < dec.size(); ++d) start[d + 1] = start[d] + cdiv(seq_lens[dec[d]], P);
+  const int64_t T = start[dec.size()];
+  // (At least ceil(T / kMaxRangePages) ranges: a range's block-table entries
+  // are staged in LDS.)
+  const int64_t R = dec.empty() ? 0
+                                : std::max<int64_t>({int64_t(1), std::min<int64_t>(cus_decode * wg_per_cu / W, T / min_pps),
+                                                     cdiv(T, kMaxRangePages)});
+  struct Piece { int32_t s, d, k0, k1; };
+  std::vector<Piece> pieces;
+  std::vector<int32_t> ranges;
+  size_t d0 = 0;   // first sequence that can overlap the current range
+  for (int64_t r = 0; r < R; ++r) {
+    ranges.push_back(int32_t(pieces.size()));
+    const int64_t lo_r = r * T / R, hi_r = (r + 1) * T / R;
+    while (d0 < dec.size() && start[d0 + 1] <= lo_r) ++d0;
+    for (size_t d = d0; d < dec.size() && start[d] < hi_r; ++d) {
+      const int64_t lo = std::max(lo_r, start[d]), hi = std::min(hi_r, start[d + 1]);
+      if (lo >= hi) continue;
+      const int32_t s = dec[d];
+      pieces.push_back({s, int32_t(d), int32_t((lo - start[d]) * P),
+                        int32_t(std::min<int64_t>(seq_lens[s], (hi - start[d]) * P))});
     }
   }
-  std::stable_sort(dec_items.begin(), dec_items.end(), [](const DecItem& a, const DecItem& b) {
-    return a.w[4] - a.w[3] > b.w[4] - b.w[3];
-  });
+  ranges.push_back(int32_t(pieces.size()));
+  const int64_t ppr = R ? cdiv(T, R) : 0;
+  std::vector<int32_t> first_piece(dec.size(), -1), n_pieces(dec.size(), 0);
+  for (size_t i = 0; i < pieces.size(); ++i) {
+    const int32_t d = pieces[i].d;
+    if (first_piece[d] < 0) first_piece[d] = int32_t(i);
+    ++n_pieces[d];
+  }
   std::vector<int32_t> dec_words;
-  for (const DecItem& it : dec_items) dec_words.insert(dec_words.end(), it.w, it.w + kItemWords);
+  int32_t n_split_seqs = 0;
+  for (size_t d = 0; d < dec.size(); ++d) n_split_seqs += n_pieces[d] > 1;
+  for (size_t i = 0; i < pieces.size(); ++i) {
+    const Piece& pc = pieces[i];
+    const int32_t item[kItemWords] = {pc.s, int32_t(i) - first_piece[pc.d], n_pieces[pc.d], pc.k0, pc.k1,
+                                      first_piece[pc.d], qsl[pc.s], int32_t(i)};
+    dec_words.insert(dec_words.end(), item, item + kItemWords);
+  }
+  const int32_t n_dec_items = int32_t(pieces.size());
 
   // Prefill tiles of bm rows, the longest causal key range first.
   struct Tile { int32_t s, t, r0, r1, kend; };
@@ -220,7 +239,16 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   plan->shape = sh;
   plan->rows_per_wg = rows_per_wg;
   const int32_t n_pre_items = int32_t(tiles.size());
-  const int32_t total = kHeaderWords + kItemWords * (n_dec_items + n_pre_items);
+  // Launch order for one work-group per piece: longest key range first.
+  std::vector<int32_t> order(n_dec_items);
+  for (int32_t i = 0; i < n_dec_items; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return pieces[a].k1 - pieces[a].k0 > pieces[b].k1 - pieces[b].k0;
+  });
+  const int32_t off_ranges = kHeaderWords + kItemWords * n_dec_items;
+  const int32_t off_order = off_ranges + int32_t(ranges.size());
+  const int32_t off_pre = off_order + n_dec_items;
+  const int32_t total = off_pre + kItemWords * n_pre_items;
   auto& w = plan->words;
   w.assign(kHeaderWords, 0);
   w[H_MAGIC] = kPlanMagic;
@@ -233,13 +261,18 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   w[H_DEC_WIDTH] = W;
   w[H_PRE_GRID_Y] = pre_grid_y;
   w[H_OFF_DEC] = kHeaderWords;
-  w[H_OFF_PRE] = kHeaderWords + kItemWords * n_dec_items;
-  w[H_PPS] = int32_t(pps);
+  w[H_OFF_PRE] = off_pre;
+  w[H_PPS] = int32_t(ppr);
   w[H_CUS_DEC] = int32_t(cus_decode);
   w[H_CUS_PRE] = int32_t(cus_prefill);
   w[H_BM] = bm;
   w[H_TOTAL_WORDS] = total;
+  w[H_N_RANGES] = int32_t(R);
+  w[H_OFF_RANGES] = off_ranges;
+  w[H_OFF_ORDER] = off_order;
   w.insert(w.end(), dec_words.begin(), dec_words.end());
+  w.insert(w.end(), ranges.begin(), ranges.end());
+  w.insert(w.end(), order.begin(), order.end());
   for (const Tile& t : tiles) {
     const int32_t item[kItemWords] = {t.s, t.t, t.r0, t.r1, t.kend, 0, 0, 0};
     w.insert(w.end(), item, item + kItemWords);
@@ -262,7 +295,8 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   info.n_split_seqs = n_split_seqs;
   info.decode_wg_width = W;
   info.prefill_grid_y = pre_grid_y;
-  info.pages_per_split = int32_t(pps);
+  info.pages_per_split = int32_t(ppr);
+  info.n_decode_ranges = int32_t(R);
   info.cus_decode = int32_t(cus_decode);
   info.cus_prefill = int32_t(cus_prefill);
   info.bm = bm;

@@ -54,7 +54,7 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("num_seqs", ctypes.c_int32), ("n_decode_seqs", ctypes.c_int32),
                 ("n_prefill_seqs", ctypes.c_int32), ("n_decode_items", ctypes.c_int32),
                 ("n_prefill_items", ctypes.c_int32), ("n_split_seqs", ctypes.c_int32),
-                ("decode_wg_width", ctypes.c_int32),
+                ("decode_wg_width", ctypes.c_int32), ("n_decode_ranges", ctypes.c_int32),
                 ("prefill_grid_y", ctypes.c_int32), ("pages_per_split", ctypes.c_int32),
                 ("cus_decode", ctypes.c_int32), ("cus_prefill", ctypes.c_int32), ("bm", ctypes.c_int32),
                 ("plan_words", ctypes.c_int32), ("device_plan_bytes", ctypes.c_size_t),

@@ -1,10 +1,10 @@
 """Invariants of the plan re-derivation (oracle/plan.py), CPU only.
 
 These pin the integer plan contract by properties that hold for any batch:
-decode splits tile [0, L) exactly with page-aligned, non-empty ranges and at
-most max_splits pieces, in consecutive workspace slots, launched longest
-first; prefill tiles tile [0, n) with the right causal key end; the tile list
-is ordered longest-first; counts agree with the header.
+decode pieces tile [0, L) exactly with page-aligned, non-empty ranges in
+consecutive workspace slots, and the balanced ranges hold floor or ceil of
+T / R pages each; prefill tiles tile [0, n) with the right causal key end;
+the tile list is ordered longest-first; counts agree with the header.
 """
 import random
 
@@ -45,35 +45,45 @@ def check_invariants(sh, opts, qsl, ls, maxp):
     b = r.blob
     P = sh.page_size
     o = opts or OP.Opts()
-    max_splits = o.max_splits or 32
-    assert b[0] == OP.MAGIC and b[15] == len(b)
-    nd, npf = b[3], b[4]
-    dec_items = [b[16 + 8 * i:24 + 8 * i] for i in range(nd)]
+    assert b[0] == OP.MAGIC and b[15] == len(b) and b[9] == OP.HEADER
+    nd, npf, R, off_r = b[3], b[4], b[16], b[17]
+    dec_items = [b[b[9] + 8 * i:b[9] + 8 * i + 8] for i in range(nd)]
     pre_items = [b[b[10] + 8 * i:b[10] + 8 * i + 8] for i in range(npf)]
+    ranges = b[off_r:off_r + R + 1]
+    order = b[b[18]:b[18] + nd]
+    assert off_r == b[9] + 8 * nd and b[18] == off_r + R + 1 and b[10] == b[18] + nd
+    assert sorted(order) == list(range(nd))
+    keys = [(-(dec_items[i][4] - dec_items[i][3]), i) for i in order]
+    assert keys == sorted(keys)                       # longest first, ties by slot
     B = len(ls)
     dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1]
     pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= 2]
     assert b[5] == len(dec) and b[6] == len(pre)
-    # decode: launch order is key count descending (ties: workspace slot);
-    # slots number the splits in batch order, a sequence's splits consecutive
-    sizes = [(it[4] - it[3], it[7]) for it in dec_items]
-    assert sizes == sorted(sizes, key=lambda x: (-x[0], x[1]))
-    assert sorted(it[7] for it in dec_items) == list(range(nd))
-    by_seq = {}
-    for it in sorted(dec_items, key=lambda it: it[7]):
-        by_seq.setdefault(it[0], []).append(it)
-    assert sorted(by_seq) == dec
-    slot_order = [it[0] for it in sorted(dec_items, key=lambda it: it[7])]
-    assert slot_order == sorted(slot_order)         # batch order
-    # each decode sequence's splits tile [0, L)
-    for d, s in enumerate(dec):
-        items = by_seq[s]
-        nspl = len(items)
-        assert 1 <= nspl <= max_splits
+    # decode: R balanced ranges over the concatenated pages of the decode sequences
+    T = sum(-(-ls[s] // P) for s in dec)
+    W = b[7]
+    if dec:
+        min_pps = -(-(o.min_split_tokens or 256) // P)
+        wgpc = o.wg_per_cu or (4 if sh.head_dim_qk == 576 else 1)
+        assert R == max(1, min(b[12] * wgpc // W, T // min_pps), -(-T // 8192))
+        assert ranges[0] == 0 and ranges[-1] == nd
+        assert all(x < y for x, y in zip(ranges, ranges[1:]))          # no empty range
+        for rr in range(R):
+            pages = sum(-(-(it[4] - it[3]) // P) for it in dec_items[ranges[rr]:ranges[rr + 1]])
+            assert pages in (T // R, -(-T // R))
+    else:
+        assert R == 0 and ranges == [0] and nd == 0
+    # pieces are listed in slot order; a sequence's pieces are consecutive and tile [0, L)
+    assert [it[7] for it in dec_items] == list(range(nd))
+    seqs = [it[0] for it in dec_items]
+    assert seqs == sorted(seqs) and sorted(set(seqs)) == dec
+    for s in dec:
+        items = [it for it in dec_items if it[0] == s]
+        slot0 = items[0][7]
         pos = 0
         for j, it in enumerate(items):
-            seq, jj, n_s, k0, k1, slot0, dseq, slot = it
-            assert (jj, n_s, slot0, dseq, slot) == (j, nspl, items[0][7], d, items[0][7] + j)
+            seq, jj, n_s, k0, k1, s0, q0, slot = it
+            assert (jj, n_s, s0, q0, slot) == (j, len(items), slot0, qsl[s], slot0 + j)
             assert k0 == pos and k1 > k0 and k0 % P == 0
             pos = k1
         assert pos == ls[s]
