@@ -184,19 +184,24 @@ def main():
     log(f"plan: {info['n_decode_items']} decode items x {info['decode_wg_width']}, "
         f"{info['n_prefill_items']} prefill tiles x {info['prefill_grid_y']}; co-run {cp}/{cd} CUs")
 
+    # The caller issues steps on a stream of its own: HIP's legacy default
+    # stream synchronizes implicitly with the co-run pair's streams, which
+    # would hold the host at every step.
+    caller = torch.cuda.Stream()
+
     def timed(mode, steps, warmup):
         corun.set_timing(True)
         for i in range(warmup):
-            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, corun=corun)
+            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
         torch.cuda.synchronize()
         corun.set_timing(True)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t_wall = time.perf_counter()
-        e0.record()
+        e0.record(caller)
         for i in range(steps):
-            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, corun=corun)
-        e1.record()
+            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
+        e1.record(caller)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t_wall
         ms = e0.elapsed_time(e1) / steps
@@ -208,6 +213,11 @@ def main():
     log(f"co-run step {c_ms * 1e3:.1f} us (prefill {c_pre * 1e3:.1f} us, decode {c_dec * 1e3:.1f} us)")
     s_ms = s_pre = s_dec = None
     if not args.no_serial:
+        # serial leg: the same batch planned for the whole device
+        pa_s = F.PagedAttention(shape, F.make_opts(cus_decode=0, bm=args.bm), b.query_start_loc.tolist(),
+                                b.seq_lens.tolist(), b.block_table.shape[1])
+        arglist = [pa_s.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+        pa = pa_s
         s_ms, _, s_pre, s_dec = timed(F.FLEX_MODE_SERIAL, args.steps, args.warmup)
         log(f"serial step {s_ms * 1e3:.1f} us (prefill {s_pre * 1e3:.1f} us, decode {s_dec * 1e3:.1f} us)")
     corun.close()

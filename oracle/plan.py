@@ -78,7 +78,7 @@ class Opts:
     min_split_tokens: int = 0    # 0 -> 256
     max_splits: int = 0          # 0 -> 32
     wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 4 (576/512 latent layout)
-    split_granule: int = 0       # 0 -> 64
+    split_granule: int = 0       # 0 -> 32
     hbm_gbps: float = 0.0        # 0 -> 8000
     decode_gbps_per_cu: float = 0.0   # 0 -> 60
     prefill_tflops_per_cu: float = 0.0  # 0 -> 5
@@ -126,7 +126,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     wg_per_cu = o.wg_per_cu or (4 if sh.head_dim_qk == 576 else 1)
     max_splits = o.max_splits or 32
     min_tokens = o.min_split_tokens or 256
-    granule = o.split_granule or 64
+    granule = o.split_granule or 32
     mla = sh.head_dim_qk == 576
     bm = o.bm or (64 if mla else 32)
     if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:

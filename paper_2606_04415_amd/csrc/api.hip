@@ -23,9 +23,11 @@ using namespace flexattn;
 struct flex_attn_corun {
   hipStream_t prefill = nullptr;
   hipStream_t decode = nullptr;
-  hipEvent_t fork = nullptr;
-  hipEvent_t join_p = nullptr;
-  hipEvent_t join_d = nullptr;
+  // Fork/join through stream memory operations on three 64-bit step counters
+  // (caller, prefill, decode): far cheaper, on the host and on the device,
+  // than event records and event waits across queues.
+  uint64_t* flags = nullptr;   // device memory, zeroed at creation
+  uint64_t step = 0;           // last step number issued
   int device = 0;
   int cus_prefill = 0;
   int cus_decode = 0;
@@ -129,16 +131,18 @@ int run_prefill(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "prefill launch");
 }
 
-// CU mask with `count` units out of `total`: bit i is set when
-// ((i >> 3) & 3) falls in [lo, lo + count/64), so each group of 32 bits and
-// each residue class of i mod 8 get the same number of units. Whether the
-// device maps mask bits to XCDs by i mod 8 or by i / 32, the units then spread
-// evenly over all eight XCDs and every XCD keeps some units for the stream.
-void build_mask(int lo_quarter, int quarters, int total, uint32_t* mask, int words) {
+// CU masks in eighths of the device. Mask bit i = 32k + 8q + r (k = i / 32,
+// q = (i >> 3) & 3, r = i & 7) belongs to eighth 2q + (((r + k) >> 2) & 1):
+// every eighth takes 4 bits of each group of 32 and 4 bits of each residue
+// class of i mod 8, so whether the device maps mask bits to XCDs by i / 32 or
+// by i mod 8, a set of eighths spreads evenly over all eight XCDs.
+int eighth_of(int i) { return 2 * ((i >> 3) & 3) + ((((i & 7) + (i >> 5)) >> 2) & 1); }
+
+void build_mask(int lo_eighth, int eighths, int total, uint32_t* mask, int words) {
   for (int i = 0; i < words; ++i) mask[i] = 0;
   for (int i = 0; i < total; ++i) {
-    const int q = (i >> 3) & 3;
-    if (q >= lo_quarter && q < lo_quarter + quarters) mask[i >> 5] |= 1u << (i & 31);
+    const int e = eighth_of(i % 256);
+    if (e >= lo_eighth && e < lo_eighth + eighths) mask[i >> 5] |= 1u << (i & 31);
   }
 }
 
@@ -219,19 +223,29 @@ extern "C" int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_arg
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (dev != corun->device) return set_error(FLEX_ERR_INVALID_ARG, "co-run pair belongs to another device");
-  if ((e = hipEventRecord(corun->fork, s)) != hipSuccess) return hip_fail(e, "fork record");
-  if ((e = hipStreamWaitEvent(corun->prefill, corun->fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
-  if ((e = hipStreamWaitEvent(corun->decode, corun->fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
+  // Fork: the caller stream publishes the step number once its earlier work
+  // is done; both phase streams wait for it. Join: each phase stream
+  // publishes the step number after its kernels; the caller stream waits for
+  // both.
+  const uint64_t step = ++corun->step;
+  uint64_t* f = corun->flags;
+  if ((e = hipStreamWriteValue64(s, f, step, 0)) != hipSuccess) return hip_fail(e, "fork write");
+  if ((e = hipStreamWaitValue64(corun->prefill, f, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
+    return hip_fail(e, "fork wait");
+  if ((e = hipStreamWaitValue64(corun->decode, f, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
+    return hip_fail(e, "fork wait");
   timing_begin_step(corun);
   st = timed_phase(corun, 0, has_pre, corun->prefill, pre);
   if (st != FLEX_OK) return st;
   st = timed_phase(corun, 1, has_dec, corun->decode, dec);
   if (st != FLEX_OK) return st;
   timing_end_step(corun);
-  if ((e = hipEventRecord(corun->join_p, corun->prefill)) != hipSuccess) return hip_fail(e, "join record");
-  if ((e = hipEventRecord(corun->join_d, corun->decode)) != hipSuccess) return hip_fail(e, "join record");
-  if ((e = hipStreamWaitEvent(s, corun->join_p, 0)) != hipSuccess) return hip_fail(e, "join wait");
-  if ((e = hipStreamWaitEvent(s, corun->join_d, 0)) != hipSuccess) return hip_fail(e, "join wait");
+  if ((e = hipStreamWriteValue64(corun->prefill, f + 1, step, 0)) != hipSuccess) return hip_fail(e, "join write");
+  if ((e = hipStreamWriteValue64(corun->decode, f + 2, step, 0)) != hipSuccess) return hip_fail(e, "join write");
+  if ((e = hipStreamWaitValue64(s, f + 1, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
+    return hip_fail(e, "join wait");
+  if ((e = hipStreamWaitValue64(s, f + 2, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
+    return hip_fail(e, "join wait");
   return FLEX_OK;
 }
 
@@ -245,17 +259,20 @@ extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, f
   hipDeviceProp_t prop;
   if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
   const int total = prop.multiProcessorCount;
-  if (cus_prefill <= 0 || cus_decode <= 0 || cus_prefill % 64 || cus_decode % 64 || cus_prefill + cus_decode > total ||
-      total % 256)
-    return set_error(FLEX_ERR_UNSUPPORTED, "co-run CU counts must be positive multiples of 64 summing to at most " +
-                                               std::to_string(total) + " on a device whose CU count is a multiple of 256");
+  if (total % 256)
+    return set_error(FLEX_ERR_UNSUPPORTED, "co-run needs a device whose CU count is a multiple of 256");
+  const int per_eighth = total / 8;
+  if (cus_prefill <= 0 || cus_decode <= 0 || cus_prefill % per_eighth || cus_decode % per_eighth ||
+      cus_prefill + cus_decode > total)
+    return set_error(FLEX_ERR_UNSUPPORTED, "co-run CU counts must be positive multiples of " +
+                                               std::to_string(per_eighth) + " summing to at most " +
+                                               std::to_string(total));
   const int words = (total + 31) / 32;
   uint32_t mask_p[64], mask_d[64];
   if (words > 64) return set_error(FLEX_ERR_UNSUPPORTED, "too many CUs");
-  // With 256 CUs a quarter is 64 units; decode takes the low quarters.
-  const int per_quarter = total / 4;
-  build_mask(0, cus_decode / per_quarter, total, mask_d, words);
-  build_mask(cus_decode / per_quarter, cus_prefill / per_quarter, total, mask_p, words);
+  // Decode takes the low eighths, prefill the next ones.
+  build_mask(0, cus_decode / per_eighth, total, mask_d, words);
+  build_mask(cus_decode / per_eighth, cus_prefill / per_eighth, total, mask_p, words);
   flex_attn_corun* c = new (std::nothrow) flex_attn_corun();
   if (!c) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
   c->device = dev;
@@ -263,9 +280,8 @@ extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, f
   c->cus_decode = cus_decode;
   if ((e = hipExtStreamCreateWithCUMask(&c->prefill, words, mask_p)) != hipSuccess ||
       (e = hipExtStreamCreateWithCUMask(&c->decode, words, mask_d)) != hipSuccess ||
-      (e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming)) != hipSuccess ||
-      (e = hipEventCreateWithFlags(&c->join_p, hipEventDisableTiming)) != hipSuccess ||
-      (e = hipEventCreateWithFlags(&c->join_d, hipEventDisableTiming)) != hipSuccess) {
+      (e = hipMalloc(reinterpret_cast<void**>(&c->flags), 3 * sizeof(uint64_t))) != hipSuccess ||
+      (e = hipMemset(c->flags, 0, 3 * sizeof(uint64_t))) != hipSuccess) {
     const int st = hip_fail(e, "co-run stream/event creation");
     flex_attn_corun_destroy(c);
     return st;
@@ -279,9 +295,10 @@ extern "C" void flex_attn_corun_destroy(flex_attn_corun_t* c) {
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
   if (c->prefill) (void)hipStreamDestroy(c->prefill);
   if (c->decode) (void)hipStreamDestroy(c->decode);
-  if (c->fork) (void)hipEventDestroy(c->fork);
-  if (c->join_p) (void)hipEventDestroy(c->join_p);
-  if (c->join_d) (void)hipEventDestroy(c->join_d);
+  if (c->flags) {
+    (void)hipDeviceSynchronize();   // no stream may still wait on the counters
+    (void)hipFree(c->flags);
+  }
   delete c;
 }
 

@@ -542,8 +542,20 @@ void rowpar_kernel(AttnParams p) {
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
-  // Decode pieces launch longest first; prefill tiles are listed that way.
-  const int32_t* it = p.items + 8 * (MODE == kDecodeLatent ? p.order[blockIdx.x] : int(blockIdx.x));
+  // Work-group -> (item, column). Decode pieces launch longest first; prefill
+  // tiles are listed that way. Grouped-query prefill with a column count
+  // dividing 8 runs a 1-D grid in which work-group id sits on XCD id % 8
+  // (round-robin dispatch) and serves column (id % 8) % grid_y: every XCD
+  // then reads the K/V of one KV head only, which its L2 can hold, instead
+  // of every head's.
+  int item = int(blockIdx.x), col = int(blockIdx.y);
+  if (MODE == kPrefillGrouped && p.xcd_remap) {
+    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
+    col = x % p.grid_y;
+    item = j * (8 / p.grid_y) + x / p.grid_y;
+    if (item >= p.n_items) return;
+  }
+  const int32_t* it = p.items + 8 * (MODE == kDecodeLatent ? p.order[item] : item);
   const int seq = it[0];
   const int L = p.seq_lens[seq];
   const int q0 = p.qsl[seq];
@@ -561,7 +573,7 @@ void rowpar_kernel(AttnParams p) {
   if constexpr (MODE == kDecodeLatent) {
     key_begin = it[3];
     key_end = min(it[4], L);
-    const int hg = blockIdx.y;
+    const int hg = col;
     head_kv = (hg * p.rows_per_wg) / p.G;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -574,7 +586,7 @@ void rowpar_kernel(AttnParams p) {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
     key_end = it[4];
-    const int h = blockIdx.y;
+    const int h = col;
     head_kv = h / p.G;
     const int wr0 = r0 + w * RB * 16;   // first row of the wave
     wave_on = wr0 < r1;
@@ -594,8 +606,8 @@ void rowpar_kernel(AttnParams p) {
     key_end = it[4];
     constexpr int HPW = NW / TB;                       // query heads per work-group
     const int chunks = (p.G + HPW - 1) / HPW;
-    head_kv = blockIdx.y / chunks;
-    const int hl = (blockIdx.y % chunks) * HPW + w / TB;   // query head within the group
+    head_kv = col / chunks;
+    const int hl = (col % chunks) * HPW + w / TB;   // query head within the group
     const int wr0 = r0 + (w % TB) * RB * 16;               // first row of the wave
     wave_on = hl < p.G && wr0 < r1;
     const int h = head_kv * p.G + (hl < p.G ? hl : 0);
@@ -930,7 +942,7 @@ void rowpar_kernel(AttnParams p) {
     }
   } else {
     const int nspl = it[2];
-    const int hg = blockIdx.y;
+    const int hg = col;
     const int W = gridDim.y;
     const int rows = p.rows_per_wg;
     const int64_t out_row0 = int64_t(q0) * p.Hq + int64_t(hg) * rows;
@@ -1066,8 +1078,16 @@ static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid,
 
 template <int P>
 static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 grid, hipStream_t stream) {
-  if (dqk == 128) return launch_prefill_grouped<128, P>(p, bm, grid, stream);
-  if (dqk == 64) return launch_prefill_grouped<64, P>(p, bm, grid, stream);
+  if (dqk == 128 || dqk == 64) {
+    // XCD-aware 1-D grid when the column count divides 8 (see rowpar_kernel).
+    AttnParams q = p;
+    if (8 % p.grid_y == 0) {
+      q.xcd_remap = 1;
+      grid = dim3((p.n_items * p.grid_y + 7) / 8 * 8, 1);
+    }
+    return dqk == 128 ? launch_prefill_grouped<128, P>(q, bm, grid, stream)
+                      : launch_prefill_grouped<64, P>(q, bm, grid, stream);
+  }
   if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   return hipErrorInvalidValue;
 }

@@ -94,7 +94,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : (sh.head_dim_qk == 576 ? 4 : 1);
   const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
-  const int64_t granule = o.split_granule ? o.split_granule : 64;
+  const int64_t granule = o.split_granule ? o.split_granule : 32;
   const int32_t bm = o.bm ? o.bm : (latent ? 64 : 32);
   if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");

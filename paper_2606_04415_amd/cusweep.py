@@ -1,0 +1,118 @@
+"""CU sweep and co-run split optimiser for one mixed batch on one MI355X.
+
+The paper's starting observation (Sec. 2, Fig. 2) is that decode attention
+stops gaining bandwidth well before it has every compute unit, while prefill
+keeps scaling with compute units; phase-aware co-location gives each phase
+the share it can use. This tool measures both curves on this device with the
+library's own CU-masked streams, then the co-run step time of every split,
+and reports the best split next to serial execution:
+
+    python -m paper_2606_04415_amd.cusweep --workload mixed
+
+Decode is timed alone on a stream masked to c CUs with a plan partitioned for
+c CUs; prefill alone on c CUs; a co-run step on (256 - c_d, c_d). Counts step
+in eighths of the device (the co-run mask granularity). Prints one JSON
+object on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+
+
+def _time_on(stream_handle, fn, reps, warmup=3):
+    import torch
+    s = torch.cuda.ExternalStream(stream_handle) if stream_handle else torch.cuda.current_stream()
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for i in range(reps):
+        fn(i)
+    e1.record(s)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps * 1e3   # us
+
+
+def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0):
+    import torch
+    from . import flexattn as F
+    from .workloads import WORKLOADS, algorithmic_work, make_batch
+
+    w = WORKLOADS[workload]
+    b = make_batch(w, seed=seed, poison=False)
+    work = algorithmic_work(w, b.extra["ns"], b.extra["ls"])
+    dev = torch.device("cuda:0")
+    q = b.q.to(dev)
+    kv = [(b.k_cache.to(dev), b.v_cache.to(dev) if b.v_cache is not None else None) for _ in range(max(1, pools))]
+    bt, sl, qsl = b.block_table.to(dev), b.seq_lens.to(dev), b.query_start_loc.to(dev)
+    shape = F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v, w.page_size,
+                         w.sm_scale, w.v_aliases_k)
+    total = torch.cuda.get_device_properties(0).multi_processor_count
+    step = total // 8
+    counts = list(range(step, total + 1, step))
+
+    def plan_for(cus_decode):
+        pa = F.PagedAttention(shape, F.make_opts(cus_decode=cus_decode), b.query_start_loc.tolist(),
+                              b.seq_lens.tolist(), b.block_table.shape[1])
+        out, _ = pa.alloc_out(q)
+        return pa, [pa.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+
+    dec_bytes, pre_flops = work["decode"]["bytes"], work["prefill"]["flops"]
+    res = {"workload": workload, "cus_total": total, "decode_bytes": dec_bytes, "prefill_flops": pre_flops,
+           "decode": {}, "prefill": {}, "corun_step_us": {}}
+    for c in counts:
+        pa, args = plan_for(c if c < total else 0)
+        corun_d = F.Corun(total - c, c) if c < total else None
+        corun_p = F.Corun(c, total - c) if c < total else None
+        sd = corun_d.streams()[1] if corun_d else None
+        sp = corun_p.streams()[0] if corun_p else None
+        if dec_bytes:
+            us = _time_on(sd, lambda i=0: F.flex_attn_decode(pa.plan, args[i % len(args)], stream=sd), reps)
+            res["decode"][c] = {"us": round(us, 2), "GBps": round(dec_bytes / (us * 1e-6) / 1e9, 1)}
+        if pre_flops:
+            us = _time_on(sp, lambda i=0: F.flex_attn_prefill(pa.plan, args[i % len(args)], stream=sp), reps)
+            res["prefill"][c] = {"us": round(us, 2), "TFLOPs": round(pre_flops / (us * 1e-6) / 1e12, 1)}
+        for cr in (corun_d, corun_p):
+            if cr:
+                cr.close()
+        print(f"cus {c}: decode {res['decode'].get(c)} prefill {res['prefill'].get(c)}", file=sys.stderr, flush=True)
+    if dec_bytes and pre_flops:
+        # steps issued from a stream of their own (the legacy default stream
+        # would synchronize with the co-run streams at every step)
+        caller = torch.cuda.Stream()
+        cs = caller.cuda_stream
+        for cd in counts[:-1]:
+            pa, args = plan_for(cd)
+            cr = F.Corun(total - cd, cd)
+            us = _time_on(cs, lambda i=0: F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_CORUN,
+                                                             stream=cs, corun=cr), reps)
+            cr.close()
+            res["corun_step_us"][cd] = round(us, 2)
+            print(f"co-run prefill {total - cd} / decode {cd}: {us:.1f} us", file=sys.stderr, flush=True)
+        pa, args = plan_for(0)
+        res["serial_us"] = round(_time_on(cs, lambda i=0: F.flex_attn_mixed(pa.plan, args[i % len(args)],
+                                                                            F.FLEX_MODE_SERIAL, stream=cs), reps), 2)
+        best = min(res["corun_step_us"], key=res["corun_step_us"].get)
+        res["best_split"] = {"cus_prefill": total - best, "cus_decode": best, "us": res["corun_step_us"][best],
+                             "speedup_vs_serial": round(res["serial_us"] / res["corun_step_us"][best], 4)}
+        # what the phase curves alone predict: max of the two phase times per split
+        pred = {cd: max(res["decode"][cd]["us"], res["prefill"][total - cd]["us"]) for cd in counts[:-1]}
+        res["predicted_step_us"] = {cd: round(v, 2) for cd, v in pred.items()}
+        res["predicted_best_cus_decode"] = min(pred, key=pred.get)
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--workload", default="mixed")
+    ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over repetitions")
+    args = ap.parse_args()
+    print(json.dumps(sweep(args.workload, args.reps, args.pools)), flush=True)
+
+
+if __name__ == "__main__":
+    main()
