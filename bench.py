@@ -54,18 +54,22 @@ def cpu_baseline(b, seconds_target=15.0):
         if time.perf_counter() - t0 > seconds_target / 2:
             break
     t_dec = time.perf_counter() - t0
-    # prefill: rows spread over each chunk, all heads
+    # prefill: groups of 32 rows spread evenly over each chunk, all heads,
+    # until the rest of the time budget is spent
     t0 = time.perf_counter()
+    budget = max(seconds_target / 2, seconds_target - t_dec)
     for s in pre:
         n, L = qsl[s + 1] - qsl[s], ls[s]
-        rows = list(range(0, n, max(1, n // 32)))
-        picks = [(s, i) for i in rows]
-        OA.attention_rows(b.q, b.k_cache, b.v_cache, b.block_table, b.seq_lens, b.query_start_loc,
-                          w.sm_scale, picks, **kw)
-        keys_pre_sample += sum(L - n + i + 1 for i in rows)
-        n_pre_rows += len(rows)
-        if time.perf_counter() - t0 > seconds_target / 2:
-            break
+        stride = max(1, n // 32)
+        ts = time.perf_counter()
+        for off in range(stride):
+            rows = list(range(off, n, stride))
+            OA.attention_rows(b.q, b.k_cache, b.v_cache, b.block_table, b.seq_lens, b.query_start_loc,
+                              w.sm_scale, [(s, i) for i in rows], **kw)
+            keys_pre_sample += sum(L - n + i + 1 for i in rows)
+            n_pre_rows += len(rows)
+            if time.perf_counter() - ts > budget / max(1, len(pre)):
+                break
     t_pre = time.perf_counter() - t0
     keys_dec_all = sum(ls[s] for s in dec)
     keys_pre_all = sum(sum(ls[s] - (qsl[s + 1] - qsl[s]) + i + 1 for i in range(qsl[s + 1] - qsl[s])) for s in pre)
@@ -138,6 +142,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run plain copies of known size (for scaling memory counters)")
+    ap.add_argument("--counter-pass", action="store_true",
+                    help="only issue the co-run plan's phases one after the other, untimed: the launches a "
+                         "co-run step makes, for counter collection (which serialises dispatches and so "
+                         "cannot pass the co-run streams' value waits)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -208,6 +216,14 @@ def main():
         pre, dec = corun.timing_read()
         return ms, wall, sum(pre) / len(pre), sum(dec) / len(dec)
 
+    if args.counter_pass:
+        for i in range(args.warmup + args.steps):
+            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], F.FLEX_MODE_SERIAL, stream=caller.cuda_stream)
+        torch.cuda.synchronize()
+        corun.close()
+        print(json.dumps({"counter_pass": True, "steps": args.warmup + args.steps, "cus_decode_plan": cd}), flush=True)
+        return
+
     log(f"co-run: {args.warmup} warmup + {args.steps} timed steps")
     c_ms, c_wall, c_pre, c_dec = timed(F.FLEX_MODE_CORUN, args.steps, args.warmup)
     log(f"co-run step {c_ms * 1e3:.1f} us (prefill {c_pre * 1e3:.1f} us, decode {c_dec * 1e3:.1f} us)")
@@ -224,20 +240,23 @@ def main():
 
     dec_bytes = work["decode"]["bytes"]
     pre_flops = work["prefill"]["flops"]
-    # dominant kernel: the one with the larger share of the co-run step
+    # dominant kernel: the one with the larger share of the co-run step;
+    # frac_of_cu_share prices it against the peak of the CUs its stream holds
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
     if dec_bytes and (not pre_flops or c_dec >= c_pre):
         achieved = dec_bytes / (c_dec * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode"),
                 "kernel": "decode_gqa_kernel" if w.head_dim_qk != 576 else "rowpar_kernel (latent decode)",
                 "algorithmic_bytes_per_launch": dec_bytes, "avg_launch_us": round(c_dec * 1e3, 2),
-                "cus": cd}
+                "cus": cd, "frac_of_cu_share": round(achieved / (HBM_PEAK_GBPS * cd / n_cus), 4)}
     else:
         achieved = pre_flops / (c_pre * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(w.name, "prefill"),
                 "kernel": "rowpar_kernel (prefill)", "algorithmic_flops_per_launch": pre_flops,
-                "avg_launch_us": round(c_pre * 1e3, 2), "cus": cp}
+                "avg_launch_us": round(c_pre * 1e3, 2), "cus": cp,
+                "frac_of_cu_share": round(achieved / (BF16_PEAK_TFLOPS * cp / n_cus), 4)}
 
     result = {
         "metric": METRIC, "value": round(c_ms * 1e3, 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
