@@ -36,7 +36,7 @@ def _time_on(stream_handle, fn, reps, warmup=3):
     return e0.elapsed_time(e1) / reps * 1e3   # us
 
 
-def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0):
+def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0, counts=None, corun: bool = True):
     import torch
     from . import flexattn as F
     from .workloads import WORKLOADS, algorithmic_work, make_batch
@@ -52,7 +52,7 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
                          w.sm_scale, w.v_aliases_k)
     total = torch.cuda.get_device_properties(0).multi_processor_count
     step = total // 8
-    counts = list(range(step, total + 1, step))
+    counts = sorted(counts) if counts else list(range(step, total + 1, step))
 
     def plan_for(cus_decode):
         pa = F.PagedAttention(shape, F.make_opts(cus_decode=cus_decode), b.query_start_loc.tolist(),
@@ -79,12 +79,12 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
             if cr:
                 cr.close()
         print(f"cus {c}: decode {res['decode'].get(c)} prefill {res['prefill'].get(c)}", file=sys.stderr, flush=True)
-    if dec_bytes and pre_flops:
+    if dec_bytes and pre_flops and corun:
         # steps issued from a stream of their own (the legacy default stream
         # would synchronize with the co-run streams at every step)
         caller = torch.cuda.Stream()
         cs = caller.cuda_stream
-        for cd in counts[:-1]:
+        for cd in [c for c in counts if c < total]:
             pa, args = plan_for(cd)
             cr = F.Corun(total - cd, cd)
             us = _time_on(cs, lambda i=0: F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_CORUN,
@@ -99,9 +99,11 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
         res["best_split"] = {"cus_prefill": total - best, "cus_decode": best, "us": res["corun_step_us"][best],
                              "speedup_vs_serial": round(res["serial_us"] / res["corun_step_us"][best], 4)}
         # what the phase curves alone predict: max of the two phase times per split
-        pred = {cd: max(res["decode"][cd]["us"], res["prefill"][total - cd]["us"]) for cd in counts[:-1]}
+        pred = {cd: max(res["decode"][cd]["us"], res["prefill"][total - cd]["us"]) for cd in res["corun_step_us"]
+                if total - cd in res["prefill"]}
         res["predicted_step_us"] = {cd: round(v, 2) for cd, v in pred.items()}
-        res["predicted_best_cus_decode"] = min(pred, key=pred.get)
+        if pred:
+            res["predicted_best_cus_decode"] = min(pred, key=pred.get)
     return res
 
 
@@ -110,8 +112,11 @@ def main():
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over repetitions")
+    ap.add_argument("--cus", default="", help="comma-separated CU counts (default: every eighth of the device)")
+    ap.add_argument("--no-corun", action="store_true", help="phase curves only")
     args = ap.parse_args()
-    print(json.dumps(sweep(args.workload, args.reps, args.pools)), flush=True)
+    counts = [int(c) for c in args.cus.split(",") if c] or None
+    print(json.dumps(sweep(args.workload, args.reps, args.pools, counts=counts, corun=not args.no_corun)), flush=True)
 
 
 if __name__ == "__main__":
