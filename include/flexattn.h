@@ -79,11 +79,11 @@ typedef struct flex_attn_shape {
 typedef struct flex_attn_plan_opts {
   int32_t cus_total;          /* [256] */
   int32_t cus_decode;         /* [0 = all CUs] */
-  int32_t bm;                 /* prefill rows per tile: 16 or 32 [32]; 64 for 576/512 */
+  int32_t bm;                 /* prefill rows per tile: 16 or 32 [32]; 64 or 128 [128] for 576/512 */
   int32_t min_split_tokens;   /* shortest balanced decode range, in keys [256] */
   int32_t max_splits;         /* accepted and ignored (must be >= 0) */
   int32_t wg_per_cu;          /* decode work-groups aimed at per CU
-                                 [1 grouped-query, 4 for 576/512] */
+                                 [1 grouped-query, 2 for 576/512] */
   int32_t split_granule;      /* co-run split granularity in CUs [32] */
   double hbm_gbps;            /* cost model: device HBM bandwidth [8000] */
   double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws [60] */

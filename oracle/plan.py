@@ -17,8 +17,8 @@ the contract is:
   all decode sequences, concatenated in batch order, form a list of
   T = sum_s P_s pages; W = work-groups per key range (grouped-query
   attention: one per group of up to 8 KV heads, W = ceil(Hkv / 8), so a
-  work-group reads whole slot rows; the 576/512 latent layout: Hq / 64). The
-  list is cut into
+  work-group reads whole slot rows; the 576/512 latent layout: Hq / 128 when
+  128 divides Hq, else Hq / 64). The list is cut into
   R = max(1, min(floor(cus_decode * wg_per_cu / W), floor(T / min_pps)),
   ceil(T / 8192)) ranges, range r = pages [floor(r T / R), floor((r + 1) T / R)),
   min_pps = ceil(min_split_tokens / P). A piece is the non-empty overlap of a
@@ -31,8 +31,8 @@ the contract is:
   the piece count), and a launch order of the pieces for one-work-group-per-
   piece launches lists them by key count descending, ties by slot.
   max_splits is accepted and ignored.
-* prefill tiles of BM rows (BM 32 by default for grouped-query heads, 64 for
-  the latent layout): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
+* prefill tiles of BM rows (BM 32 by default for grouped-query heads, 128 for
+  the latent layout, which also takes 64): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
   ordered by key_end descending, then sequence, then tile. Each tile is served
   by Hkv * ceil(G / 8) work-groups (grouped-query) or Hq (latent).
 * co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
@@ -74,10 +74,10 @@ class Shape:
 class Opts:
     cus_total: int = 0           # 0 -> 256
     cus_decode: int = 0          # 0 -> all; -1 -> cost model
-    bm: int = 0                  # 0 -> 32 (64 for the 576/512 layout)
+    bm: int = 0                  # 0 -> 32 (128 for the 576/512 layout)
     min_split_tokens: int = 0    # 0 -> 256
     max_splits: int = 0          # 0 -> 32
-    wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 4 (576/512 latent layout)
+    wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 2 (576/512 latent layout)
     split_granule: int = 0       # 0 -> 32
     hbm_gbps: float = 0.0        # 0 -> 8000
     decode_gbps_per_cu: float = 0.0   # 0 -> 60
@@ -91,7 +91,8 @@ class PlanResult:
     info: Optional[dict] = None
 
 
-MLA_ROWS_PER_WG = 64
+MLA_ROWS_PER_WG = 64        # latent heads must be a multiple of this
+MLA_ROWS_PER_WG_WIDE = 128  # latent decode work-group rows when they divide Hq
 MAX_RANGE_PAGES = 8192
 
 
@@ -123,17 +124,17 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         return PlanResult(ERR_UNSUPPORTED)
     # --- option checks / defaults
     cus_total = o.cus_total or 256
-    wg_per_cu = o.wg_per_cu or (4 if sh.head_dim_qk == 576 else 1)
+    wg_per_cu = o.wg_per_cu or (2 if sh.head_dim_qk == 576 else 1)
     max_splits = o.max_splits or 32
     min_tokens = o.min_split_tokens or 256
     granule = o.split_granule or 32
     mla = sh.head_dim_qk == 576
-    bm = o.bm or (64 if mla else 32)
+    bm = o.bm or (128 if mla else 32)
     if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:
         return PlanResult(ERR_INVALID_ARG)
     if o.cus_decode < -1 or o.cus_decode > cus_total:
         return PlanResult(ERR_INVALID_ARG)
-    if (mla and bm != 64) or (not mla and bm not in (16, 32)):
+    if (mla and bm not in (64, 128)) or (not mla and bm not in (16, 32)):
         return PlanResult(ERR_UNSUPPORTED)
     # --- integer metadata checks
     if max_pages_per_seq < 0:
@@ -150,8 +151,9 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         return PlanResult(ERR_INVALID_ARG)
 
     heads_per_wg = min(sh.num_kv_heads, 8)
-    W = (sh.num_q_heads // MLA_ROWS_PER_WG) if mla else cdiv(sh.num_kv_heads, heads_per_wg)
-    rows_per_wg = MLA_ROWS_PER_WG if mla else heads_per_wg * (sh.num_q_heads // sh.num_kv_heads)
+    mla_rows = MLA_ROWS_PER_WG_WIDE if sh.num_q_heads % MLA_ROWS_PER_WG_WIDE == 0 else MLA_ROWS_PER_WG
+    W = (sh.num_q_heads // mla_rows) if mla else cdiv(sh.num_kv_heads, heads_per_wg)
+    rows_per_wg = mla_rows if mla else heads_per_wg * (sh.num_q_heads // sh.num_kv_heads)
     dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1]
     pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= 2]
 

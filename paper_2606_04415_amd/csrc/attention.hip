@@ -901,7 +901,9 @@ void rowpar_kernel(AttnParams p) {
 
     const int n_steady = wave_on ? max(0, min(max(0, wave_full - wk0) / BN, ntiles - (NS - 1))) : 0;
     int kt = 0;
-    for (; kt < n_steady; ++kt) {
+    // (The 576-wide latent rows take every tile through the general loop:
+    // a second copy of their compute would not fit two waves per SIMD.)
+    for (; !VALIAS && kt < n_steady; ++kt) {
       wait_vmem<(NS - 2) * C::NI>();
       lds_barrier();
       issue(wk0 + (kt + NS - 1) * BN, (kt + NS - 1) % NS, pt_base);
@@ -1039,7 +1041,10 @@ static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t
   switch (dqk) {
     case 128: return p16 ? launch_decode_gqa<128, 16>(p, stream) : launch_decode_gqa<128, 64>(p, stream);
     case 64: return p16 ? launch_decode_gqa<64, 16>(p, stream) : launch_decode_gqa<64, 64>(p, stream);
-    case 576:   // one work-group per (piece, group of 64 heads)
+    case 576:   // one work-group per (piece, group of 128 or 64 heads), a wave per 16 heads
+      if (p.rows_per_wg == 128)
+        return p16 ? launch_rowpar<576, 512, 8, 1, 32, true, kDecodeLatent, 16, 3>(p, pieces, stream)
+                   : launch_rowpar<576, 512, 8, 1, 32, true, kDecodeLatent, 64, 3>(p, pieces, stream);
       return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16, 3>(p, pieces, stream)
                  : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64, 3>(p, pieces, stream);
     default: return hipErrorInvalidValue;
@@ -1088,6 +1093,8 @@ static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 gr
     return dqk == 128 ? launch_prefill_grouped<128, P>(q, bm, grid, stream)
                       : launch_prefill_grouped<64, P>(q, bm, grid, stream);
   }
+  // Latent prefill: one work-group per (tile, query head), a wave per 16 rows.
+  if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   return hipErrorInvalidValue;
 }

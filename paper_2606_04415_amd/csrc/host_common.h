@@ -41,7 +41,8 @@ constexpr int64_t kMaxRangePages = 8192;
 constexpr int32_t kDecodeHeadsPerWG = 8;
 
 // Rows (query heads) one decode work-group owns in the 576/512 layout.
-constexpr int kLatentRowsPerWG = 64;
+constexpr int kLatentRowsPerWG = 64;       // latent heads must be a multiple of this
+constexpr int kLatentRowsPerWGWide = 128;  // heads per latent decode work-group when they divide
 
 int set_error(int status, const std::string& msg);
 void clear_error();

@@ -91,17 +91,17 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t cus_total = o.cus_total ? o.cus_total : 256;
   // Grouped-query decode: one work-group per CU walking a long range measured
   // fastest; latent decode launches one work-group per piece, so more pieces.
-  const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : (sh.head_dim_qk == 576 ? 4 : 1);
+  const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : (sh.head_dim_qk == 576 ? 2 : 1);
   const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
   const int64_t granule = o.split_granule ? o.split_granule : 32;
-  const int32_t bm = o.bm ? o.bm : (latent ? 64 : 32);
+  const int32_t bm = o.bm ? o.bm : (latent ? 128 : 32);
   if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
   if (o.cus_decode < -1 || o.cus_decode > cus_total)
     return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
-  if (latent ? bm != 64 : (bm != 16 && bm != 32))
-    return set_error(FLEX_ERR_UNSUPPORTED, "bm must be 16 or 32 (grouped-query) or 64 (latent layout)");
+  if (latent ? (bm != 64 && bm != 128) : (bm != 16 && bm != 32))
+    return set_error(FLEX_ERR_UNSUPPORTED, "bm must be 16 or 32 (grouped-query) or 64 or 128 (latent layout)");
   if (max_pages_per_seq < 0) return set_error(FLEX_ERR_INVALID_ARG, "max_pages_per_seq < 0");
   if (num_seqs > 0 && qsl[0] != 0) return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc[0] != 0");
 
@@ -118,14 +118,17 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
 
   // Decode work-groups per key range: one per group of up to 8 KV heads for
   // grouped-query attention (a work-group then reads whole slot rows, which
-  // spreads its stream over every memory channel), Hq / 64 for the latent layout.
+  // spreads its stream over every memory channel); for the latent layout one
+  // per 128 query heads (eight waves of 16 heads share each key tile), or per
+  // 64 when 128 does not divide Hq.
   const int32_t heads_per_wg = std::min(sh.num_kv_heads, kDecodeHeadsPerWG);
-  const int32_t W = latent ? sh.num_q_heads / kLatentRowsPerWG : int32_t(cdiv(sh.num_kv_heads, heads_per_wg));
+  const int32_t latent_rows = sh.num_q_heads % kLatentRowsPerWGWide == 0 ? kLatentRowsPerWGWide : kLatentRowsPerWG;
+  const int32_t W = latent ? sh.num_q_heads / latent_rows : int32_t(cdiv(sh.num_kv_heads, heads_per_wg));
   // Prefill work-groups per tile: one per query head (latent layout), or one per
   // KV head and group of up to 8 of its query heads (grouped-query layout).
   const int32_t G = sh.num_q_heads / sh.num_kv_heads;
   const int32_t pre_grid_y = latent ? sh.num_q_heads : sh.num_kv_heads * ((G + 7) / 8);
-  const int32_t rows_per_wg = latent ? kLatentRowsPerWG : heads_per_wg * (sh.num_q_heads / sh.num_kv_heads);
+  const int32_t rows_per_wg = latent ? latent_rows : heads_per_wg * (sh.num_q_heads / sh.num_kv_heads);
   std::vector<int32_t> dec, pre;
   for (int32_t s = 0; s < num_seqs; ++s) {
     const int32_t n = qsl[s + 1] - qsl[s];

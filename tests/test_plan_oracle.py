@@ -62,9 +62,13 @@ def check_invariants(sh, opts, qsl, ls, maxp):
     # decode: R balanced ranges over the concatenated pages of the decode sequences
     T = sum(-(-ls[s] // P) for s in dec)
     W = b[7]
+    if sh.head_dim_qk == 576:   # a latent work-group takes 128 heads when they divide Hq, else 64
+        assert W == sh.num_q_heads // (128 if sh.num_q_heads % 128 == 0 else 64)
+    else:                       # one work-group per 8 KV heads
+        assert W == -(-sh.num_kv_heads // 8)
     if dec:
         min_pps = -(-(o.min_split_tokens or 256) // P)
-        wgpc = o.wg_per_cu or (4 if sh.head_dim_qk == 576 else 1)
+        wgpc = o.wg_per_cu or (2 if sh.head_dim_qk == 576 else 1)
         assert R == max(1, min(b[12] * wgpc // W, T // min_pps), -(-T // 8192))
         assert ranges[0] == 0 and ranges[-1] == nd
         assert all(x < y for x, y in zip(ranges, ranges[1:]))          # no empty range
