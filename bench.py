@@ -128,6 +128,31 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": reps}), flush=True)
 
 
+def time_kv_append(b, kv, shape, steps, stream):
+    """The step's new tokens appended to the paged pool (not part of `value`):
+    average time per append and its HBM rate (rows read once, written once)."""
+    import torch
+    from paper_2606_04415_amd import flexattn as F
+    from paper_2606_04415_amd.workloads import make_append
+    a = make_append(b, seed=1)
+    dev = torch.device("cuda:0")
+    k_new = a.k_new.to(dev)
+    v_new = a.v_new.to(dev) if a.v_new is not None else None
+    sm = a.slot_mapping.to(dev)
+    args = [F.make_append_args(k_new, v_new, sm, k, v) for k, v in kv]
+    for i in range(3):
+        F.flex_attn_kv_append(shape, args[i % len(args)], stream=stream.cuda_stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(steps):
+        F.flex_attn_kv_append(shape, args[i % len(args)], stream=stream.cuda_stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / steps * 1e3
+    nbytes = 2 * (k_new.numel() + (v_new.numel() if v_new is not None else 0)) * 2
+    return {"tokens": int(sm.numel()), "us": round(us, 2), "GBps": round(nbytes / (us * 1e-6) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,7 +176,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: this path has no multi-GPU component "
-              "(sequences shard across GPUs with no exchange; see the design notes)", file=sys.stderr)
+              "(sequences shard across GPUs with no exchange between them)", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration:
@@ -278,6 +303,7 @@ def main():
             result["prefill_TFLOPs_all_cus"] = round(pre_flops / (s_pre * 1e-3) / 1e12, 2)
     result["bound_us"] = round(max((dec_bytes + work["prefill"]["bytes"]) / (HBM_PEAK_GBPS * 1e3),
                                    (pre_flops + work["decode"]["flops"]) / (BF16_PEAK_TFLOPS * 1e6)), 1)
+    result["kv_append"] = time_kv_append(b, kv, shape, args.steps, caller)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)

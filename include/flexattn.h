@@ -17,17 +17,19 @@
  *   (natural log).
  *
  * The paper writes none of this down (it defines no kernel); the definition
- * is textbook scaled dot-product attention, and every reading of a detail the
- * paper leaves open (layout, causal alignment, head mapping, rounding) is
- * listed with its reason in the repository's design notes.
+ * is textbook scaled dot-product attention. Where the paper leaves a detail
+ * open, this library reads it as: pages laid out [page][slot][kv_head][dim];
+ * bottom-right causal alignment; consecutive query heads share a KV head;
+ * bf16 inputs, fp32 accumulation and softmax, bf16 output rounded to nearest
+ * even.
  *
  * Conventions for every call:
  *  - Every call returns an int status (FLEX_OK or a negative FLEX_ERR_*);
  *    nothing throws across this boundary. flex_attn_last_error() returns a
  *    thread-local text describing the last failure on the calling thread.
- *  - Device memory is owned by the caller; the library never allocates device
- *    memory. Host plan objects and co-run stream pairs are owned by the
- *    library until their destroy call.
+ *  - Device memory is owned by the caller; the library allocates device
+ *    memory only for a co-run pair's 24-byte counter buffer. Host plan objects
+ *    and co-run pairs are owned by the library until their destroy call.
  *  - Run calls (decode, prefill, mixed, debug gather, workspace init) only
  *    enqueue work on the given HIP stream (a hipStream_t passed as void*;
  *    NULL is the null stream) and return; they never synchronise.
@@ -252,6 +254,44 @@ int flex_attn_debug_gather(const flex_attn_plan_t* plan, const flex_attn_args* a
 /* Zero a buffer (e.g. a workspace) on stream with a fill kernel; bytes must
  * be a multiple of 4. No run call requires it. */
 int flex_attn_workspace_init(void* workspace, size_t bytes, void* stream);
+
+/* KV append: the write side of the KV pool both phases share (Sec. 3.4,
+ * "Memory Locality": co-located prefill and decode extend and read one pool
+ * in place instead of moving KV caches between workers). Token t's key row
+ * (and value row unless the shape has v_aliases_k) is copied into slot
+ * slot_mapping[t] of the paged caches: page slot / page_size, row
+ * slot % page_size, the same addressing the attention calls read through
+ * block_table. Typically called for a step's new tokens before the step's
+ * attention, on the same stream.
+ *  k_new        bf16 [n_tokens][Hkv][d_qk]: token t's row starts at element
+ *               t * k_new_stride; the Hkv*d_qk values of a row are contiguous.
+ *  v_new        bf16 [n_tokens][Hkv][d_v] with v_new_stride; ignored (may be
+ *               NULL) when the shape has v_aliases_k.
+ *  slot_mapping int32 [n_tokens], device: a negative entry skips its token
+ *               (padding); an entry >= num_pages * page_size also skips it and
+ *               adds 1 to *bad_count when bad_count is not NULL (device int32,
+ *               not reset by the call). Two tokens given one slot leave one of
+ *               the two rows there (unspecified which).
+ *  k_cache, k_stride, v_cache, v_stride, num_pages: as in flex_attn_args; the
+ *               caches are written.
+ * Pointers and row strides must be 16-byte multiples; n_tokens >= 0 (0 launches
+ * nothing). Enqueues one kernel on stream and returns. */
+typedef struct flex_attn_append_args {
+  const void* k_new;
+  const void* v_new;
+  int64_t k_new_stride;
+  int64_t v_new_stride;
+  const int32_t* slot_mapping;
+  int64_t n_tokens;
+  void* k_cache;
+  int64_t k_stride[3];
+  void* v_cache;
+  int64_t v_stride[3];
+  int64_t num_pages;
+  int32_t* bad_count;
+} flex_attn_append_args;
+
+int flex_attn_kv_append(const flex_attn_shape* shape, const flex_attn_append_args* args, void* stream);
 
 #ifdef __cplusplus
 }

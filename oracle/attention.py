@@ -23,8 +23,7 @@ keys and values sit in fixed-size pages of a shared cache:
 With ``v_aliases_k`` (absorbed MLA) the value row of a key is the first d_v
 columns of its key row.
 
-Readings taken where the paper is silent are listed in the design doc; the ones
-that shape this code: page layout [page][slot][kv_head][dim]; bottom-right
+Readings taken where the paper is silent that shape this code: page layout [page][slot][kv_head][dim]; bottom-right
 causal alignment; consecutive query heads share a KV head; the scale is an
 explicit input; n = 0 produces no rows; bf16 inputs are widened exactly to
 fp64 and everything after that is fp64 with a two-pass softmax (no online

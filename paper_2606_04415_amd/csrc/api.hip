@@ -1,5 +1,5 @@
 // Run calls of the C ABI: argument checks, kernel parameter blocks, serial and
-// co-run launch, plan upload, debug gather and workspace fill.
+// co-run launch, plan upload, debug gather, workspace fill and KV append.
 //
 // Co-run is the one-device analog of the paper's dynamic prefill/decode
 // co-location (Sec. 3.4): the two phases of one step share the device and its
@@ -378,4 +378,47 @@ extern "C" int flex_attn_workspace_init(void* workspace, size_t bytes, void* str
     return set_error(FLEX_ERR_INVALID_ARG, "workspace must be non-NULL, 16-byte aligned, whole 4-byte words");
   const hipError_t e = launch_fill_zero(workspace, bytes, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "fill launch");
+}
+
+extern "C" int flex_attn_kv_append(const flex_attn_shape* shape, const flex_attn_append_args* a, void* stream) {
+  clear_error();
+  if (!shape || !a) return set_error(FLEX_ERR_INVALID_ARG, "shape or args is NULL");
+  if (const int st = check_shape(*shape); st != FLEX_OK) return st;
+  if (a->n_tokens < 0) return set_error(FLEX_ERR_INVALID_ARG, "n_tokens < 0");
+  if (a->n_tokens == 0) return FLEX_OK;
+  const bool has_v = !shape->v_aliases_k;
+  if (!a->k_new || !a->slot_mapping || !a->k_cache || (has_v && (!a->v_new || !a->v_cache)))
+    return set_error(FLEX_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (!aligned16(a->k_new) || !aligned16(a->k_cache) || (has_v && (!aligned16(a->v_new) || !aligned16(a->v_cache))))
+    return set_error(FLEX_ERR_INVALID_ARG, "new rows and caches must be 16-byte aligned");
+  const int64_t Hkv = shape->num_kv_heads, dk = shape->head_dim_qk, dv = shape->head_dim_v;
+  if (a->k_new_stride < Hkv * dk || (a->k_new_stride * 2) % 16 ||
+      (has_v && (a->v_new_stride < Hkv * dv || (a->v_new_stride * 2) % 16)))
+    return set_error(FLEX_ERR_INVALID_ARG, "new-row strides must cover Hkv * d and be 16-byte multiples");
+  for (int i = 0; i < 3; ++i) {
+    if (a->k_stride[i] <= 0 || (a->k_stride[i] * 2) % 16 || (has_v && (a->v_stride[i] <= 0 || (a->v_stride[i] * 2) % 16)))
+      return set_error(FLEX_ERR_INVALID_ARG, "cache strides must be positive multiples of 16 bytes");
+  }
+  if (a->k_stride[2] < dk || (has_v && a->v_stride[2] < dv))
+    return set_error(FLEX_ERR_INVALID_ARG, "cache head stride smaller than the head dimension");
+  if (a->num_pages <= 0) return set_error(FLEX_ERR_INVALID_ARG, "num_pages must be positive");
+  AppendParams p{};
+  p.k_new = static_cast<const uint16_t*>(a->k_new);
+  p.v_new = static_cast<const uint16_t*>(has_v ? a->v_new : a->k_new);
+  p.k_new_stride = a->k_new_stride;
+  p.v_new_stride = has_v ? a->v_new_stride : a->k_new_stride;
+  p.slot_mapping = a->slot_mapping;
+  p.n_tokens = a->n_tokens;
+  p.kc = CacheRef{static_cast<const uint16_t*>(a->k_cache), a->k_stride[0], a->k_stride[1], a->k_stride[2]};
+  p.vc = has_v ? CacheRef{static_cast<const uint16_t*>(a->v_cache), a->v_stride[0], a->v_stride[1], a->v_stride[2]}
+               : p.kc;
+  p.num_slots = a->num_pages * shape->page_size;
+  p.P = shape->page_size;
+  p.dk = int32_t(dk);
+  p.dv = int32_t(dv);
+  p.ck = Hkv * dk / 8;
+  p.cv = has_v ? Hkv * dv / 8 : 0;
+  p.bad_count = a->bad_count;
+  const hipError_t e = launch_kv_append(p, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "kv append launch");
 }

@@ -45,6 +45,8 @@ constexpr int kLatentRowsPerWG = 64;       // latent heads must be a multiple of
 constexpr int kLatentRowsPerWGWide = 128;  // heads per latent decode work-group when they divide
 
 int set_error(int status, const std::string& msg);
+// Validates an attention shape (sets the error text); FLEX_OK if supported.
+int check_shape(const flex_attn_shape& sh);
 void clear_error();
 
 }  // namespace flexattn

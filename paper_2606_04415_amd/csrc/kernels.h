@@ -1,4 +1,5 @@
-// Kernel parameter blocks and launchers (host-callable, defined in attention.hip).
+// Kernel parameter blocks and launchers (host-callable, defined in attention.hip
+// and kv_append.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -42,5 +43,21 @@ hipError_t launch_gather(const CacheRef& kc, const CacheRef& vc, bool has_v, con
                          int32_t L, int32_t P, int32_t Hkv, int32_t dqk, int32_t dv,
                          uint16_t* k_out, uint16_t* v_out, hipStream_t stream);
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+struct AppendParams {
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  int64_t k_new_stride, v_new_stride;   // elements per token row
+  const int32_t* slot_mapping;
+  int64_t n_tokens;
+  CacheRef kc, vc;                      // destinations (base cast back to writable)
+  int64_t num_slots;                    // num_pages * P
+  int32_t P;
+  int32_t dk, dv;                       // head dimensions of the copied rows (dv unused when ck only)
+  int64_t ck, cv;                       // 16-byte chunks per token: Hkv*dk/8 and Hkv*dv/8 (0 if aliased)
+  int32_t* bad_count;                   // optional: tokens whose slot lies outside the pool
+};
+
+hipError_t launch_kv_append(const AppendParams& a, hipStream_t stream);
 
 }  // namespace flexattn

@@ -24,7 +24,7 @@ thread_local std::string g_last_error;
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-bool supported(const flex_attn_shape& s) {
+bool supported_dims(const flex_attn_shape& s) {
   const int dq = s.head_dim_qk, dv = s.head_dim_v;
   const bool gqa = (dq == 64 && dv == 64) || (dq == 128 && dv == 128);
   const bool latent = dq == 576 && dv == 512;
@@ -35,6 +35,19 @@ bool supported(const flex_attn_shape& s) {
 }
 
 }  // namespace
+
+int check_shape(const flex_attn_shape& sh) {
+  if (sh.num_q_heads <= 0 || sh.num_kv_heads <= 0 || sh.num_q_heads % sh.num_kv_heads)
+    return set_error(FLEX_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (!std::isfinite(sh.sm_scale) || !(sh.sm_scale > 0.0f))
+    return set_error(FLEX_ERR_INVALID_ARG, "sm_scale must be finite and positive");
+  if (sh.v_aliases_k && (sh.num_kv_heads != 1 || sh.head_dim_v > sh.head_dim_qk))
+    return set_error(FLEX_ERR_INVALID_ARG, "v_aliases_k needs one KV head and head_dim_v <= head_dim_qk");
+  if (!supported_dims(sh))
+    return set_error(FLEX_ERR_UNSUPPORTED, "shape outside (64,64)/(128,128) GQA with group <= 16, "
+                                           "or (576,512) aliased latent with Hq % 64 == 0; page 16/64");
+  return FLEX_OK;
+}
 
 int set_error(int status, const std::string& msg) {
   g_last_error = msg;
@@ -74,15 +87,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   if (!qsl || (num_seqs > 0 && !seq_lens))
     return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc or seq_lens is NULL");
   const flex_attn_shape sh = *shape;
-  if (sh.num_q_heads <= 0 || sh.num_kv_heads <= 0 || sh.num_q_heads % sh.num_kv_heads)
-    return set_error(FLEX_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
-  if (!std::isfinite(sh.sm_scale) || !(sh.sm_scale > 0.0f))
-    return set_error(FLEX_ERR_INVALID_ARG, "sm_scale must be finite and positive");
-  if (sh.v_aliases_k && (sh.num_kv_heads != 1 || sh.head_dim_v > sh.head_dim_qk))
-    return set_error(FLEX_ERR_INVALID_ARG, "v_aliases_k needs one KV head and head_dim_v <= head_dim_qk");
-  if (!supported(sh))
-    return set_error(FLEX_ERR_UNSUPPORTED, "shape outside (64,64)/(128,128) GQA with group <= 16, "
-                                           "or (576,512) aliased latent with Hq % 64 == 0; page 16/64");
+  if (const int st = check_shape(sh); st != FLEX_OK) return st;
 
   flex_attn_plan_opts o;
   std::memset(&o, 0, sizeof(o));

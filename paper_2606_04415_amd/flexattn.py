@@ -30,7 +30,7 @@ EXPORTED = [
     "flex_attn_plan_export", "flex_attn_plan_upload", "flex_attn_plan_destroy", "flex_attn_decode",
     "flex_attn_prefill", "flex_attn_mixed", "flex_attn_corun_create", "flex_attn_corun_destroy",
     "flex_attn_corun_streams", "flex_attn_corun_set_timing", "flex_attn_corun_timing_read",
-    "flex_attn_debug_gather", "flex_attn_workspace_init",
+    "flex_attn_debug_gather", "flex_attn_workspace_init", "flex_attn_kv_append",
 ]
 FLEX_TIMING_RING = 1024
 
@@ -75,6 +75,13 @@ class Args(ctypes.Structure):
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
+class AppendArgs(ctypes.Structure):
+    _fields_ = [("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p), ("k_new_stride", ctypes.c_int64),
+                ("v_new_stride", ctypes.c_int64), ("slot_mapping", ctypes.c_void_p), ("n_tokens", ctypes.c_int64),
+                ("k_cache", ctypes.c_void_p), ("k_stride", ctypes.c_int64 * 3), ("v_cache", ctypes.c_void_p),
+                ("v_stride", ctypes.c_int64 * 3), ("num_pages", ctypes.c_int64), ("bad_count", ctypes.c_void_p)]
+
+
 class FlexAttnError(RuntimeError):
     def __init__(self, status: int, what: str, detail: str):
         super().__init__(f"{what}: status {status} ({detail})")
@@ -117,6 +124,7 @@ def lib():
                                               i32, ctypes.POINTER(i32)]
     L.flex_attn_debug_gather.argtypes = [vp, ctypes.POINTER(Args), i32, i32, vp, vp, vp]
     L.flex_attn_workspace_init.argtypes = [vp, sz, vp]
+    L.flex_attn_kv_append.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(AppendArgs), vp]
     for f in EXPORTED:
         if f not in ("flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan_destroy",
                      "flex_attn_corun_destroy"):
@@ -280,6 +288,34 @@ def flex_attn_workspace_init(workspace, stream=None):
     check(lib().flex_attn_workspace_init(ctypes.c_void_p(workspace.data_ptr()),
                                          workspace.numel() * workspace.element_size(), s),
           "flex_attn_workspace_init")
+
+
+def make_append_args(k_new, v_new, slot_mapping, k_cache, v_cache, bad_count=None) -> AppendArgs:
+    """AppendArgs from device tensors: k_new [n, Hkv, d_qk] / v_new [n, Hkv, d_v] with
+    contiguous rows, slot_mapping int32 [n], caches [pages, P, Hkv, d]."""
+    a = AppendArgs()
+    a.k_new = k_new.data_ptr()
+    a.k_new_stride = k_new.stride(0)
+    if v_new is not None:
+        a.v_new = v_new.data_ptr()
+        a.v_new_stride = v_new.stride(0)
+    a.slot_mapping = slot_mapping.data_ptr()
+    a.n_tokens = slot_mapping.numel()
+    a.k_cache = k_cache.data_ptr()
+    ks = k_cache.stride()
+    a.k_stride = (ctypes.c_int64 * 3)(ks[0], ks[1], ks[2])
+    vsrc = v_cache if v_cache is not None else k_cache
+    a.v_cache = v_cache.data_ptr() if v_cache is not None else None
+    vs = vsrc.stride()
+    a.v_stride = (ctypes.c_int64 * 3)(vs[0], vs[1], vs[2])
+    a.num_pages = k_cache.shape[0]
+    a.bad_count = bad_count.data_ptr() if bad_count is not None else None
+    return a
+
+
+def flex_attn_kv_append(shape: Shape, args: AppendArgs, stream=None):
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_kv_append(ctypes.byref(shape), ctypes.byref(args), s), "flex_attn_kv_append")
 
 
 class Corun:

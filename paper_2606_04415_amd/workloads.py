@@ -230,3 +230,48 @@ def algorithmic_work(w: Workload, ns: List[int], ls: List[int]) -> dict:
         out[ph]["flops"] += Hq * 2 * (dqk + dv) * pairs
         out[ph]["bytes"] += L * kv_row + n * Hq * (dqk + dv) * 2 + 4 * (-(-L // P))
     return out
+
+
+@dataclass
+class AppendBatch:
+    """New tokens' rows and their cache slots (torch CPU tensors)."""
+    k_new: torch.Tensor             # bf16 [n, Hkv, d_qk]
+    v_new: Optional[torch.Tensor]   # bf16 [n, Hkv, d_v] (None when V aliases K)
+    slot_mapping: torch.Tensor      # int32 [n]
+    n_pad: int                      # entries set to -1
+    n_out_of_range: int             # entries at or past num_pages * P
+
+
+def make_append(b: Batch, seed: int = 0, n_pad: int = 0, n_out_of_range: int = 0) -> AppendBatch:
+    """The new tokens of batch ``b`` as a serving step would append them before
+    its attention: query i of sequence s is key position L - n + i, whose slot
+    is ``block_table[s][pos // P] * P + pos % P`` (the position-to-slot map an
+    engine keeps). ``n_pad`` padding entries (-1) and ``n_out_of_range`` entries
+    past the pool are then inserted at seeded random positions.
+
+    Draw order (one torch CPU generator, seeded): k_new, v_new (skipped when V
+    aliases K) as ``randn`` rounded to bf16; then ``randperm`` of the final
+    token count to place the padding and out-of-range entries.
+    """
+    w = b.workload
+    gen = torch.Generator().manual_seed(seed)
+    ns, ls = b.extra["ns"], b.extra["ls"]
+    P = w.page_size
+    slots = []
+    for s, (n, L) in enumerate(zip(ns, ls)):
+        for i in range(n):
+            pos = L - n + i
+            slots.append(int(b.block_table[s, pos // P]) * P + pos % P)
+    extra = [-1] * n_pad + [b.num_pages * P + 7 * j for j in range(n_out_of_range)]
+    n_tot = len(slots) + len(extra)
+    k_new = torch.randn((n_tot, w.num_kv_heads, w.head_dim_qk), generator=gen).to(torch.bfloat16)
+    v_new = None
+    if not w.v_aliases_k:
+        v_new = torch.randn((n_tot, w.num_kv_heads, w.head_dim_v), generator=gen).to(torch.bfloat16)
+    order = torch.randperm(n_tot, generator=gen).tolist()
+    merged = [0] * n_tot
+    vals = slots + extra
+    for dst, src in zip(order, range(n_tot)):
+        merged[dst] = vals[src]
+    return AppendBatch(k_new=k_new, v_new=v_new, slot_mapping=torch.tensor(merged, dtype=torch.int32),
+                       n_pad=n_pad, n_out_of_range=n_out_of_range)
