@@ -293,6 +293,103 @@ typedef struct flex_attn_append_args {
 
 int flex_attn_kv_append(const flex_attn_shape* shape, const flex_attn_append_args* args, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Online co-location controller (host only, no HIP call).
+ *
+ * Sec. 3.4 "Phase-Aware Dispatch": the runtime watches (1) pending prefill and
+ * decode work, (2) recent per-phase execution times, (3) memory-bandwidth
+ * pressure, (4) decode progress and the active sequence count and (5)
+ * device utilisation, and moves the prefill/decode balance step by step:
+ * when decode is close to saturating bandwidth, more compute units would not
+ * speed it up, so prefill gets them; when decode work backs up, decode's
+ * share grows. Sec. 3.3: the per-phase profile it uses is coarse and updated
+ * continuously during execution.
+ *
+ * Here the balance is the CU split of the next co-run step (or serial
+ * execution). The controller keeps, per candidate split, a running estimate
+ * of each phase's rate in that split (decode GB/s, prefill TFLOP/s), seeded
+ * by a prior (flex_ctl_set_profile, else the cost model of the options) and
+ * updated from every observed step (exponentially weighted). For the next
+ * step it predicts each split's time, max(B / decode rate, F / prefill rate)
+ * + a co-run overhead, and serial time B / rate + F / rate, then applies the
+ * rule above among the co-run splits within `tolerance` of the best
+ * prediction: decode backlog (pending_decode_seqs >= backlog_seqs) takes the
+ * largest decode share; otherwise decode bandwidth pressure (the last
+ * observed decode rate reached sat_frac of hbm_gbps) or a prefill backlog
+ * (pending_prefill_tokens >= backlog_prefill_tokens) takes the smallest;
+ * otherwise the best prediction. Serial runs when it is predicted fastest or
+ * one phase has no work. Every explore_every-th decision tries a neighbouring
+ * split instead, so stale estimates are refreshed. Signal (5), utilisation,
+ * enters through the observations: a split whose phases finish unevenly
+ * leaves CUs idle and shows up as a slower observed rate.
+ * ---------------------------------------------------------------------- */
+typedef struct flex_ctl flex_ctl_t;
+
+/* A zero field takes the default in brackets (use a tiny positive value for
+ * a tolerance or overhead of zero). */
+typedef struct flex_ctl_opts {
+  int32_t cus_total;            /* [256] */
+  int32_t granule;              /* candidate splits are multiples [64]; must divide cus_total */
+  int32_t explore_every;        /* [16]; a negative value disables exploration */
+  int32_t backlog_seqs;         /* decode backlog that raises decode's share [256] */
+  int32_t backlog_prefill_tokens; /* prefill backlog that lowers it [8192] */
+  double alpha;                 /* weight of a new observation (0, 1] [0.25] */
+  double tolerance;             /* relative band around the best prediction [0.03] */
+  double sat_frac;              /* bandwidth-pressure threshold, fraction of hbm_gbps [0.6] */
+  double hbm_gbps;              /* [8000] */
+  double corun_overhead_us;     /* fork/join cost added to co-run predictions [10] */
+  double decode_gbps_per_cu;    /* prior when no profile is set [60] */
+  double prefill_tflops_per_cu; /* prior when no profile is set [5] */
+} flex_ctl_opts;
+
+/* Signals describing the step about to run and the queues behind it. */
+typedef struct flex_ctl_signals {
+  double decode_bytes;          /* algorithmic KV bytes of the step's decode phase (plan info) */
+  double prefill_flops;         /* algorithmic flops of its prefill phase (plan info) */
+  int32_t pending_prefill_tokens; /* (1) prompt tokens still waiting for prefill */
+  int32_t pending_decode_seqs;  /* (1)/(4) sequences waiting to decode beyond this step */
+  int32_t active_decode_seqs;   /* (4) sequences decoding in this step */
+} flex_ctl_signals;
+
+/* What the last step measured (e.g. flex_attn_corun_timing_read). */
+typedef struct flex_ctl_observation {
+  int32_t cus_decode;           /* split it ran with; 0 or cus_total = serial */
+  double decode_bytes, prefill_flops;
+  double decode_ms, prefill_ms; /* phase durations (0 for a phase with no work) */
+} flex_ctl_observation;
+
+#define FLEX_CTL_ONE_PHASE 0      /* one phase has no work: serial */
+#define FLEX_CTL_BEST 1           /* best predicted split */
+#define FLEX_CTL_SERIAL_FASTER 2  /* serial predicted fastest */
+#define FLEX_CTL_BACKLOG 3        /* decode backlog: largest decode share in the band */
+#define FLEX_CTL_BW_SATURATED 4   /* bandwidth pressure: smallest decode share in the band */
+#define FLEX_CTL_EXPLORE 5        /* neighbour of the choice, to refresh its estimate */
+#define FLEX_CTL_PREFILL_BACKLOG 6 /* prefill backlog: smallest decode share in the band */
+
+typedef struct flex_ctl_decision {
+  int32_t mode;                 /* FLEX_MODE_SERIAL or FLEX_MODE_CORUN */
+  int32_t cus_decode;           /* co-run: decode CUs (plan opts cus_decode); serial: cus_total */
+  int32_t cus_prefill;
+  int32_t reason;               /* FLEX_CTL_* */
+  double predicted_us;          /* predicted step time of the returned choice */
+} flex_ctl_decision;
+
+int flex_ctl_create(const flex_ctl_opts* opts, flex_ctl_t** out);
+void flex_ctl_destroy(flex_ctl_t* ctl);
+/* Seed the estimates from a measured profile (Sec. 3.3), e.g. the CU sweep:
+ * n points of (cus, decode GB/s alone on cus CUs, prefill TFLOP/s alone on cus
+ * CUs), cus ascending multiples of the granule; rates between points are
+ * interpolated linearly, and a split's co-run estimate starts at the alone
+ * rates of its two shares. Resets every estimate. */
+int flex_ctl_set_profile(flex_ctl_t* ctl, int32_t n, const int32_t* cus, const double* decode_gbps,
+                         const double* prefill_tflops);
+int flex_ctl_observe(flex_ctl_t* ctl, const flex_ctl_observation* obs);
+int flex_ctl_decide(flex_ctl_t* ctl, const flex_ctl_signals* sig, flex_ctl_decision* out);
+/* Current estimates: for each decode share k * granule (k = 1 .. K - 1,
+ * K = cus_total / granule) the co-run decode GB/s and prefill TFLOP/s of that
+ * split, then the serial pair; K entries each, capacity >= K. */
+int flex_ctl_estimates(const flex_ctl_t* ctl, double* decode_gbps, double* prefill_tflops, int32_t capacity);
+
 #ifdef __cplusplus
 }
 #endif

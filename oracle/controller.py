@@ -1,0 +1,176 @@
+"""Re-derivation of the online co-location controller's decisions (host policy).
+
+TEST INFRASTRUCTURE. Only ``tests/`` may import this module. The library never
+does, and this module imports nothing from the library.
+
+The paper's runtime rebalances prefill and decode step by step from five
+signals (Sec. 3.4, "Phase-Aware Dispatch"): pending work of each phase,
+recent per-phase execution times, memory-bandwidth pressure, decode progress
+and active sequences, device utilisation; decode near bandwidth saturation
+cedes compute to prefill, a decode backlog takes more. Its profile is coarse
+and updated while serving (Sec. 3.3). The paper gives no formula, so the
+library fixes one (stated in include/flexattn.h) and this module restates it
+independently, step by step, so that tests can compare every decision of the
+library with it exactly:
+
+* candidates: co-run with decode on k * g CUs (k = 1 .. K-1, K = cus_total / g)
+  and serial (index K);
+* estimates per candidate: decode GB/s and prefill TFLOP/s, seeded by a prior
+  (min(hbm, cus * bw_cu), cus * tflops_cu) or by a profile (linear
+  interpolation of alone rates, proportional below the first point, flat past
+  the last), then exponentially weighted toward each observation (the first
+  observation replaces the prior);
+* prediction in microseconds: co-run max(B / (dec * 1e3), F / (pre * 1e6)) +
+  overhead, serial B / (dec * 1e3) + F / (pre * 1e6);
+* choice: serial if a phase is empty or serial predicts strictly fastest (ties
+  go to the smaller index); else, among co-run splits within
+  (1 + tolerance) of the best, the largest decode share under a decode backlog,
+  else the smallest under bandwidth pressure (last observed decode rate >=
+  sat_frac * hbm) or a prefill backlog, else the best; every explore_every-th
+  decision moves to a neighbour (+1 on odd multiples, -1 on even ones, the
+  other way at the ends).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+ONE_PHASE, BEST, SERIAL_FASTER, BACKLOG, BW_SATURATED, EXPLORE, PREFILL_BACKLOG = range(7)
+MODE_SERIAL, MODE_CORUN = 0, 1
+
+
+@dataclass
+class CtlOpts:
+    cus_total: int = 256
+    granule: int = 64
+    explore_every: int = 16
+    backlog_seqs: int = 256
+    backlog_prefill_tokens: int = 8192
+    alpha: float = 0.25
+    tolerance: float = 0.03
+    sat_frac: float = 0.6
+    hbm_gbps: float = 8000.0
+    corun_overhead_us: float = 10.0
+    decode_gbps_per_cu: float = 60.0
+    prefill_tflops_per_cu: float = 5.0
+
+
+OC_DEFAULTS = CtlOpts()
+
+
+@dataclass
+class Controller:
+    o: CtlOpts
+    dec: List[float] = field(default_factory=list)
+    pre: List[float] = field(default_factory=list)
+    n_dec: List[int] = field(default_factory=list)
+    n_pre: List[int] = field(default_factory=list)
+    last_bw: float = 0.0
+    decisions: int = 0
+
+    @property
+    def K(self) -> int:
+        return self.o.cus_total // self.o.granule
+
+    def shares(self, k: int):
+        """(decode CUs, prefill CUs) of candidate k (K = serial: both get all)."""
+        if k == self.K:
+            return float(self.o.cus_total), float(self.o.cus_total)
+        cd = float(k * self.o.granule)
+        return cd, float(self.o.cus_total) - cd
+
+    def __post_init__(self):
+        # a zero option takes its default, as in the library's options
+        d = OC_DEFAULTS
+        for name in vars(d):
+            if getattr(self.o, name) == 0:
+                setattr(self.o, name, getattr(d, name))
+        K = self.K
+        self.dec = [0.0] * (K + 1)
+        self.pre = [0.0] * (K + 1)
+        for k in range(1, K + 1):
+            cd, cp = self.shares(k)
+            self.dec[k] = min(self.o.hbm_gbps, cd * self.o.decode_gbps_per_cu)
+            self.pre[k] = cp * self.o.prefill_tflops_per_cu
+        self.n_dec = [0] * (K + 1)
+        self.n_pre = [0] * (K + 1)
+
+    def set_profile(self, cus: Sequence[int], dgbps: Sequence[float], ptflops: Sequence[float]):
+        def curve(ys, c):
+            if c <= cus[0]:
+                return ys[0] * c / cus[0]
+            for i in range(1, len(cus)):
+                if c <= cus[i]:
+                    t = (c - cus[i - 1]) / float(cus[i] - cus[i - 1])
+                    return ys[i - 1] + t * (ys[i] - ys[i - 1])
+            return ys[-1]
+        for k in range(1, self.K + 1):
+            cd, cp = self.shares(k)
+            self.dec[k] = curve(dgbps, cd)
+            self.pre[k] = curve(ptflops, cp)
+        self.n_dec = [0] * (self.K + 1)
+        self.n_pre = [0] * (self.K + 1)
+        self.last_bw = 0.0
+
+    def _blend(self, table, counts, k, value):
+        table[k] = value if counts[k] == 0 else (1.0 - self.o.alpha) * table[k] + self.o.alpha * value
+        counts[k] += 1
+
+    def observe(self, cus_decode: int, decode_bytes: float, prefill_flops: float,
+                decode_ms: float, prefill_ms: float):
+        k = self.K if cus_decode in (0, self.o.cus_total) else cus_decode // self.o.granule
+        if decode_ms > 0 and decode_bytes > 0:
+            r = decode_bytes / (decode_ms * 1e-3) / 1e9
+            self._blend(self.dec, self.n_dec, k, r)
+            self.last_bw = r
+        if prefill_ms > 0 and prefill_flops > 0:
+            self._blend(self.pre, self.n_pre, k, prefill_flops / (prefill_ms * 1e-3) / 1e12)
+
+    def decide(self, decode_bytes: float, prefill_flops: float, pending_prefill_tokens: int = 0,
+               pending_decode_seqs: int = 0, active_decode_seqs: int = 1) -> dict:
+        o, K = self.o, self.K
+        self.decisions += 1
+        B, F = decode_bytes, prefill_flops
+
+        def phase_times(k):
+            td = B / (self.dec[k] * 1e3) if B > 0 else 0.0
+            tp = F / (self.pre[k] * 1e6) if F > 0 else 0.0
+            return td, tp
+
+        def serial(reason):
+            td, tp = phase_times(K)
+            return dict(mode=MODE_SERIAL, cus_decode=o.cus_total, cus_prefill=o.cus_total,
+                        reason=reason, predicted_us=td + tp)
+
+        if not (B > 0) or not (F > 0) or active_decode_seqs == 0:
+            return serial(ONE_PHASE)
+        pred = {}
+        for k in range(1, K + 1):
+            td, tp = phase_times(k)
+            pred[k] = max(td, tp) + o.corun_overhead_us if k < K else td + tp
+        best = 1
+        for k in range(2, K + 1):
+            if pred[k] < pred[best]:
+                best = k
+        if best == K:
+            return serial(SERIAL_FASTER)
+        band = [k for k in range(1, K) if pred[k] <= pred[best] * (1.0 + o.tolerance)]
+        choice, reason = best, BEST
+        if pending_decode_seqs >= o.backlog_seqs:
+            choice, reason = max(band), BACKLOG
+        elif self.last_bw >= o.sat_frac * o.hbm_gbps:
+            choice, reason = min(band), BW_SATURATED
+        elif pending_prefill_tokens >= o.backlog_prefill_tokens:
+            choice, reason = min(band), PREFILL_BACKLOG
+        if o.explore_every > 0 and self.decisions % o.explore_every == 0:
+            step = 1 if (self.decisions // o.explore_every) % 2 else -1
+            k = choice + step
+            if not 1 <= k < K:
+                k = choice - step
+            if 1 <= k < K:
+                choice, reason = k, EXPLORE
+        return dict(mode=MODE_CORUN, cus_decode=choice * o.granule, cus_prefill=o.cus_total - choice * o.granule,
+                    reason=reason, predicted_us=pred[choice])
+
+    def estimates(self):
+        return self.dec[1:], self.pre[1:]

@@ -17,7 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libflexattn.so")
-SOURCES = ["attention.hip", "kv_append.hip", "api.hip", "plan.cpp"]
+SOURCES = ["attention.hip", "kv_append.hip", "api.hip", "plan.cpp", "controller.cpp"]
 ARCH = "gfx950"
 
 

@@ -31,7 +31,16 @@ EXPORTED = [
     "flex_attn_prefill", "flex_attn_mixed", "flex_attn_corun_create", "flex_attn_corun_destroy",
     "flex_attn_corun_streams", "flex_attn_corun_set_timing", "flex_attn_corun_timing_read",
     "flex_attn_debug_gather", "flex_attn_workspace_init", "flex_attn_kv_append",
+    "flex_ctl_create", "flex_ctl_destroy", "flex_ctl_set_profile", "flex_ctl_observe", "flex_ctl_decide",
+    "flex_ctl_estimates",
 ]
+FLEX_CTL_ONE_PHASE = 0
+FLEX_CTL_BEST = 1
+FLEX_CTL_SERIAL_FASTER = 2
+FLEX_CTL_BACKLOG = 3
+FLEX_CTL_BW_SATURATED = 4
+FLEX_CTL_EXPLORE = 5
+FLEX_CTL_PREFILL_BACKLOG = 6
 FLEX_TIMING_RING = 1024
 
 
@@ -82,6 +91,30 @@ class AppendArgs(ctypes.Structure):
                 ("v_stride", ctypes.c_int64 * 3), ("num_pages", ctypes.c_int64), ("bad_count", ctypes.c_void_p)]
 
 
+class CtlOpts(ctypes.Structure):
+    _fields_ = [("cus_total", ctypes.c_int32), ("granule", ctypes.c_int32), ("explore_every", ctypes.c_int32),
+                ("backlog_seqs", ctypes.c_int32), ("backlog_prefill_tokens", ctypes.c_int32),
+                ("alpha", ctypes.c_double), ("tolerance", ctypes.c_double), ("sat_frac", ctypes.c_double),
+                ("hbm_gbps", ctypes.c_double), ("corun_overhead_us", ctypes.c_double),
+                ("decode_gbps_per_cu", ctypes.c_double), ("prefill_tflops_per_cu", ctypes.c_double)]
+
+
+class CtlSignals(ctypes.Structure):
+    _fields_ = [("decode_bytes", ctypes.c_double), ("prefill_flops", ctypes.c_double),
+                ("pending_prefill_tokens", ctypes.c_int32), ("pending_decode_seqs", ctypes.c_int32),
+                ("active_decode_seqs", ctypes.c_int32)]
+
+
+class CtlObservation(ctypes.Structure):
+    _fields_ = [("cus_decode", ctypes.c_int32), ("decode_bytes", ctypes.c_double),
+                ("prefill_flops", ctypes.c_double), ("decode_ms", ctypes.c_double), ("prefill_ms", ctypes.c_double)]
+
+
+class CtlDecision(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("cus_decode", ctypes.c_int32), ("cus_prefill", ctypes.c_int32),
+                ("reason", ctypes.c_int32), ("predicted_us", ctypes.c_double)]
+
+
 class FlexAttnError(RuntimeError):
     def __init__(self, status: int, what: str, detail: str):
         super().__init__(f"{what}: status {status} ({detail})")
@@ -125,6 +158,14 @@ def lib():
     L.flex_attn_debug_gather.argtypes = [vp, ctypes.POINTER(Args), i32, i32, vp, vp, vp]
     L.flex_attn_workspace_init.argtypes = [vp, sz, vp]
     L.flex_attn_kv_append.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(AppendArgs), vp]
+    L.flex_ctl_create.argtypes = [ctypes.POINTER(CtlOpts), ctypes.POINTER(vp)]
+    L.flex_ctl_destroy.argtypes = [vp]
+    L.flex_ctl_destroy.restype = None
+    L.flex_ctl_set_profile.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_double)]
+    L.flex_ctl_observe.argtypes = [vp, ctypes.POINTER(CtlObservation)]
+    L.flex_ctl_decide.argtypes = [vp, ctypes.POINTER(CtlSignals), ctypes.POINTER(CtlDecision)]
+    L.flex_ctl_estimates.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i32]
     for f in EXPORTED:
         if f not in ("flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan_destroy",
                      "flex_attn_corun_destroy"):
@@ -316,6 +357,53 @@ def make_append_args(k_new, v_new, slot_mapping, k_cache, v_cache, bad_count=Non
 def flex_attn_kv_append(shape: Shape, args: AppendArgs, stream=None):
     s = stream if stream is not None else current_stream()
     check(lib().flex_attn_kv_append(ctypes.byref(shape), ctypes.byref(args), s), "flex_attn_kv_append")
+
+
+class Controller:
+    """The online co-location controller (flex_ctl_*): observe steps, decide splits."""
+
+    def __init__(self, **opts):
+        o = CtlOpts()
+        for k, v in opts.items():
+            setattr(o, k, v)
+        h = ctypes.c_void_p()
+        check(lib().flex_ctl_create(ctypes.byref(o), ctypes.byref(h)), "flex_ctl_create")
+        self.handle = h
+        self.K = (o.cus_total or 256) // (o.granule or 64)
+
+    def close(self):
+        if self.handle:
+            lib().flex_ctl_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_profile(self, cus, decode_gbps, prefill_tflops):
+        n = len(cus)
+        check(lib().flex_ctl_set_profile(self.handle, n, (ctypes.c_int32 * n)(*cus),
+                                         (ctypes.c_double * n)(*decode_gbps), (ctypes.c_double * n)(*prefill_tflops)),
+              "flex_ctl_set_profile")
+
+    def observe(self, cus_decode, decode_bytes, prefill_flops, decode_ms, prefill_ms):
+        ob = CtlObservation(cus_decode, decode_bytes, prefill_flops, decode_ms, prefill_ms)
+        check(lib().flex_ctl_observe(self.handle, ctypes.byref(ob)), "flex_ctl_observe")
+
+    def decide(self, decode_bytes, prefill_flops, pending_prefill_tokens=0, pending_decode_seqs=0,
+               active_decode_seqs=1) -> dict:
+        sg = CtlSignals(decode_bytes, prefill_flops, pending_prefill_tokens, pending_decode_seqs, active_decode_seqs)
+        d = CtlDecision()
+        check(lib().flex_ctl_decide(self.handle, ctypes.byref(sg), ctypes.byref(d)), "flex_ctl_decide")
+        return {"mode": d.mode, "cus_decode": d.cus_decode, "cus_prefill": d.cus_prefill, "reason": d.reason,
+                "predicted_us": d.predicted_us}
+
+    def estimates(self):
+        dg, pt = (ctypes.c_double * self.K)(), (ctypes.c_double * self.K)()
+        check(lib().flex_ctl_estimates(self.handle, dg, pt, self.K), "flex_ctl_estimates")
+        return list(dg), list(pt)
 
 
 class Corun:

@@ -1,0 +1,181 @@
+"""The online co-location controller (host policy, CPU only).
+
+Parity: every decision of the library's controller equals the re-derivation
+in oracle/controller.py on long random observe/decide sequences (exact float
+equality of the predicted time). Pins, independent of both: the rule's
+directions from the paper (Sec. 3.4: bandwidth saturation cedes CUs to
+prefill, decode backlog takes more), monotonicity in the step's work, the
+argmin on a profile whose optimum is known in closed form, convergence of the
+estimates, the exploration pattern, and one planted mistake.
+"""
+import random
+
+import pytest
+
+import oracle.controller as OC
+from paper_2606_04415_amd import flexattn as F
+
+
+def both(**opts):
+    return F.Controller(**opts), OC.Controller(OC.CtlOpts(**opts))
+
+
+def same(a, b):
+    assert a["mode"] == b["mode"] and a["cus_decode"] == b["cus_decode"] and a["cus_prefill"] == b["cus_prefill"]
+    assert a["reason"] == b["reason"], (a, b)
+    assert a["predicted_us"] == b["predicted_us"], (a, b)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_decisions_match_the_re_derivation(seed):
+    rng = random.Random(seed)
+    opts = dict(granule=rng.choice([32, 64, 128]), explore_every=rng.choice([0, -1, 5, 16]),
+                backlog_seqs=rng.choice([64, 256]), tolerance=rng.choice([0.0, 1e-12, 0.2]))
+    lib, ref = both(**opts)
+    if seed % 2:
+        prof = ([32, 64, 128, 192, 256], [1500.0, 2800.0, 4660.0, 5600.0, 5550.0], [135.0, 268.0, 488.0, 517.0, 733.0])
+        lib.set_profile(*prof)
+        ref.set_profile(*prof)
+    K = 256 // opts["granule"]
+    for step in range(400):
+        B = rng.choice([0.0, rng.uniform(1e8, 3e9)])
+        Fl = rng.choice([0.0, rng.uniform(1e10, 3e12)])
+        sig = dict(pending_prefill_tokens=rng.randrange(0, 20000), pending_decode_seqs=rng.randrange(0, 400),
+                   active_decode_seqs=rng.randrange(0, 300))
+        a = lib.decide(B, Fl, **sig)
+        b = ref.decide(B, Fl, **sig)
+        same(a, b)
+        cd = a["cus_decode"] if a["mode"] == F.FLEX_MODE_CORUN else rng.choice([0, 256])
+        obs = (cd, B, Fl, rng.uniform(0.05, 3.0) if B else 0.0, rng.uniform(0.05, 9.0) if Fl else 0.0)
+        lib.observe(*obs)
+        ref.observe(*obs)
+    assert lib.estimates() == ref.estimates()
+
+
+def profile_linear(ctl, bw_per_cu, sat_gbps, tf_per_cu):
+    """A profile with decode rate min(sat, bw_per_cu * c), prefill tf_per_cu * c."""
+    cus = list(range(32, 257, 32))
+    ctl.set_profile(cus, [min(sat_gbps, bw_per_cu * c) for c in cus], [tf_per_cu * c for c in cus])
+
+
+def test_argmin_matches_closed_form_optimum():
+    # decode 40 GB/s per CU, saturating at 5120 GB/s from 128 CUs; prefill 4 TFLOP/s
+    # per CU. Below saturation the phase times balance where B / (40 c) = F / (4 (256 - c));
+    # B, F are chosen so that this happens at c = 96: F = B * 4e12 * 160 / (40 * 96e9).
+    # Serial then takes B / 5120 GB/s + F / 1024 TFLOP/s = 358 us, co-run 260 us.
+    ctl = F.Controller(granule=32, explore_every=-1, tolerance=1e-12, corun_overhead_us=1e-9)
+    profile_linear(ctl, 40.0, 5120.0, 4.0)
+    B = 1.0e9
+    Fl = B * 4e12 * 160 / (40 * 96e9)
+    d = ctl.decide(B, Fl, active_decode_seqs=10)
+    assert d["mode"] == F.FLEX_MODE_CORUN and d["cus_decode"] == 96 and d["reason"] == F.FLEX_CTL_BEST
+    # at the balance point both phases take B / (40 GB/s * 96) = 260.4 us
+    assert abs(d["predicted_us"] - B / (40e9 * 96) * 1e6) < 1e-6
+
+
+def test_monotone_in_the_steps_work():
+    ctl = F.Controller(granule=32, explore_every=-1, tolerance=1e-12)
+    profile_linear(ctl, 36.0, 5600.0, 3.0)
+    last = None
+    for Fl in [2e10, 5e10, 1e11, 2e11, 4e11, 8e11]:   # more prefill work: decode share never grows
+        d = ctl.decide(1.0e9, Fl, active_decode_seqs=64)
+        if d["mode"] == F.FLEX_MODE_CORUN:
+            assert last is None or d["cus_decode"] <= last
+            last = d["cus_decode"]
+    last = None
+    for B in [2e8, 5e8, 1e9, 2e9, 4e9]:               # more decode work: decode share never shrinks
+        d = ctl.decide(B, 1.5e11, active_decode_seqs=64)
+        if d["mode"] == F.FLEX_MODE_CORUN:
+            assert last is None or d["cus_decode"] >= last
+            last = d["cus_decode"]
+
+
+def test_saturated_decode_cedes_cus_and_backlog_takes_them():
+    # decode saturates at 4800 GB/s from 160 CUs on: a wide band of equally fast
+    # splits once prefill is small
+    def fresh():
+        c = F.Controller(granule=32, explore_every=-1, tolerance=0.05)
+        profile_linear(c, 30.0, 4800.0, 3.0)
+        return c
+    B, Fl = 1.3e9, 2.0e10
+    base = fresh().decide(B, Fl, active_decode_seqs=128)
+    sat = fresh()
+    sat.observe(160, B, 0.0, B / 4.9e12 * 1e3, 0.0)     # observed 4.9 TB/s >= 0.6 * 8 TB/s
+    d_sat = sat.decide(B, Fl, active_decode_seqs=128)
+    d_back = fresh().decide(B, Fl, pending_decode_seqs=1000, active_decode_seqs=128)
+    assert d_sat["reason"] == F.FLEX_CTL_BW_SATURATED and d_back["reason"] == F.FLEX_CTL_BACKLOG
+    assert d_sat["cus_decode"] <= base["cus_decode"] <= d_back["cus_decode"]
+    assert d_sat["cus_decode"] < d_back["cus_decode"]
+    # saturated decode never gets more CUs than saturation needs (within the band)
+    assert d_sat["cus_decode"] <= 192
+
+
+def test_one_phase_runs_serial():
+    ctl = F.Controller()
+    for B, Fl, act in [(0.0, 1e11, 0), (1e9, 0.0, 5), (1e9, 1e11, 0)]:
+        d = ctl.decide(B, Fl, active_decode_seqs=act)
+        assert d["mode"] == F.FLEX_MODE_SERIAL and d["reason"] == F.FLEX_CTL_ONE_PHASE
+        assert d["cus_decode"] == 256
+
+
+def test_estimates_converge_to_observed_rates():
+    ctl = F.Controller(alpha=0.25, explore_every=-1)
+    prior_d, prior_p = ctl.estimates()
+    for _ in range(40):
+        ctl.observe(128, 1.0e9, 1.0e11, 0.25, 0.2)       # 4000 GB/s, 500 TFLOP/s
+    d, p = ctl.estimates()
+    assert abs(d[1] - 4000.0) < 1e-9 and abs(p[1] - 500.0) < 1e-9   # first observation replaces the prior
+    assert d[0] == prior_d[0] and p[2] == prior_p[2]                  # other splits untouched
+    ctl.observe(128, 1.0e9, 1.0e11, 0.5, 0.4)            # one slower step moves the estimate by alpha
+    d, p = ctl.estimates()
+    assert abs(d[1] - (0.75 * 4000.0 + 0.25 * 2000.0)) < 1e-9
+
+
+def test_exploration_visits_neighbours():
+    # saturating decode: the best split is 128 (293 us; serial 341 us)
+    ctl = F.Controller(granule=64, explore_every=4, tolerance=1e-12, corun_overhead_us=1e-9)
+    profile_linear(ctl, 40.0, 5120.0, 4.0)
+    picks = [ctl.decide(1e9, 1.5e11, active_decode_seqs=8) for _ in range(16)]
+    for i, d in enumerate(picks, start=1):
+        if i % 4 == 0:
+            assert d["reason"] == F.FLEX_CTL_EXPLORE
+        else:
+            assert d["reason"] == F.FLEX_CTL_BEST
+    best = picks[0]["cus_decode"]
+    assert {picks[3]["cus_decode"], picks[7]["cus_decode"]} == {best - 64, best + 64}
+
+
+def test_planted_mistake_is_caught():
+    # An oracle that applies the bandwidth rule before the backlog rule must
+    # disagree with the library somewhere on the parity sequence.
+    class Swapped(OC.Controller):
+        def decide(self, B, Fl, pending_prefill_tokens=0, pending_decode_seqs=0, active_decode_seqs=1):
+            if self.last_bw >= self.o.sat_frac * self.o.hbm_gbps:
+                pending_decode_seqs = 0
+            return super().decide(B, Fl, pending_prefill_tokens, pending_decode_seqs, active_decode_seqs)
+    lib = F.Controller(explore_every=-1)
+    bad = Swapped(OC.CtlOpts(explore_every=-1))
+    rng = random.Random(1)
+    differ = False
+    for _ in range(300):
+        B, Fl = rng.uniform(5e8, 2e9), rng.uniform(2e10, 4e11)
+        sig = dict(pending_decode_seqs=rng.randrange(0, 600), active_decode_seqs=100)
+        a, b = lib.decide(B, Fl, **sig), bad.decide(B, Fl, **sig)
+        differ |= (a["cus_decode"], a["reason"]) != (b["cus_decode"], b["reason"])
+        cd = a["cus_decode"] if a["mode"] == F.FLEX_MODE_CORUN else 0
+        obs = (cd, B, Fl, B / rng.uniform(3e12, 6e12) * 1e3, Fl / rng.uniform(2e14, 6e14) * 1e3)
+        lib.observe(*obs)
+        bad.observe(*obs)
+    assert differ
+
+
+def test_invalid_options_rejected():
+    with pytest.raises(F.FlexAttnError):
+        F.Controller(granule=96)          # does not divide 256
+    with pytest.raises(F.FlexAttnError):
+        F.Controller(alpha=1.5)
+    ctl = F.Controller()
+    with pytest.raises(F.FlexAttnError):
+        ctl.observe(100, 1e9, 1e11, 0.1, 0.1)   # not a candidate split
+    with pytest.raises(F.FlexAttnError):
+        ctl.set_profile([64, 32], [1.0, 2.0], [1.0, 2.0])
