@@ -1,0 +1,31 @@
+"""GPU run of the step-level serving loop (KV append + mixed attention per step,
+three policies). Every policy must see the same batches: the same decode-token
+count and the same number of prompts finishing prefill; the controller's
+co-run steps must be valid candidate splits."""
+import argparse
+
+import pytest
+
+from paper_2606_04415_amd import serve_sim
+
+from gpu_common import log
+
+pytestmark = pytest.mark.gpu
+
+
+def test_policies_replay_the_same_stream():
+    args = argparse.Namespace(steps=24, seed=3, warm=40, max_active=48, chunk=2048, burst=8, burst_every=10,
+                              rate=0.3, fixed_decode_cus=128, per_mix_limits=False)
+    res = {}
+    for pol in ("serial", "fixed", "controller"):
+        log(f"serve loop: mix long, policy {pol}, 24 steps")
+        res[pol] = serve_sim.simulate("long", pol, args, profile=None)
+    toks = {p: r["tpot_ms"]["tokens"] for p, r in res.items()}
+    firsts = {p: r["ttft_ms"]["n"] for p, r in res.items()}
+    assert len(set(toks.values())) == 1 and len(set(firsts.values())) == 1, (toks, firsts)
+    assert toks["serial"] > 0 and firsts["serial"] > 0
+    assert set(res["serial"]["splits"]) == {"serial"}
+    for k in res["controller"]["splits"]:
+        assert k == "serial" or k in ("192:64", "128:128", "64:192")
+    for r in res.values():
+        assert r["total_ms"] > 0 and r["step_ms"]["max"] < 50.0
