@@ -218,8 +218,9 @@ int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, in
                     void* stream, flex_attn_corun_t* corun);
 
 /* Create two streams on the current device, restricted by CU masks to
- * cus_prefill and cus_decode compute units (disjoint, balanced over the
- * chip's XCDs), and a 24-byte device buffer of step counters through which
+ * cus_prefill and cus_decode compute units (disjoint; each eighth of the
+ * device holds one CU of every shader engine of every XCD, so any split keeps
+ * the engines evenly equipped), and a 24-byte device buffer of step counters through which
  * flex_attn_mixed forks and joins them (stream memory writes and waits). Each
  * count must be a positive multiple of an eighth of the device's CUs (32 on
  * a 256-CU MI355X) and their sum at most the device's CU count. One pair

@@ -131,12 +131,15 @@ int run_prefill(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "prefill launch");
 }
 
-// CU masks in eighths of the device. Mask bit i = 32k + 8q + r (k = i / 32,
-// q = (i >> 3) & 3, r = i & 7) belongs to eighth 2q + (((r + k) >> 2) & 1):
-// every eighth takes 4 bits of each group of 32 and 4 bits of each residue
-// class of i mod 8, so whether the device maps mask bits to XCDs by i / 32 or
-// by i mod 8, a set of eighths spreads evenly over all eight XCDs.
-int eighth_of(int i) { return 2 * ((i >> 3) & 3) + ((((i & 7) + (i >> 5)) >> 2) & 1); }
+// CU masks in eighths of the device. On MI355X (8 XCDs x 4 shader engines x 8
+// CUs) mask bit i selects a CU of XCD i % 8, shader engine (i >> 3) & 3,
+// position i >> 5 within the engine (measured by recording the hardware ids
+// of the work-groups each mask admits). Eighth k is the 32-bit word k: one CU
+// of every shader engine of every XCD. Work-groups are handed to XCDs and to
+// engines in turn, so a phase runs as fast as its least-equipped engine: any
+// set of eighths keeps the engines equal (a mask that fills some engines and
+// half-fills others ran no faster than the half-filled engines allow).
+int eighth_of(int i) { return i >> 5; }
 
 void build_mask(int lo_eighth, int eighths, int total, uint32_t* mask, int words) {
   for (int i = 0; i < words; ++i) mask[i] = 0;
