@@ -12,7 +12,9 @@ classifies each sequence by its number of new tokens and lays out the work of
 each phase. The partition itself is not in the paper (it defines no kernel);
 the contract is:
 
-* classification: n = 1 -> decode, n >= 2 -> prefill, n = 0 -> nothing.
+* classification: n = 1 -> decode, n >= 2 -> prefill, n = 0 -> nothing; in
+  the (192, 128) layout (latent attention with heads split out, prefill only)
+  every n >= 1 is prefill.
 * decode partition (balanced split-K): P_s = ceil(L_s / P); the pages of
   all decode sequences, concatenated in batch order, form a list of
   T = sum_s P_s pages; W = work-groups per key range (grouped-query
@@ -34,7 +36,7 @@ the contract is:
 * prefill tiles of BM rows (BM 32 by default for grouped-query heads, 128 for
   the latent layout, which also takes 64): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
   ordered by key_end descending, then sequence, then tile. Each tile is served
-  by Hkv * ceil(G / 8) work-groups (grouped-query) or Hq (latent).
+  by Hkv * ceil(G / 8) work-groups (grouped-query) or Hq (latent layouts).
 * co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
@@ -98,12 +100,14 @@ MAX_RANGE_PAGES = 8192
 
 def _supported(sh: Shape) -> bool:
     pair = (sh.head_dim_qk, sh.head_dim_v)
-    if pair not in ((64, 64), (128, 128), (576, 512)):
+    if pair not in ((64, 64), (128, 128), (576, 512), (192, 128)):
         return False
     if sh.page_size not in (16, 64):
         return False
     if pair == (576, 512):
         return bool(sh.v_aliases_k) and sh.num_q_heads % MLA_ROWS_PER_WG == 0
+    if pair == (192, 128):
+        return not sh.v_aliases_k and sh.page_size == 64 and (sh.num_q_heads // sh.num_kv_heads) <= 16
     return (sh.num_q_heads // sh.num_kv_heads) <= 16
 
 
@@ -129,12 +133,13 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     min_tokens = o.min_split_tokens or 256
     granule = o.split_granule or 32
     mla = sh.head_dim_qk == 576
-    bm = o.bm or (128 if mla else 32)
+    split = sh.head_dim_qk == 192     # heads split out: prefill only, one tile per query head
+    bm = o.bm or (128 if mla or split else 32)
     if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:
         return PlanResult(ERR_INVALID_ARG)
     if o.cus_decode < -1 or o.cus_decode > cus_total:
         return PlanResult(ERR_INVALID_ARG)
-    if (mla and bm not in (64, 128)) or (not mla and bm not in (16, 32)):
+    if (mla and bm not in (64, 128)) or (split and bm != 128) or (not mla and not split and bm not in (16, 32)):
         return PlanResult(ERR_UNSUPPORTED)
     # --- integer metadata checks
     if max_pages_per_seq < 0:
@@ -154,8 +159,8 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     mla_rows = MLA_ROWS_PER_WG_WIDE if sh.num_q_heads % MLA_ROWS_PER_WG_WIDE == 0 else MLA_ROWS_PER_WG
     W = (sh.num_q_heads // mla_rows) if mla else cdiv(sh.num_kv_heads, heads_per_wg)
     rows_per_wg = mla_rows if mla else heads_per_wg * (sh.num_q_heads // sh.num_kv_heads)
-    dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1]
-    pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= 2]
+    dec = [s for s in range(B) if qsl[s + 1] - qsl[s] == 1 and not split]
+    pre = [s for s in range(B) if qsl[s + 1] - qsl[s] >= (1 if split else 2)]
 
     # --- co-run CU split
     dec_bytes = 0
@@ -229,7 +234,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     off_pre = off_order + nd_
     total = off_pre + ITEM * np_
     G = sh.num_q_heads // sh.num_kv_heads
-    pre_height = sh.num_q_heads if mla else sh.num_kv_heads * cdiv(G, 8)
+    pre_height = sh.num_q_heads if mla or split else sh.num_kv_heads * cdiv(G, 8)
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
            HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, 0]
     blob = hdr + [x for it in dec_items for x in it] + ranges + order + [x for it in tiles for x in it]

@@ -500,7 +500,7 @@ template <int DQK, bool VALIAS>
 __device__ __forceinline__ int swz_k(int x, int r) {
   if constexpr (VALIAS) return x;
   else if constexpr (DQK == 128) return x ^ (r & 15);        // 256-byte rows
-  else return x ^ ((r >> 1) & 7);                            // 128-byte rows
+  else return x ^ ((r >> 1) & 7);   // 128-byte rows; 384-byte rows (odd rows start half a bank row on)
 }
 template <int DV>
 __device__ __forceinline__ int swz_v(int x, int r) {
@@ -554,6 +554,14 @@ void rowpar_kernel(AttnParams p) {
     col = x % p.grid_y;
     item = j * (8 / p.grid_y) + x / p.grid_y;
     if (item >= p.n_items) return;
+  }
+  // One query head per work-group (a multiple of 8 heads): head h runs on
+  // XCD h % 8 for all its tiles, tiles longest first, so each XCD's L2 holds
+  // the keys and values of its own heads only.
+  if (MODE == kPrefillPerHead && p.xcd_remap) {
+    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3, hp8 = p.grid_y / 8;
+    item = j / hp8;
+    col = (j % hp8) * 8 + x;
   }
   const int32_t* it = p.items + 8 * (MODE == kDecodeLatent ? p.order[item] : item);
   const int seq = it[0];
@@ -684,7 +692,8 @@ void rowpar_kernel(AttnParams p) {
     const int row0 = blk * 64 < C::K_SLOTS ? blk * 64 / C::CPR : (blk * 64 - C::K_SLOTS) / (C::CPRV > 0 ? C::CPRV : 1);
     return __builtin_amdgcn_readfirstlane(row0 / P);
   };
-  static_assert(VALIAS || (64 % C::CPR == 0 && P % (64 / C::CPR) == 0), "a load instruction stays in one page");
+  static_assert(VALIAS || P >= BN || (64 % C::CPR == 0 && P % (64 / C::CPR) == 0),
+                "a load instruction stays in one page");
   uint32_t ld_lane_off[C::NI];
 #pragma unroll
   for (int j = 0; j < C::NI; ++j) {
@@ -1093,9 +1102,26 @@ static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 gr
     return dqk == 128 ? launch_prefill_grouped<128, P>(q, bm, grid, stream)
                       : launch_prefill_grouped<64, P>(q, bm, grid, stream);
   }
-  // Latent prefill: one work-group per (tile, query head), a wave per 16 rows.
+  // One work-group per (tile, query head), a wave per 16 rows; XCD-aware
+  // 1-D grid when the head count is a multiple of 8.
+  if (p.grid_y % 8 == 0) {
+    AttnParams q = p;
+    q.xcd_remap = 1;
+    const dim3 g1(p.n_items * p.grid_y, 1);
+    if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(q, g1, stream);
+    if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(q, g1, stream);
+    if constexpr (P == 64) {
+      if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 64, false, kPrefillPerHead, 64, 3>(q, g1, stream);
+    }
+    return hipErrorInvalidValue;
+  }
   if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
+  // Heads split out (keys 192, values 128): one work-group per (128-token
+  // tile, query head); 64-key tiles, each inside one 64-slot page.
+  if constexpr (P == 64) {
+    if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 64, false, kPrefillPerHead, 64, 3>(p, grid, stream);
+  }
   return hipErrorInvalidValue;
 }
 

@@ -28,9 +28,11 @@ bool supported_dims(const flex_attn_shape& s) {
   const int dq = s.head_dim_qk, dv = s.head_dim_v;
   const bool gqa = (dq == 64 && dv == 64) || (dq == 128 && dv == 128);
   const bool latent = dq == 576 && dv == 512;
-  if (!gqa && !latent) return false;
+  const bool split = dq == 192 && dv == 128;   // latent attention with heads split out (prefill)
+  if (!gqa && !latent && !split) return false;
   if (s.page_size != 16 && s.page_size != 64) return false;
   if (latent) return s.v_aliases_k && s.num_q_heads % kLatentRowsPerWG == 0;
+  if (split) return !s.v_aliases_k && s.page_size == 64 && s.num_q_heads / s.num_kv_heads <= 16;
   return s.num_q_heads / s.num_kv_heads <= 16;
 }
 
@@ -45,7 +47,8 @@ int check_shape(const flex_attn_shape& sh) {
     return set_error(FLEX_ERR_INVALID_ARG, "v_aliases_k needs one KV head and head_dim_v <= head_dim_qk");
   if (!supported_dims(sh))
     return set_error(FLEX_ERR_UNSUPPORTED, "shape outside (64,64)/(128,128) GQA with group <= 16, "
-                                           "or (576,512) aliased latent with Hq % 64 == 0; page 16/64");
+                                           "(576,512) aliased latent with Hq % 64 == 0, page 16/64, "
+                                           "or (192,128) with group <= 16, page 64");
   return FLEX_OK;
 }
 
@@ -93,6 +96,11 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   std::memset(&o, 0, sizeof(o));
   if (opts) o = *opts;
   const bool latent = sh.head_dim_qk == 576;
+  // (192, 128): latent attention with its heads split out (keys 128 + 64
+  // rope, values 128 per head), the layout in which a long prompt costs the
+  // fewest flops. Prefill only: every sequence with new tokens, one token
+  // included, runs as a prefill tile of one query head.
+  const bool split = sh.head_dim_qk == 192;
   const int64_t cus_total = o.cus_total ? o.cus_total : 256;
   // Grouped-query decode: one work-group per CU walking a long range measured
   // fastest; latent decode launches one work-group per piece, so more pieces.
@@ -100,13 +108,14 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
   const int64_t granule = o.split_granule ? o.split_granule : 32;
-  const int32_t bm = o.bm ? o.bm : (latent ? 128 : 32);
+  const int32_t bm = o.bm ? o.bm : (latent || split ? 128 : 32);
   if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
   if (o.cus_decode < -1 || o.cus_decode > cus_total)
     return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
-  if (latent ? (bm != 64 && bm != 128) : (bm != 16 && bm != 32))
-    return set_error(FLEX_ERR_UNSUPPORTED, "bm must be 16 or 32 (grouped-query) or 64 or 128 (latent layout)");
+  if (latent ? (bm != 64 && bm != 128) : split ? bm != 128 : (bm != 16 && bm != 32))
+    return set_error(FLEX_ERR_UNSUPPORTED,
+                     "bm must be 16 or 32 (grouped-query), 64 or 128 (latent layout), 128 (192/128 layout)");
   if (max_pages_per_seq < 0) return set_error(FLEX_ERR_INVALID_ARG, "max_pages_per_seq < 0");
   if (num_seqs > 0 && qsl[0] != 0) return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc[0] != 0");
 
@@ -132,13 +141,13 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   // Prefill work-groups per tile: one per query head (latent layout), or one per
   // KV head and group of up to 8 of its query heads (grouped-query layout).
   const int32_t G = sh.num_q_heads / sh.num_kv_heads;
-  const int32_t pre_grid_y = latent ? sh.num_q_heads : sh.num_kv_heads * ((G + 7) / 8);
+  const int32_t pre_grid_y = latent || split ? sh.num_q_heads : sh.num_kv_heads * ((G + 7) / 8);
   const int32_t rows_per_wg = latent ? latent_rows : heads_per_wg * (sh.num_q_heads / sh.num_kv_heads);
   std::vector<int32_t> dec, pre;
   for (int32_t s = 0; s < num_seqs; ++s) {
     const int32_t n = qsl[s + 1] - qsl[s];
-    if (n == 1) dec.push_back(s);
-    else if (n >= 2) pre.push_back(s);
+    if (n == 1 && !split) dec.push_back(s);
+    else if (n >= 1) pre.push_back(s);
   }
 
   // Algorithmic work of each phase (feeds the cost model and the plan info).

@@ -14,7 +14,8 @@ attention geometry of those two models:
 * Qwen2.5-7B: 28 query heads, 4 KV heads (GQA 7:1), head_dim 128.
 * DeepSeek-R1 MLA in absorbed form: 128 query heads, one latent KV head of
   width 576 (512 latent + 64 rope), value width 512 (the first 512 columns of
-  the latent row), softmax scale 1/sqrt(192).
+  the latent row), softmax scale 1/sqrt(192); and for prefill with its heads
+  split out: 128 heads with keys of 192 (128 + 64 rope) and values of 128.
 
 Draw order for a workload (one torch CPU generator, seeded):
   1. ``seq_lens`` per segment, in batch order, via ``randint(lo, hi + 1)``;
@@ -105,6 +106,12 @@ WORKLOADS = {
         segments=(Segment(256, 1, (1024, 16384)), Segment(1, None, (4096, 4096))),
         description="DeepSeek-R1-style absorbed MLA, one GPU's share: 128 heads, latent 576 "
                     "(V = first 512), page 64; 256 decodes U[1024,16384] + one 4096-token prompt"),
+    "mla_split": Workload(
+        name="mla_split", num_q_heads=128, num_kv_heads=128, head_dim_qk=192, head_dim_v=128,
+        page_size=64, sm_scale=1.0 / math.sqrt(192.0), v_aliases_k=False,
+        segments=(Segment(1, None, (4096, 4096)),),
+        description="DeepSeek-R1-style MLA prefill with heads split out (keys 128 + 64 rope, values 128, "
+                    "128 heads), page 64; one 4096-token prompt"),
 }
 
 

@@ -80,7 +80,8 @@ def test_plan_matches_rederivation_fuzz():
     rng = random.Random(1)
     shapes = [OP.Shape(28, 4, 128, 128, 16, 128 ** -0.5, 0), OP.Shape(4, 1, 64, 64, 16, 0.125, 0),
               OP.Shape(32, 2, 128, 128, 64, 0.1, 0), OP.Shape(128, 1, 576, 512, 64, 192 ** -0.5, 1),
-              OP.Shape(64, 1, 576, 512, 64, 0.07, 1)]
+              OP.Shape(64, 1, 576, 512, 64, 0.07, 1), OP.Shape(16, 16, 192, 128, 64, 192 ** -0.5, 0),
+              OP.Shape(8, 4, 192, 128, 64, 0.1, 0)]
     for trial in range(400):
         sh = rng.choice(shapes)
         P = sh.page_size

@@ -224,3 +224,21 @@ def test_full_mixed_corun_sampled():
 
 def test_full_latent_sampled():
     sampled_check("mla", n_dec=4, n_pre_rows=6)
+
+
+SPLIT = WORKLOADS["mla_split"]
+
+
+def test_split_head_latent_prefill_ragged():
+    # keys 192, values 128, two query heads per KV head; prefill only: the one-token
+    # sequences run as prefill tiles too; ragged 128-token tiles, an empty sequence
+    ns, ls = [1, 130, 5, 0, 64, 300], [70, 130, 200, 10, 300, 700]
+    b = custom_batch(SPLIT, ns, ls, seed=7, num_q_heads=8, num_kv_heads=4)
+    log("split-head latent prefill 8/4 heads, 192/128, page 64, ragged")
+    out, lse = full_check(b, what="split-head")
+    _, _, pa = run(b)
+    assert pa.plan.info["n_decode_items"] == 0 and pa.plan.info["n_prefill_seqs"] == 5
+
+
+def test_full_split_head_latent_sampled():
+    sampled_check("mla_split", n_pre_rows=8)
