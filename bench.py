@@ -12,6 +12,12 @@ cannot serve repeated steps.
 Default workload: the Qwen2.5-7B-shaped mixed step (one 2048-token chunk on
 4096 cached tokens plus 128 decodes with context U[1024, 8192], GQA 28/4,
 head_dim 128, page 16). Prints one JSON line on stdout.
+
+Each mode runs W warm-up steps, K timed steps (the step time: HIP events on
+the issuing stream around the K steps), then K more steps with HIP events
+around each phase's kernel on the stream it runs on (the phase durations and
+the roofline's kernel duration), kept apart because recording those events
+adds about 10 us to a step.
 """
 from __future__ import annotations
 
@@ -156,8 +162,9 @@ def time_kv_append(b, kv, shape, steps, stream):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=200,
+                    help="untimed steps first: the first passes over the rotated KV copies pay for TLB and clock warm-up")
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--split", default="128:128", help="prefill:decode CUs for co-run")
     ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over steps")
@@ -223,13 +230,15 @@ def main():
     caller = torch.cuda.Stream()
 
     def timed(mode, steps, warmup):
-        corun.set_timing(True)
+        """K timed steps with nothing but the step in the stream (the step time),
+        then K more with HIP events around each phase's kernel on the stream it
+        runs on (the phase and kernel durations): recording those events costs
+        about 10 us per step, so they stay out of the step time."""
+        corun.set_timing(False)
         for i in range(warmup):
             F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
         torch.cuda.synchronize()
-        corun.set_timing(True)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
         t_wall = time.perf_counter()
         e0.record(caller)
         for i in range(steps):
@@ -238,7 +247,12 @@ def main():
         torch.cuda.synchronize()
         wall = time.perf_counter() - t_wall
         ms = e0.elapsed_time(e1) / steps
+        corun.set_timing(True)
+        for i in range(steps):
+            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
+        torch.cuda.synchronize()
         pre, dec = corun.timing_read()
+        corun.set_timing(False)
         return ms, wall, sum(pre) / len(pre), sum(dec) / len(dec)
 
     if args.counter_pass:
