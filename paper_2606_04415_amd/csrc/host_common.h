@@ -54,6 +54,7 @@ void clear_error();
 struct flex_attn_plan {
   flex_attn_shape shape;
   flex_attn_plan_info info;
+  int32_t cus_total;        // the CU count the plan was partitioned against
   int32_t rows_per_wg;      // query rows of one decode work-group
   std::vector<int32_t> words;
 };

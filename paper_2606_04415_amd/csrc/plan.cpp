@@ -255,6 +255,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   if (!plan) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
   plan->shape = sh;
   plan->rows_per_wg = rows_per_wg;
+  plan->cus_total = int32_t(cus_total);
   const int32_t n_pre_items = int32_t(tiles.size());
   // Launch order for one work-group per piece: longest key range first.
   std::vector<int32_t> order(n_dec_items);

@@ -21,7 +21,7 @@ import json
 import sys
 
 
-def _time_on(stream_handle, fn, reps, warmup=3):
+def _time_on(stream_handle, fn, reps, warmup=30):
     import torch
     s = torch.cuda.ExternalStream(stream_handle) if stream_handle else torch.cuda.current_stream()
     for _ in range(warmup):
