@@ -41,7 +41,7 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
   const int slot0 = it[5], nspl = it[2];   // workspace slots slot0 .. slot0 + nspl - 1
   const int col = blockIdx.y, W = gridDim.y, rows = p.rows_per_wg;
   const int64_t out_row0 = int64_t(it[6]) * p.Hq + int64_t(col) * rows;
-  for (int idx = threadIdx.x; idx < rows * (DV / 4); idx += blockDim.x) {
+  for (int idx = blockIdx.z * blockDim.x + threadIdx.x; idx < rows * (DV / 4); idx += blockDim.x * gridDim.z) {
     const int i = idx / (DV / 4);
     const int d = 4 * (idx % (DV / 4));
     float M = -INFINITY, den = 0.f;
@@ -1071,13 +1071,18 @@ static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t
 
 hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStream_t stream) {
   if (p.n_items == 0) return hipSuccess;
-  const dim3 grid(p.n_items, p.grid_y);
   hipError_t e = launch_decode_kernel(p, dqk, stream);
   if (e != hipSuccess || !has_splits) return e;
+  // Merge: one work-group per (piece, column, slice of the output rows);
+  // only a split sequence's first piece has work, each thread at most a few
+  // (row, 4 columns) outputs so all their loads are in flight together.
+  const int dv = dqk == 576 ? 512 : dqk;
+  const int units = p.rows_per_wg * (dv / 4);
+  const dim3 mgrid(p.n_items, p.grid_y, std::min(8, (units + 255) / 256));
   switch (dqk) {
-    case 128: hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, p); break;
-    case 64: hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, p); break;
-    case 576: hipLaunchKernelGGL(merge_kernel<512>, grid, dim3(256), 0, stream, p); break;
+    case 128: hipLaunchKernelGGL(merge_kernel<128>, mgrid, dim3(256), 0, stream, p); break;
+    case 64: hipLaunchKernelGGL(merge_kernel<64>, mgrid, dim3(256), 0, stream, p); break;
+    case 576: hipLaunchKernelGGL(merge_kernel<512>, mgrid, dim3(256), 0, stream, p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
