@@ -30,9 +30,10 @@ the contract is:
   Item words: [s, j, n_s, k0, k1, slot of piece 0 of s, qsl[s], slot], j the
   piece's rank within its sequence and n_s the sequence's piece count. A range
   table of R + 1 words gives the first piece of each range (the last word is
-  the piece count), and a launch order of the pieces for one-work-group-per-
-  piece launches lists them by key count descending, ties by slot.
-  max_splits is accepted and ignored.
+  the piece count), a launch order of the pieces for one-work-group-per-
+  piece launches lists them by key count descending, ties by slot, and a
+  merge list gives the first piece of every sequence cut into several pieces
+  (batch order). max_splits is accepted and ignored.
 * prefill tiles of BM rows (BM 32 by default for grouped-query heads, 128 for
   the latent layout, which also takes 64): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
   ordered by key_end descending, then sequence, then tile. Each tile is served
@@ -41,8 +42,9 @@ the contract is:
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
 
-Blob layout (int32): 20-word header, 8 words per decode item, the range
-table, the piece launch order, 8 words per prefill item; see ``build_plan``.
+Blob layout (int32, version 4): 20-word header (word 19: offset of the
+merge list), 8 words per decode item, the range table, the piece launch
+order, the merge list, 8 words per prefill item; see ``build_plan``.
 """
 from __future__ import annotations
 
@@ -52,7 +54,7 @@ from typing import List, Optional, Sequence
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
 MAGIC = 0x46504C58
-VERSION = 3
+VERSION = 4
 HEADER = 20
 ITEM = 8
 
@@ -231,13 +233,16 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     order = sorted(range(nd_), key=lambda i: (-(dec_items[i][4] - dec_items[i][3]), i))
     off_ranges = HEADER + ITEM * nd_
     off_order = off_ranges + len(ranges)
-    off_pre = off_order + nd_
+    # merge list: the first piece of every decode sequence cut into several pieces
+    merge = [it[5] for it in dec_items if it[1] == 0 and it[2] > 1]
+    off_merge = off_order + nd_
+    off_pre = off_merge + len(merge)
     total = off_pre + ITEM * np_
     G = sh.num_q_heads // sh.num_kv_heads
     pre_height = sh.num_q_heads if mla or split else sh.num_kv_heads * cdiv(G, 8)
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
-           HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, 0]
-    blob = hdr + [x for it in dec_items for x in it] + ranges + order + [x for it in tiles for x in it]
+           HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, off_merge]
+    blob = hdr + [x for it in dec_items for x in it] + ranges + order + merge + [x for it in tiles for x in it]
     # workspace: (max, sum) per decode item, column and row, then the partial outputs;
     # only needed when some decode sequence is split
     if n_split == 0:

@@ -115,6 +115,8 @@ int run_decode(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args*
   p.ranges = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_RANGES];
   p.n_ranges = plan->words[H_N_RANGES];
   p.order = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_ORDER];
+  p.merge = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_MERGE];
+  p.n_merge = info.n_split_seqs;
   p.range_pages = info.pages_per_split;
   p.whole_device = info.cus_decode >= plan->cus_total ? 1 : 0;
   p.grid_y = info.decode_wg_width;

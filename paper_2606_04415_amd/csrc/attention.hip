@@ -36,8 +36,7 @@ __device__ __forceinline__ PagedCache as_cache(const CacheRef& c) { return Paged
 template <int DV>
 __global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
   constexpr int KB = 8;   // pieces folded per step
-  const int32_t* it = p.items + 8 * blockIdx.x;
-  if (it[1] != 0 || it[2] <= 1) return;
+  const int32_t* it = p.items + 8 * p.merge[blockIdx.x];   // the sequence's first piece
   const int slot0 = it[5], nspl = it[2];   // workspace slots slot0 .. slot0 + nspl - 1
   const int col = blockIdx.y, W = gridDim.y, rows = p.rows_per_wg;
   const int64_t out_row0 = int64_t(it[6]) * p.Hq + int64_t(col) * rows;
@@ -1073,12 +1072,13 @@ hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStrea
   if (p.n_items == 0) return hipSuccess;
   hipError_t e = launch_decode_kernel(p, dqk, stream);
   if (e != hipSuccess || !has_splits) return e;
-  // Merge: one work-group per (piece, column, slice of the output rows);
-  // only a split sequence's first piece has work, each thread at most a few
-  // (row, 4 columns) outputs so all their loads are in flight together.
+  // Merge: one work-group per (split sequence, column, slice of the output
+  // rows), each thread at most a few (row, 4 columns) outputs so all their
+  // loads are in flight together.
+  if (p.n_merge == 0) return hipSuccess;
   const int dv = dqk == 576 ? 512 : dqk;
   const int units = p.rows_per_wg * (dv / 4);
-  const dim3 mgrid(p.n_items, p.grid_y, std::min(8, (units + 255) / 256));
+  const dim3 mgrid(p.n_merge, p.grid_y, std::min(8, (units + 255) / 256));
   switch (dqk) {
     case 128: hipLaunchKernelGGL(merge_kernel<128>, mgrid, dim3(256), 0, stream, p); break;
     case 64: hipLaunchKernelGGL(merge_kernel<64>, mgrid, dim3(256), 0, stream, p); break;

@@ -12,14 +12,14 @@ namespace flexattn {
 // Plan word layout: a 16-word header, then 8 words per decode item, then 8
 // words per prefill item.
 constexpr int32_t kPlanMagic = 0x46504C58;
-constexpr int32_t kPlanVersion = 3;
+constexpr int32_t kPlanVersion = 4;
 constexpr int kHeaderWords = 20;
 constexpr int kItemWords = 8;
 
 enum HeaderField {
   H_MAGIC = 0, H_VERSION, H_NUM_SEQS, H_N_DEC_ITEMS, H_N_PRE_ITEMS, H_N_DEC_SEQS,
   H_N_PRE_SEQS, H_DEC_WIDTH, H_PRE_GRID_Y, H_OFF_DEC, H_OFF_PRE, H_PPS, H_CUS_DEC,
-  H_CUS_PRE, H_BM, H_TOTAL_WORDS, H_N_RANGES, H_OFF_RANGES, H_OFF_ORDER, H_RESERVED
+  H_CUS_PRE, H_BM, H_TOTAL_WORDS, H_N_RANGES, H_OFF_RANGES, H_OFF_ORDER, H_OFF_MERGE
 };
 
 // Decode item (one piece: the overlap of a balanced page range with one
@@ -29,7 +29,9 @@ enum HeaderField {
 // index). The range table after the decode items holds the first piece of
 // each range, then the piece count; the launch order after it lists the
 // pieces by key count descending (ties: slot) for launches of one
-// work-group per piece.
+// work-group per piece; the merge list after that holds, for each decode
+// sequence cut into several pieces (batch order), the index of its first
+// piece.
 // Prefill item words: seq, tile, row_begin, row_end, key_end, unused x3.
 
 // Most pages one balanced decode range may hold (its block-table entries are

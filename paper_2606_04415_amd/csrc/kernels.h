@@ -25,6 +25,8 @@ struct AttnParams {
   int32_t n_items;
   const int32_t* ranges;  // decode: first piece of each balanced range (+ the piece count)
   const int32_t* order;   // decode: pieces longest first, for one work-group per piece
+  const int32_t* merge;   // decode: first piece of every split sequence
+  int32_t n_merge;
   int32_t n_ranges;
   int32_t range_pages;    // decode: most pages a range holds
   float* ws_stats;        // decode: [item][W][rows][2] (max in log2 units, sum)

@@ -263,9 +263,13 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
     return pieces[a].k1 - pieces[a].k0 > pieces[b].k1 - pieces[b].k0;
   });
+  std::vector<int32_t> merge_list;   // first piece of every split sequence
+  for (size_t d = 0; d < dec.size(); ++d)
+    if (n_pieces[d] > 1) merge_list.push_back(first_piece[d]);
   const int32_t off_ranges = kHeaderWords + kItemWords * n_dec_items;
   const int32_t off_order = off_ranges + int32_t(ranges.size());
-  const int32_t off_pre = off_order + n_dec_items;
+  const int32_t off_merge = off_order + n_dec_items;
+  const int32_t off_pre = off_merge + int32_t(merge_list.size());
   const int32_t total = off_pre + kItemWords * n_pre_items;
   auto& w = plan->words;
   w.assign(kHeaderWords, 0);
@@ -288,9 +292,11 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   w[H_N_RANGES] = int32_t(R);
   w[H_OFF_RANGES] = off_ranges;
   w[H_OFF_ORDER] = off_order;
+  w[H_OFF_MERGE] = off_merge;
   w.insert(w.end(), dec_words.begin(), dec_words.end());
   w.insert(w.end(), ranges.begin(), ranges.end());
   w.insert(w.end(), order.begin(), order.end());
+  w.insert(w.end(), merge_list.begin(), merge_list.end());
   for (const Tile& t : tiles) {
     const int32_t item[kItemWords] = {t.s, t.t, t.r0, t.r1, t.kend, 0, 0, 0};
     w.insert(w.end(), item, item + kItemWords);

@@ -51,7 +51,10 @@ def check_invariants(sh, opts, qsl, ls, maxp):
     pre_items = [b[b[10] + 8 * i:b[10] + 8 * i + 8] for i in range(npf)]
     ranges = b[off_r:off_r + R + 1]
     order = b[b[18]:b[18] + nd]
-    assert off_r == b[9] + 8 * nd and b[18] == off_r + R + 1 and b[10] == b[18] + nd
+    assert off_r == b[9] + 8 * nd and b[18] == off_r + R + 1 and b[19] == b[18] + nd
+    merge = b[b[19]:b[10]]
+    assert merge == [i for i, it in enumerate(dec_items) if it[1] == 0 and it[2] > 1]
+    assert len(merge) == r.info["n_split_seqs"]
     assert sorted(order) == list(range(nd))
     keys = [(-(dec_items[i][4] - dec_items[i][3]), i) for i in order]
     assert keys == sorted(keys)                       # longest first, ties by slot
