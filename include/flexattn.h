@@ -57,6 +57,7 @@ extern "C" {
 /* Modes of flex_attn_mixed. */
 #define FLEX_MODE_SERIAL 0  /* prefill then decode on the caller stream, all CUs */
 #define FLEX_MODE_CORUN 1   /* prefill and decode on two CU-masked streams, joined */
+#define FLEX_MODE_FUSED 2   /* one launch holding both phases' work-groups, interleaved */
 
 /* Attention geometry of one layer.
  * Supported: (head_dim_qk, head_dim_v) in {(64,64), (128,128)} with
@@ -88,8 +89,9 @@ typedef struct flex_attn_plan_opts {
                                  [1 grouped-query, 2 for 576/512] */
   int32_t split_granule;      /* co-run split granularity in CUs [32] */
   double hbm_gbps;            /* cost model: device HBM bandwidth [8000] */
-  double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws [60] */
-  double prefill_tflops_per_cu; /* cost model: prefill rate of one CU [5] */
+  double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws [37] */
+  double prefill_tflops_per_cu; /* cost model: prefill rate of one CU [4] (both defaults
+                                   measured with half an MI355X running the phase) */
 } flex_attn_plan_opts;
 
 /* Summary of a plan. */
@@ -112,6 +114,8 @@ typedef struct flex_attn_plan_info {
   size_t workspace_bytes;    /* bytes of workspace decode needs (0 if none) */
   double decode_bytes;       /* algorithmic KV bytes of the decode phase */
   double prefill_flops;      /* algorithmic flops of the prefill phase */
+  int32_t n_fused_wgs;       /* work-groups of the one-launch (FUSED) form; 0 when the
+                                shape has none (see flex_attn_mixed) */
 } flex_attn_plan_info;
 
 /* Device tensors of one run. Strides are in elements.
@@ -208,9 +212,19 @@ int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, 
  * decode on stream; FLEX_MODE_CORUN forks stream into the two CU-masked
  * streams of corun (prefill on its prefill stream, decode on its decode
  * stream) and joins them back into stream, the one-device analog of the
- * paper's dynamic co-location (Sec. 3.4). Outputs are bit-identical between
- * the modes for the same plan. For SERIAL, corun may be NULL; if given, it is
- * used only for phase timing (flex_attn_corun_set_timing). For CORUN, pass a
+ * paper's dynamic co-location (Sec. 3.4). FLEX_MODE_FUSED runs both phases
+ * in one launch on stream (then the split-K merge): each work-group of the
+ * launch serves one prefill work-group's tile and column or one or two
+ * decode ranges, in the plan's fused order, which interleaves the phases so
+ * they progress together; the device's dispatcher hands work-groups to
+ * compute units as they free up, so the phases share the device without CU
+ * masks (the alternative to two streams; an analog of the paper's temporal
+ * sharing, Sec. 3.4). FUSED needs a plan with n_fused_wgs > 0: grouped-query
+ * heads with G = Hq / Hkv > 4, 3 <= Hkv <= 8 and 32-row tiles; otherwise it
+ * returns FLEX_ERR_UNSUPPORTED. Outputs are bit-identical between the three
+ * modes for the same plan. corun is ignored by FUSED. For SERIAL, corun may
+ * be NULL; if given, it is used only for phase timing
+ * (flex_attn_corun_set_timing). For CORUN, pass a
  * stream of your own, not HIP's legacy default (NULL) stream: that stream
  * synchronizes implicitly with the pair's streams, which stalls the host at
  * every step (measured: 230 us of host time per step instead of 24). */

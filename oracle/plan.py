@@ -42,9 +42,28 @@ the contract is:
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
 
-Blob layout (int32, version 4): 20-word header (word 19: offset of the
-merge list), 8 words per decode item, the range table, the piece launch
-order, the merge list, 8 words per prefill item; see ``build_plan``.
+* fused order (one launch for both phases), only for grouped-query heads
+  with G > 4, W = 1, 3 <= Hkv <= 8 and BM = 32 (else empty): prefill
+  work-group e = tile * grid_y + column, decode work-group j holding ranges
+  [rpw j, rpw j + rpw) (rpw = 2 when Hkv <= 4, else 1) as entry
+  n_tiles * grid_y + j. Launch work-group b runs on XCD b % 8; prefill
+  column c belongs to XCD c + grid_y * (tile % (8 / grid_y)) when grid_y
+  divides 8 (else to XCD entry % 8), decode work-group j to XCD j % 8. Each
+  XCD's entries are listed by their start time in a simulation of its
+  cus_total / 8 CUs split into a decode pool of cus_decode / cus_total of
+  them (half without a split; at least one CU each; all of them when the
+  other phase has no work there) and a prefill pool of the rest, each pool
+  giving its phase's work-groups, in order, to its earliest-free CU (lowest
+  index on ties). Durations in whole ns plus one: prefill
+  2 (d_qk + d_v) x heads of the column x causal pairs of the tile /
+  (prefill_tflops_per_cu 1e12); decode pages of the ranges x page bytes /
+  (decode_gbps_per_cu 1e9). Ties in start time: prefill first, then phase
+  order. Entry 8 k + x is the k-th of XCD x's list, -1 past its end.
+
+Blob layout (int32, version 5): 22-word header (word 19: offset of the
+merge list, 20: offset of the fused order, 21: its length), 8 words per
+decode item, the range table, the piece launch order, the merge list, 8
+words per prefill item, the fused order; see ``build_plan``.
 """
 from __future__ import annotations
 
@@ -54,9 +73,13 @@ from typing import List, Optional, Sequence
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
 MAGIC = 0x46504C58
-VERSION = 4
-HEADER = 20
+VERSION = 5
+HEADER = 22
 ITEM = 8
+# cost-model rates of one CU when the options leave them 0 (the library's
+# defaults: measured with half of an MI355X running one phase alone)
+DEFAULT_DECODE_GBPS_PER_CU = 37.0
+DEFAULT_PREFILL_TFLOPS_PER_CU = 4.0
 
 
 def cdiv(a: int, b: int) -> int:
@@ -84,8 +107,8 @@ class Opts:
     wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 2 (576/512 latent layout)
     split_granule: int = 0       # 0 -> 32
     hbm_gbps: float = 0.0        # 0 -> 8000
-    decode_gbps_per_cu: float = 0.0   # 0 -> 60
-    prefill_tflops_per_cu: float = 0.0  # 0 -> 5
+    decode_gbps_per_cu: float = 0.0   # 0 -> 37
+    prefill_tflops_per_cu: float = 0.0  # 0 -> 4
 
 
 @dataclass
@@ -179,8 +202,8 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         cus_decode = o.cus_decode
     else:
         hbm = (o.hbm_gbps or 8000.0) * 1e9
-        bw_cu = (o.decode_gbps_per_cu or 60.0) * 1e9
-        fl_cu = (o.prefill_tflops_per_cu or 5.0) * 1e12
+        bw_cu = (o.decode_gbps_per_cu or DEFAULT_DECODE_GBPS_PER_CU) * 1e9
+        fl_cu = (o.prefill_tflops_per_cu or DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
         best, best_t = None, None
         nd = granule
         while nd < cus_total:
@@ -240,9 +263,16 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     total = off_pre + ITEM * np_
     G = sh.num_q_heads // sh.num_kv_heads
     pre_height = sh.num_q_heads if mla or split else sh.num_kv_heads * cdiv(G, 8)
+    fused = fused_order(tiles, pre_height, R, T, heads_per_wg,
+                        not mla and not split and G > 4 and W == 1 and heads_per_wg >= 3 and bm == 32,
+                        G=G, sh=sh, o=o, cus_total=cus_total, cus_decode=cus_decode)
+    off_fused = total
+    total += len(fused)
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
-           HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, off_merge]
-    blob = hdr + [x for it in dec_items for x in it] + ranges + order + merge + [x for it in tiles for x in it]
+           HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, off_merge,
+           off_fused, len(fused)]
+    blob = (hdr + [x for it in dec_items for x in it] + ranges + order + merge + [x for it in tiles for x in it]
+            + fused)
     # workspace: (max, sum) per decode item, column and row, then the partial outputs;
     # only needed when some decode sequence is split
     if n_split == 0:
@@ -255,5 +285,61 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
                 n_decode_ranges=R, prefill_grid_y=pre_height, pages_per_split=ppr,
                 cus_decode=cus_decode, cus_prefill=cus_prefill, bm=bm,
                 plan_words=total, device_plan_bytes=cdiv(total * 4, 256) * 256,
-                workspace_bytes=ws, decode_bytes=dec_bytes, prefill_flops=pre_flops)
+                workspace_bytes=ws, decode_bytes=dec_bytes, prefill_flops=pre_flops, n_fused_wgs=len(fused))
     return PlanResult(OK, blob, info)
+
+
+def fused_order(tiles, grid_y: int, R: int, T: int, kv_heads_per_wg: int, fusable: bool, *, G: int,
+                sh: "Shape", o: "Opts", cus_total: int, cus_decode: int) -> List[int]:
+    """Work of each work-group of the one-launch form (see the module contract)."""
+    if not fusable or (not tiles and R == 0):
+        return []
+    per_wg = 2 if kv_heads_per_wg <= 4 else 1        # decode ranges per work-group
+    n_pre_wg = len(tiles) * grid_y
+    fl_cu = (o.prefill_tflops_per_cu or DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
+    bw_cu = (o.decode_gbps_per_cu or DEFAULT_DECODE_GBPS_PER_CU) * 1e9
+    pre_q = [[] for _ in range(8)]                  # per XCD: (entry, duration in ns)
+    dec_q = [[] for _ in range(8)]
+    columns_per_kv = cdiv(G, 8)
+    for i, t in enumerate(tiles):
+        r0, r1, kend = t[2], t[3], t[4]
+        # query row r of the tile sees keys 0 .. kend - r1 + r (inclusive)
+        pairs = sum(kend - r1 + r + 1 for r in range(r0, r1))
+        for c in range(grid_y):
+            e = i * grid_y + c
+            x = c + grid_y * (i % (8 // grid_y)) if 8 % grid_y == 0 else e % 8
+            heads = min(8, G - 8 * (c % columns_per_kv))
+            flops = float(pairs) * float(heads) * float(2 * (sh.head_dim_qk + sh.head_dim_v))
+            pre_q[x].append((e, int(flops / fl_cu * 1e9) + 1))
+    page_bytes = sh.page_size * sh.num_kv_heads * (sh.head_dim_qk + sh.head_dim_v) * 2
+    for j in range(cdiv(R, per_wg)):
+        lo, hi = per_wg * j, min(R, per_wg * j + per_wg)
+        nbytes = float((hi * T) // R - (lo * T) // R) * float(page_bytes)
+        dec_q[j % 8].append((n_pre_wg + j, int(nbytes / bw_cu * 1e9) + 1))
+    cap = max(2, cus_total // 8)                     # CUs of one XCD
+    n_dec_cus = cus_decode * cap // cus_total if cus_decode < cus_total else cap // 2
+    n_dec_cus = min(cap - 1, max(1, n_dec_cus))
+
+    def starts(queue, machines):
+        # each work-group, in order, to the CU that frees up first (lowest index on ties)
+        free_at = [0] * machines
+        out = []
+        for _, dur in queue:
+            q = free_at.index(min(free_at))
+            out.append(free_at[q])
+            free_at[q] += dur
+        return out
+
+    lists = []
+    for x in range(8):
+        sp = starts(pre_q[x], cap if not dec_q[x] else cap - n_dec_cus)
+        sd = starts(dec_q[x], cap if not pre_q[x] else n_dec_cus)
+        ev = [(t0, 0, k) for k, t0 in enumerate(sp)] + [(t0, 1, k) for k, t0 in enumerate(sd)]
+        ev.sort()
+        lists.append([pre_q[x][k][0] if kind == 0 else dec_q[x][k][0] for _, kind, k in ev])
+    longest = max(len(l) for l in lists)
+    order = [-1] * (8 * longest)
+    for x in range(8):
+        for k, e in enumerate(lists[x]):
+            order[8 * k + x] = e
+    return order

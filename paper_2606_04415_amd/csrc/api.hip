@@ -134,6 +134,34 @@ int run_prefill(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "prefill launch");
 }
 
+// Both phases in one launch through the plan's fused order.
+int run_fused(const flex_attn_plan_t* plan, const AttnParams& p, const flex_attn_args* a, hipStream_t s) {
+  const flex_attn_plan_info& info = plan->info;
+  if (info.n_prefill_items + info.n_decode_items == 0) return FLEX_OK;
+  const int32_t n = plan->words[H_N_FUSED];
+  if (n == 0)
+    return set_error(FLEX_ERR_UNSUPPORTED,
+                     "no one-launch form for this plan (needs grouped-query heads, G > 4, 3..8 KV heads, bm 32)");
+  const int32_t* d = static_cast<const int32_t*>(a->d_plan);
+  AttnParams pp = p, pd = p;
+  pp.items = d + plan->words[H_OFF_PRE];
+  pp.n_items = info.n_prefill_items;
+  pp.grid_y = info.prefill_grid_y;
+  pd.items = d + plan->words[H_OFF_DEC];
+  pd.n_items = info.n_decode_items;
+  pd.ranges = d + plan->words[H_OFF_RANGES];
+  pd.n_ranges = plan->words[H_N_RANGES];
+  pd.order = d + plan->words[H_OFF_ORDER];
+  pd.merge = d + plan->words[H_OFF_MERGE];
+  pd.n_merge = info.n_split_seqs;
+  pd.range_pages = info.pages_per_split;
+  pd.grid_y = info.decode_wg_width;
+  const int heads_per_wg = plan->rows_per_wg / p.G;
+  const hipError_t e = launch_fused(pp, pd, d + plan->words[H_OFF_FUSED], n, plan->shape.head_dim_qk,
+                                    heads_per_wg <= 4 ? 2 : 1, info.n_split_seqs > 0, s);
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "fused launch");
+}
+
 // CU masks in eighths of the device. On MI355X (8 XCDs x 4 shader engines x 8
 // CUs) mask bit i selects a CU of XCD i % 8, shader engine (i >> 3) & 3,
 // position i >> 5 within the engine (measured by recording the hardware ids
@@ -207,11 +235,13 @@ extern "C" int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_a
 extern "C" int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode, void* stream,
                                flex_attn_corun_t* corun) {
   clear_error();
-  if (mode != FLEX_MODE_SERIAL && mode != FLEX_MODE_CORUN) return set_error(FLEX_ERR_INVALID_ARG, "unknown mode");
+  if (mode != FLEX_MODE_SERIAL && mode != FLEX_MODE_CORUN && mode != FLEX_MODE_FUSED)
+    return set_error(FLEX_ERR_INVALID_ARG, "unknown mode");
   AttnParams p;
   int st = prepare(plan, args, &p);
   if (st != FLEX_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (mode == FLEX_MODE_FUSED) return run_fused(plan, p, args, s);
   const bool has_pre = plan->info.n_prefill_items > 0, has_dec = plan->info.n_decode_items > 0;
   auto pre = [&](hipStream_t ps) { return run_prefill(plan, p, args, ps); };
   auto dec = [&](hipStream_t ds) { return run_decode(plan, p, args, ds); };

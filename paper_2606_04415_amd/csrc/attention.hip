@@ -172,9 +172,13 @@ struct DecodeCursor {
 
 __device__ __forceinline__ int pages_in(int k0, int k1, int P) { return (k1 - 1) / P - k0 / P + 1; }
 
+// One decode work-group's work: balanced range `range` (-1: none) of the
+// plan, column `col` of W, with threads tid = 0 .. NW*64-1 and the range's
+// block-table window at s_pt. Every call passes exactly one work-group
+// barrier (two or more per piece with COMBINE).
 template <int D, int NW, int P, bool COMBINE, bool NT>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 8)))
-void decode_gqa_kernel(AttnParams p) {
+__device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, int col, int W, int tid,
+                                                int* s_pt) {
   // K/V loads marked non-temporal when the launch has the whole device: with
   // every CU streaming the cache this measured 12% faster (6.2 vs 5.6 TB/s),
   // on a half-device co-run share it measured slower.
@@ -183,7 +187,6 @@ void decode_gqa_kernel(AttnParams p) {
   constexpr int DC = D / 32;   // 32-dim chunks of the QK^T contraction
   constexpr int DPL = D / 16;  // value dims each lane owns in PV
   using Chunk = DecodeChunk<D>;
-  const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
@@ -191,9 +194,9 @@ void decode_gqa_kernel(AttnParams p) {
   const int HW = p.rows_per_wg / G;        // KV heads of this work-group
   const int WPH = max(1, NW / HW);         // waves per head
   const int hh = w / WPH, u = w % WPH;     // this wave's head within the group, rank among its waves
-  const int g = blockIdx.y * HW + hh;      // this wave's KV head
+  const int g = col * HW + hh;             // this wave's KV head
   const bool active = hh < HW && g < p.Hkv;
-  const int i_begin = p.ranges[blockIdx.x], i_end = p.ranges[blockIdx.x + 1];
+  const int i_begin = range >= 0 ? p.ranges[range] : 0, i_end = range >= 0 ? p.ranges[range + 1] : 0;
   // Byte strides (the host checks that a page's slots span less than 2^31
   // bytes) and per-lane byte offsets of a chunk's loads from the page bases.
   const uint8_t* kbase_b = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(active ? g : 0) * p.kc.sh);
@@ -202,7 +205,6 @@ void decode_gqa_kernel(AttnParams p) {
   const uint32_t vsp_b = uint32_t(p.vc.sp) * 2u, vss_b = uint32_t(p.vc.ss) * 2u;
   const uint32_t k_lane = uint32_t(n) * kss_b + 16u * gq;
   const uint32_t v_lane = uint32_t(4 * gq) * vss_b + 2u * DPL * n;
-  extern __shared__ int s_pt[];   // block-table entries of the range
   __shared__ float s_m[NW][16];
   __shared__ float s_l[NW][16];
   __shared__ float s_o[COMBINE ? NW : 1][16][D];   // wave combine (several waves per head)
@@ -317,7 +319,7 @@ void decode_gqa_kernel(AttnParams p) {
     const int32_t* it = p.items + 8 * i;
     const int nspl = it[2];
     const int tok = it[6];
-    const int64_t slot = int64_t(it[7]) * gridDim.y + blockIdx.y;   // this piece's workspace slot
+    const int64_t slot = int64_t(it[7]) * W + col;   // this piece's workspace slot
     const float ltot = group_sum(l);
     if constexpr (!COMBINE) {   // one wave per head
       if (active) {
@@ -371,7 +373,7 @@ void decode_gqa_kernel(AttnParams p) {
       for (int idx = tid; idx < HW * G * (D / 2); idx += NW * 64) {
         const int h = idx / (G * (D / 2));
         const int row = (idx / (D / 2)) % G, d = 2 * (idx % (D / 2));
-        const int gh = blockIdx.y * HW + h;
+        const int gh = col * HW + h;
         if (gh >= p.Hkv) continue;
         const int w0 = h * WPH;
         float M = s_m[w0][row];
@@ -439,6 +441,14 @@ void decode_gqa_kernel(AttnParams p) {
     c = c3;
   }
   for (; fin < i_end; ++fin) finish(fin);
+}
+
+template <int D, int NW, int P, bool COMBINE, bool NT>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void decode_gqa_kernel(AttnParams p) {
+  extern __shared__ int s_pt[];   // block-table entries of the range
+  decode_gqa_body<D, NW, P, COMBINE, NT>(p, int(blockIdx.x), int(blockIdx.y), int(gridDim.y), int(threadIdx.x),
+                                         s_pt);
 }
 
 // ---------------------------------------------------------------------------
@@ -531,9 +541,10 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   wait_vmem<0>();
 }
 
+// One work-group's work: item `item` of the phase, column `col`, threads
+// 0 .. NW*64-1 of the work-group, the work-group's dynamic LDS.
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)))
-void rowpar_kernel(AttnParams p) {
+__device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int col) {
   using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
   static_assert(NS >= 2 && NS <= 6, "stages");
   static_assert(BN % 32 == 0, "whole 32-key chunks per tile");
@@ -545,27 +556,6 @@ void rowpar_kernel(AttnParams p) {
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, gq = lane >> 4;
-  // Work-group -> (item, column). Decode pieces launch longest first; prefill
-  // tiles are listed that way. Grouped-query prefill with a column count
-  // dividing 8 runs a 1-D grid in which work-group id sits on XCD id % 8
-  // (round-robin dispatch) and serves column (id % 8) % grid_y: every XCD
-  // then reads the K/V of one KV head only, which its L2 can hold, instead
-  // of every head's.
-  int item = int(blockIdx.x), col = int(blockIdx.y);
-  if (MODE == kPrefillGrouped && p.xcd_remap) {
-    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
-    col = x % p.grid_y;
-    item = j * (8 / p.grid_y) + x / p.grid_y;
-    if (item >= p.n_items) return;
-  }
-  // One query head per work-group (a multiple of 8 heads): head h runs on
-  // XCD h % 8 for all its tiles, tiles longest first, so each XCD's L2 holds
-  // the keys and values of its own heads only.
-  if (MODE == kPrefillPerHead && p.xcd_remap) {
-    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3, hp8 = p.grid_y / 8;
-    item = j / hp8;
-    col = (j % hp8) * 8 + x;
-  }
   const int32_t* it = p.items + 8 * (MODE == kDecodeLatent ? p.order[item] : item);
   const int seq = it[0];
   const int L = p.seq_lens[seq];
@@ -645,11 +635,20 @@ void rowpar_kernel(AttnParams p) {
   }
 
   float m[RB];
+  // Row sums of the probabilities: through the MFMA unit against a ones
+  // operand (lsum, rows 4*gq + r like the accumulators), or, for the 576-wide
+  // latent rows, whose operands fill the register file, as one partial per
+  // lane on the VALU (lpart, row n, this lane's keys; summed over the four
+  // lane groups at the end). Both add the bf16-rounded probabilities that
+  // feed the P x V product.
+  constexpr bool kValuSum = VALIAS;
   f32x4 o[RB][C::NACC], lsum[RB];
+  float lpart[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     m[rb] = -INFINITY;
     lsum[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    lpart[rb] = 0.f;
 #pragma unroll
     for (int a = 0; a < C::NACC; ++a) o[rb][a] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -844,10 +843,11 @@ void rowpar_kernel(AttnParams p) {
         const float m_new = need ? cmax[rb] : m[rb];
         const float alpha = fast_exp2(m[rb] - m_new);   // 1 if unchanged, 0 from -inf
         m[rb] = m_new;
+        if constexpr (kValuSum) lpart[rb] *= alpha;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float ar = shfl_f(alpha, 4 * gq + r);
-          lsum[rb][r] *= ar;
+          if constexpr (!kValuSum) lsum[rb][r] *= ar;
 #pragma unroll
           for (int a = 0; a < C::NACC; ++a) o[rb][a][r] *= ar;
         }
@@ -867,8 +867,10 @@ void rowpar_kernel(AttnParams p) {
           const int r = 2 * (e2 & 1);
           pop[rb][e2] = pack_bf16x2(fast_exp2(fmaf(sb[r], p.scale_log2, neg_m)),
                                     fast_exp2(fmaf(sb[r + 1], p.scale_log2, neg_m)));
+          if constexpr (kValuSum)
+            lpart[rb] += __uint_as_float(pop[rb][e2] << 16) + __uint_as_float(pop[rb][e2] & 0xFFFF0000u);
         }
-        lsum[rb] = mfma_16x16x32(pop[rb], ones, lsum[rb]);
+        if constexpr (!kValuSum) lsum[rb] = mfma_16x16x32(pop[rb], ones, lsum[rb]);
       }
       // Transposing LDS reads give each lane its 8 keys of value column
       // 16cv + n (keys 4gq + e and 16 + 4gq + e of the chunk).
@@ -932,7 +934,11 @@ void rowpar_kernel(AttnParams p) {
   }
 
   // Epilogue. Lane (n, gq) holds rows 4*gq + r of each row block at value
-  // columns 16*cv + n, and each row's probability sum in lsum[r].
+  // columns 16*cv + n, and each row's probability sum in lsum[r] (or the
+  // total of row n in ltot, from the per-lane partials).
+  float ltot[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) ltot[rb] = kValuSum ? group_sum(lpart[rb]) : 0.f;
   if constexpr (MODE != kDecodeLatent) {
     if (!wave_on) return;
     const int r0 = it[2], r1 = it[3];
@@ -943,8 +949,8 @@ void rowpar_kernel(AttnParams p) {
       for (int r = 0; r < 4; ++r) {
         const int local = r0 + blk * 16 + 4 * gq + r;
         const float mr = shfl_f(m[rb], 4 * gq + r);
+        const float lr = kValuSum ? shfl_f(ltot[rb], 4 * gq + r) : lsum[rb][r];
         if (local < r1) {
-          const float lr = lsum[rb][r];
           const float inv = 1.f / lr;
           uint16_t* dst = p.out + (int64_t(q0 + local) * p.Hq + row_head[rb]) * DV + n;
 #pragma unroll
@@ -967,7 +973,7 @@ void rowpar_kernel(AttnParams p) {
       for (int r = 0; r < 4; ++r) {
         const int rowi = (w * RB + rb) * 16 + 4 * gq + r;
         const float mr = shfl_f(m[rb], 4 * gq + r);
-        const float lr = lsum[rb][r];
+        const float lr = kValuSum ? shfl_f(ltot[rb], 4 * gq + r) : lsum[rb][r];
         if (nspl == 1) {
           const float inv = 1.f / lr;
           uint16_t* dst = p.out + (out_row0 + rowi) * DV + n;
@@ -987,6 +993,103 @@ void rowpar_kernel(AttnParams p) {
       }
     }
   }
+}
+
+template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)))
+void rowpar_kernel(AttnParams p) {
+  // Work-group -> (item, column). Decode pieces launch longest first; prefill
+  // tiles are listed that way. Grouped-query prefill with a column count
+  // dividing 8 runs a 1-D grid in which work-group id sits on XCD id % 8
+  // (round-robin dispatch) and serves column (id % 8) % grid_y: every XCD
+  // then reads the K/V of one KV head only, which its L2 can hold, instead
+  // of every head's.
+  int item = int(blockIdx.x), col = int(blockIdx.y);
+  if (MODE == kPrefillGrouped && p.xcd_remap) {
+    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
+    col = x % p.grid_y;
+    item = j * (8 / p.grid_y) + x / p.grid_y;
+    if (item >= p.n_items) return;
+  }
+  // One query head per work-group (a multiple of 8 heads): head h runs on
+  // XCD h % 8 for all its tiles, tiles longest first, so each XCD's L2 holds
+  // the keys and values of its own heads only.
+  if (MODE == kPrefillPerHead && p.xcd_remap) {
+    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3, hp8 = p.grid_y / 8;
+    item = j / hp8;
+    col = (j % hp8) * 8 + x;
+  }
+  rowpar_body<DQK, DV, NW, RB, BN, VALIAS, MODE, P, NS, TB>(p, item, col);
+}
+
+// ---------------------------------------------------------------------------
+// One-launch mixed step (grouped-query heads): work-group b takes entry
+// order[b] of the plan's fused order, either one prefill work-group (tile,
+// column), served by the 8-wave, 32-row-per-wave prefill body, or one
+// decode work-group of RPW balanced ranges, a 4-wave decode body per range
+// (RPW = 2) or one 8-wave body (RPW = 1). Prefill and decode work-groups
+// share the device in the proportion the order interleaves them, instead
+// of two CU-masked streams; the dispatcher hands work-groups out in id
+// order as compute units free up. Decode K/V loads are plain (the phase
+// never has the whole device to itself). Entries < 0 are padding.
+// ---------------------------------------------------------------------------
+template <int D, int P, int RPW>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+void fused_kernel(AttnParams pp, AttnParams pd, const int32_t* order) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+  constexpr int NS = D == 128 ? 3 : 4;
+  const int e = order[blockIdx.x];
+  if (e < 0) return;
+  const int n_pre = pp.n_items * pp.grid_y;
+  if (e < n_pre) {
+    rowpar_body<D, D, 8, 2, 64, false, kPrefillGrouped, P, NS, 1>(pp, e / pp.grid_y, e % pp.grid_y);
+    return;
+  }
+  const int j = e - n_pre;
+  constexpr int DNW = 8 / RPW;
+  const int sub = int(threadIdx.x) / (DNW * 64);
+  const int r = RPW * j + sub;
+  decode_gqa_body<D, DNW, P, false, false>(pd, r < pd.n_ranges ? r : -1, 0, 1, int(threadIdx.x) % (DNW * 64),
+                                           reinterpret_cast<int*>(lds) + sub * pd.range_pages);
+}
+
+template <int D, int P, int RPW>
+static hipError_t launch_fused_t(const AttnParams& pp, const AttnParams& pd, const int32_t* order, int n_order,
+                                 hipStream_t stream) {
+  constexpr int NS = D == 128 ? 3 : 4;
+  using C = RowParCfg<D, D, 8, 2, 64, false, NS>;
+  const size_t dec_lds = size_t(RPW) * size_t(pd.range_pages) * 4;
+  const size_t lds = C::LDS_BYTES > dec_lds ? C::LDS_BYTES : dec_lds;
+  auto kern = fused_kernel<D, P, RPW>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(n_order), dim3(512), lds, stream, pp, pd, order);
+  return hipGetLastError();
+}
+
+static hipError_t launch_merge(const AttnParams& p, int dqk, hipStream_t stream);
+
+hipError_t launch_fused(const AttnParams& pp, const AttnParams& pd, const int32_t* order, int n_order, int dqk,
+                        int ranges_per_wg, bool has_splits, hipStream_t stream) {
+  if (n_order == 0) return hipSuccess;
+  if (pd.P != 16 && pd.P != 64) return hipErrorInvalidValue;
+  if (dqk != 64 && dqk != 128) return hipErrorInvalidValue;
+  if (ranges_per_wg != 1 && ranges_per_wg != 2) return hipErrorInvalidValue;
+  const bool p16 = pd.P == 16, two = ranges_per_wg == 2;
+  hipError_t e;
+  if (dqk == 128)
+    e = p16 ? (two ? launch_fused_t<128, 16, 2>(pp, pd, order, n_order, stream)
+                   : launch_fused_t<128, 16, 1>(pp, pd, order, n_order, stream))
+            : (two ? launch_fused_t<128, 64, 2>(pp, pd, order, n_order, stream)
+                   : launch_fused_t<128, 64, 1>(pp, pd, order, n_order, stream));
+  else
+    e = p16 ? (two ? launch_fused_t<64, 16, 2>(pp, pd, order, n_order, stream)
+                   : launch_fused_t<64, 16, 1>(pp, pd, order, n_order, stream))
+            : (two ? launch_fused_t<64, 64, 2>(pp, pd, order, n_order, stream)
+                   : launch_fused_t<64, 64, 1>(pp, pd, order, n_order, stream));
+  if (e != hipSuccess || !has_splits || pd.n_items == 0) return e;
+  return launch_merge(pd, dqk, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -1068,13 +1171,10 @@ static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t
   }
 }
 
-hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStream_t stream) {
-  if (p.n_items == 0) return hipSuccess;
-  hipError_t e = launch_decode_kernel(p, dqk, stream);
-  if (e != hipSuccess || !has_splits) return e;
-  // Merge: one work-group per (split sequence, column, slice of the output
-  // rows), each thread at most a few (row, 4 columns) outputs so all their
-  // loads are in flight together.
+// Merge: one work-group per (split sequence, column, slice of the output
+// rows), each thread at most a few (row, 4 columns) outputs so all their
+// loads are in flight together.
+static hipError_t launch_merge(const AttnParams& p, int dqk, hipStream_t stream) {
   if (p.n_merge == 0) return hipSuccess;
   const int dv = dqk == 576 ? 512 : dqk;
   const int units = p.rows_per_wg * (dv / 4);
@@ -1086,6 +1186,13 @@ hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStrea
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStream_t stream) {
+  if (p.n_items == 0) return hipSuccess;
+  hipError_t e = launch_decode_kernel(p, dqk, stream);
+  if (e != hipSuccess || !has_splits) return e;
+  return launch_merge(p, dqk, stream);
 }
 
 // Grouped-query prefill: one wave per query head of a KV head (4 waves when

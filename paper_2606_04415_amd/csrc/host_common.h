@@ -9,17 +9,19 @@
 
 namespace flexattn {
 
-// Plan word layout: a 16-word header, then 8 words per decode item, then 8
-// words per prefill item.
+// Plan word layout: a 22-word header, 8 words per decode item, the range
+// table, the piece launch order, the merge list, 8 words per prefill item,
+// the fused order.
 constexpr int32_t kPlanMagic = 0x46504C58;
-constexpr int32_t kPlanVersion = 4;
-constexpr int kHeaderWords = 20;
+constexpr int32_t kPlanVersion = 5;
+constexpr int kHeaderWords = 22;
 constexpr int kItemWords = 8;
 
 enum HeaderField {
   H_MAGIC = 0, H_VERSION, H_NUM_SEQS, H_N_DEC_ITEMS, H_N_PRE_ITEMS, H_N_DEC_SEQS,
   H_N_PRE_SEQS, H_DEC_WIDTH, H_PRE_GRID_Y, H_OFF_DEC, H_OFF_PRE, H_PPS, H_CUS_DEC,
-  H_CUS_PRE, H_BM, H_TOTAL_WORDS, H_N_RANGES, H_OFF_RANGES, H_OFF_ORDER, H_OFF_MERGE
+  H_CUS_PRE, H_BM, H_TOTAL_WORDS, H_N_RANGES, H_OFF_RANGES, H_OFF_ORDER, H_OFF_MERGE,
+  H_OFF_FUSED, H_N_FUSED
 };
 
 // Decode item (one piece: the overlap of a balanced page range with one
@@ -33,6 +35,28 @@ enum HeaderField {
 // sequence cut into several pieces (batch order), the index of its first
 // piece.
 // Prefill item words: seq, tile, row_begin, row_end, key_end, unused x3.
+// Fused order (one launch for both phases, FLEX_MODE_FUSED): entry b is the
+// work of launch work-group b: e < n_pre_items * prefill_grid_y is prefill
+// work-group e (tile e / grid_y, column e % grid_y); e >= that is decode
+// work-group j = e - n_pre_items * prefill_grid_y, balanced ranges
+// [rpw * j, rpw * j + rpw) (rpw = 2 when a decode work-group covers at most
+// 4 KV heads, else 1); -1 is padding. Work-group b runs on XCD b % 8 (the
+// dispatcher deals work-groups to XCDs in turn, and within an XCD in id order
+// as CUs free up). Prefill column c goes to the XCDs x with x % grid_y == c
+// when grid_y divides 8 (as the prefill launch places them), other entries
+// to XCD (index % 8). Per XCD the entries are listed by the start time a
+// simulation gives them: the XCD's CUs (cus_total / 8) form a prefill pool
+// and a decode pool sized by the plan's split (cus_decode / cus_total of
+// them decode, half when the plan has no split, at least one each; a phase
+// with no work on the XCD leaves the other all of them); each pool hands its
+// phase's work-groups, in phase order, to its earliest-free CU (lowest index
+// on ties), a work-group lasting its cost-model time in whole ns plus one
+// (prefill: 2 (d_qk + d_v) x its query heads x the tile's causal query-key
+// pairs / prefill_tflops_per_cu; decode: the ranges' pages x page bytes /
+// decode_gbps_per_cu); ties in start time list prefill first, then phase
+// order. Empty (0 entries) when the shape has no fused form: grouped-query
+// heads, G > 4, 3..8 KV heads, 32-row tiles.
+constexpr int kFusedMinKvHeads = 3;
 
 // Most pages one balanced decode range may hold (its block-table entries are
 // staged in LDS by the decode kernel).
@@ -41,6 +65,12 @@ constexpr int64_t kMaxRangePages = 8192;
 // KV heads one grouped-query decode work-group covers (one wave each, or
 // several waves per head when fewer heads than 4).
 constexpr int32_t kDecodeHeadsPerWG = 8;
+
+// Cost-model rates of one CU when the options leave them 0: measured on
+// MI355X with half the device (128 CUs) running one phase of the
+// Qwen2.5-7B-shaped mixed step alone (decode 4.79 TB/s, prefill 511 TFLOP/s).
+constexpr double kDefaultDecodeGBpsPerCU = 37.0;
+constexpr double kDefaultPrefillTFlopsPerCU = 4.0;
 
 // Rows (query heads) one decode work-group owns in the 576/512 layout.
 constexpr int kLatentRowsPerWG = 64;       // latent heads must be a multiple of this

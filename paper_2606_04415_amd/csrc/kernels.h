@@ -42,6 +42,11 @@ struct AttnParams {
 
 hipError_t launch_decode(const AttnParams& p, int head_dim_qk, bool has_splits, hipStream_t stream);
 hipError_t launch_prefill(const AttnParams& p, int head_dim_qk, int bm, hipStream_t stream);
+// One launch for both phases (grouped-query heads, 32-row prefill tiles):
+// pp / pd are the prefill and decode parameter blocks, order the plan's fused
+// order (n_order entries), then the split-K merge when has_splits.
+hipError_t launch_fused(const AttnParams& pp, const AttnParams& pd, const int32_t* order, int n_order,
+                        int head_dim_qk, int ranges_per_wg, bool has_splits, hipStream_t stream);
 hipError_t launch_gather(const CacheRef& kc, const CacheRef& vc, bool has_v, const int32_t* bt_row,
                          int32_t L, int32_t P, int32_t Hkv, int32_t dqk, int32_t dv,
                          uint16_t* k_out, uint16_t* v_out, hipStream_t stream);

@@ -170,8 +170,8 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     cus_decode = o.cus_decode;
   } else {
     const double hbm = (o.hbm_gbps != 0.0 ? o.hbm_gbps : 8000.0) * 1e9;
-    const double bw_cu = (o.decode_gbps_per_cu != 0.0 ? o.decode_gbps_per_cu : 60.0) * 1e9;
-    const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : 5.0) * 1e12;
+    const double bw_cu = (o.decode_gbps_per_cu != 0.0 ? o.decode_gbps_per_cu : kDefaultDecodeGBpsPerCU) * 1e9;
+    const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : kDefaultPrefillTFlopsPerCU) * 1e12;
     int64_t best = -1;
     double best_t = 0.0;
     for (int64_t nd = granule; nd < cus_total; nd += granule) {
@@ -251,6 +251,77 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     return a.t < b.t;
   });
 
+  // Fused order for FLEX_MODE_FUSED (its layout and rule are described with
+  // the plan words in host_common.h).
+  std::vector<int32_t> fused;
+  const bool fusable = !latent && !split && G > 4 && W == 1 && heads_per_wg >= kFusedMinKvHeads && bm == 32;
+  if (fusable && (!tiles.empty() || !pieces.empty())) {
+    const int64_t rpw = heads_per_wg <= 4 ? 2 : 1;
+    const int64_t J = cdiv(R, rpw);
+    const int64_t n_pre_wg = int64_t(tiles.size()) * pre_grid_y;
+    const double bw_cu = (o.decode_gbps_per_cu != 0.0 ? o.decode_gbps_per_cu : kDefaultDecodeGBpsPerCU) * 1e9;
+    const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : kDefaultPrefillTFlopsPerCU) * 1e12;
+    const int64_t chunks = (G + 7) / 8;   // prefill columns per KV head
+    // Per XCD: entries and estimated durations (ns) in each phase's order.
+    std::vector<int32_t> pe[8], de[8];
+    std::vector<int64_t> pd[8], dd[8];
+    for (size_t i = 0; i < tiles.size(); ++i) {
+      const Tile& t = tiles[i];
+      const int64_t rows = t.r1 - t.r0;
+      const int64_t pairs = rows * (t.kend - t.r1) + (int64_t(t.r0) + 1 + t.r1) * rows / 2;
+      for (int32_t c = 0; c < pre_grid_y; ++c) {
+        const int64_t e = int64_t(i) * pre_grid_y + c;
+        const int x = 8 % pre_grid_y == 0 ? int(c + pre_grid_y * (int64_t(i) % (8 / pre_grid_y))) : int(e % 8);
+        const int64_t heads = std::min<int64_t>(8, G - 8 * (c % chunks));
+        const double flops = double(pairs) * double(heads) * double(2 * (sh.head_dim_qk + sh.head_dim_v));
+        pe[x].push_back(int32_t(e));
+        pd[x].push_back(int64_t(flops / fl_cu * 1e9) + 1);
+      }
+    }
+    const int64_t page_bytes = int64_t(P) * sh.num_kv_heads * (sh.head_dim_qk + sh.head_dim_v) * 2;
+    for (int64_t j = 0; j < J; ++j) {
+      const int64_t r0 = rpw * j, r1 = std::min(R, rpw * j + rpw);
+      const double bytes = double(r1 * T / R - r0 * T / R) * double(page_bytes);
+      de[j % 8].push_back(int32_t(n_pre_wg + j));
+      dd[j % 8].push_back(int64_t(bytes / bw_cu * 1e9) + 1);
+    }
+    // Two CU pools per XCD, sized by the plan's CU split (half each when it
+    // has none), each handing its phase's work-groups, in order, to its
+    // earliest-free CU; entries are listed by simulated start time (prefill
+    // first on ties, then phase order).
+    const int64_t cap = std::max<int64_t>(2, cus_total / 8);
+    int64_t cd = cus_decode < cus_total ? cus_decode * cap / cus_total : cap / 2;
+    cd = std::min(cap - 1, std::max<int64_t>(1, cd));
+    struct Ev { int64_t start; int kind; size_t k; };
+    auto simulate = [](const std::vector<int64_t>& dur, int64_t m, int kind, std::vector<Ev>& out) {
+      std::vector<int64_t> free_at(size_t(m), 0);
+      for (size_t k = 0; k < dur.size(); ++k) {
+        size_t best = 0;
+        for (size_t q = 1; q < free_at.size(); ++q)
+          if (free_at[q] < free_at[best]) best = q;
+        out.push_back({free_at[best], kind, k});
+        free_at[best] += dur[k];
+      }
+    };
+    std::vector<int32_t> lists[8];
+    size_t longest = 0;
+    for (int x = 0; x < 8; ++x) {
+      std::vector<Ev> ev;
+      simulate(pd[x], de[x].empty() ? cap : cap - cd, 0, ev);
+      simulate(dd[x], pe[x].empty() ? cap : cd, 1, ev);
+      std::sort(ev.begin(), ev.end(), [](const Ev& a, const Ev& b) {
+        if (a.start != b.start) return a.start < b.start;
+        if (a.kind != b.kind) return a.kind < b.kind;
+        return a.k < b.k;
+      });
+      for (const Ev& v : ev) lists[x].push_back(v.kind == 0 ? pe[x][v.k] : de[x][v.k]);
+      longest = std::max(longest, lists[x].size());
+    }
+    fused.assign(8 * longest, -1);
+    for (int x = 0; x < 8; ++x)
+      for (size_t k = 0; k < lists[x].size(); ++k) fused[8 * k + x] = lists[x][k];
+  }
+
   flex_attn_plan_t* plan = new (std::nothrow) flex_attn_plan_t();
   if (!plan) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
   plan->shape = sh;
@@ -270,7 +341,8 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int32_t off_order = off_ranges + int32_t(ranges.size());
   const int32_t off_merge = off_order + n_dec_items;
   const int32_t off_pre = off_merge + int32_t(merge_list.size());
-  const int32_t total = off_pre + kItemWords * n_pre_items;
+  const int32_t off_fused = off_pre + kItemWords * n_pre_items;
+  const int32_t total = off_fused + int32_t(fused.size());
   auto& w = plan->words;
   w.assign(kHeaderWords, 0);
   w[H_MAGIC] = kPlanMagic;
@@ -293,6 +365,8 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   w[H_OFF_RANGES] = off_ranges;
   w[H_OFF_ORDER] = off_order;
   w[H_OFF_MERGE] = off_merge;
+  w[H_OFF_FUSED] = off_fused;
+  w[H_N_FUSED] = int32_t(fused.size());
   w.insert(w.end(), dec_words.begin(), dec_words.end());
   w.insert(w.end(), ranges.begin(), ranges.end());
   w.insert(w.end(), order.begin(), order.end());
@@ -301,6 +375,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     const int32_t item[kItemWords] = {t.s, t.t, t.r0, t.r1, t.kend, 0, 0, 0};
     w.insert(w.end(), item, item + kItemWords);
   }
+  w.insert(w.end(), fused.begin(), fused.end());
 
   // Workspace: per (decode item, column) the rows' (max, sum) pairs, then the
   // unnormalised partial outputs; needed only when some sequence is split.
@@ -329,6 +404,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   info.workspace_bytes = ws;
   info.decode_bytes = double(dec_bytes);
   info.prefill_flops = double(pre_flops);
+  info.n_fused_wgs = int32_t(fused.size());
   *out_plan = plan;
   return FLEX_OK;
 }

@@ -24,6 +24,7 @@ FLEX_ERR_HIP = -4
 FLEX_ERR_INTERNAL = -5
 FLEX_MODE_SERIAL = 0
 FLEX_MODE_CORUN = 1
+FLEX_MODE_FUSED = 2
 
 EXPORTED = [
     "flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan", "flex_attn_plan_info_get",
@@ -68,7 +69,7 @@ class PlanInfo(ctypes.Structure):
                 ("cus_decode", ctypes.c_int32), ("cus_prefill", ctypes.c_int32), ("bm", ctypes.c_int32),
                 ("plan_words", ctypes.c_int32), ("device_plan_bytes", ctypes.c_size_t),
                 ("workspace_bytes", ctypes.c_size_t), ("decode_bytes", ctypes.c_double),
-                ("prefill_flops", ctypes.c_double)]
+                ("prefill_flops", ctypes.c_double), ("n_fused_wgs", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -57,7 +57,7 @@ def compare(sh, opts, qsl, ls, maxp):
     if st == OP.OK:
         assert words == ref.blob
         for k in ("n_decode_items", "n_prefill_items", "n_split_seqs", "pages_per_split", "cus_decode", "cus_prefill",
-                  "workspace_bytes", "device_plan_bytes", "plan_words", "decode_wg_width"):
+                  "workspace_bytes", "device_plan_bytes", "plan_words", "decode_wg_width", "n_fused_wgs"):
             assert info[k] == ref.info[k], k
         assert info["decode_bytes"] == ref.info["decode_bytes"]
         assert info["prefill_flops"] == ref.info["prefill_flops"]
@@ -81,7 +81,8 @@ def test_plan_matches_rederivation_fuzz():
     shapes = [OP.Shape(28, 4, 128, 128, 16, 128 ** -0.5, 0), OP.Shape(4, 1, 64, 64, 16, 0.125, 0),
               OP.Shape(32, 2, 128, 128, 64, 0.1, 0), OP.Shape(128, 1, 576, 512, 64, 192 ** -0.5, 1),
               OP.Shape(64, 1, 576, 512, 64, 0.07, 1), OP.Shape(16, 16, 192, 128, 64, 192 ** -0.5, 0),
-              OP.Shape(8, 4, 192, 128, 64, 0.1, 0)]
+              OP.Shape(8, 4, 192, 128, 64, 0.1, 0), OP.Shape(40, 5, 64, 64, 16, 0.125, 0),
+              OP.Shape(48, 3, 128, 128, 64, 0.09, 0), OP.Shape(64, 8, 128, 128, 16, 0.088, 0)]
     for trial in range(400):
         sh = rng.choice(shapes)
         P = sh.page_size

@@ -109,7 +109,40 @@ def check_invariants(sh, opts, qsl, ls, maxp):
         assert all(a[1] == b_[0] for a, b_ in zip(rr, rr[1:]))
     kends = [it[4] for it in pre_items]
     assert kends == sorted(kends, reverse=True)
+    check_fused(sh, r, b)
     return r
+
+
+def check_fused(sh, r, b):
+    """The one-launch order: every work-group once, on its XCD, each phase in order."""
+    nd, npf, R, bm, gy = b[3], b[4], b[16], b[14], b[8]
+    off_f, nf = b[20], b[21]
+    assert off_f == b[10] + 8 * npf and off_f + nf == len(b) and r.info["n_fused_wgs"] == nf
+    fused = b[off_f:]
+    G = sh.num_q_heads // sh.num_kv_heads
+    fusable = sh.head_dim_qk != 576 and G > 4 and 3 <= sh.num_kv_heads <= 8 and bm == 32 and nd + npf > 0
+    assert (nf > 0) == fusable and nf % 8 == 0
+    if not nf:
+        return
+    rpw = 2 if sh.num_kv_heads <= 4 else 1
+    n_pre_wg, J = npf * gy, -(-R // rpw)
+    assert sorted(e for e in fused if e >= 0) == list(range(n_pre_wg + J)) and min(fused) >= -1
+    for x in range(8):
+        col = fused[x::8]
+        k = len(col)
+        while k and col[k - 1] == -1:
+            k -= 1
+        col = col[:k]
+        assert -1 not in col                               # padding only at the end
+        for e in col:                                      # work-group b runs on XCD b % 8
+            if e < n_pre_wg and 8 % gy == 0:
+                assert e % gy == x % gy and (e // gy) % (8 // gy) == x // gy
+            elif e >= n_pre_wg:
+                assert (e - n_pre_wg) % 8 == x
+        # each phase keeps its own order (a pool starts its work-groups in order)
+        pre = [e for e in col if e < n_pre_wg]
+        dec = [e for e in col if e >= n_pre_wg]
+        assert pre == sorted(pre) and dec == sorted(dec)
 
 
 def test_fuzz_invariants():
@@ -117,7 +150,7 @@ def test_fuzz_invariants():
     for trial in range(300):
         mla = trial % 3 == 0
         sh = shape(mla=mla) if mla else shape(P=rng.choice([16, 64]), d=rng.choice([64, 128]),
-                                             Hq=rng.choice([4, 28, 32]), Hkv=rng.choice([1, 4]))
+                                             Hq=rng.choice([4, 28, 32, 40, 48]), Hkv=rng.choice([1, 3, 4, 5, 8]))
         if sh.num_q_heads % sh.num_kv_heads or sh.num_q_heads // sh.num_kv_heads > 16:
             continue
         qsl, ls, maxp = random_batch(rng, sh.page_size, rng.randint(0, 40), rng.randint(0, 4))
@@ -158,3 +191,33 @@ def test_unsupported_shapes():
     assert OP.build_plan(OP.Shape(28, 3, 128, 128, 16, 0.1, 0), None, [0, 1], [5], 4).status == OP.ERR_INVALID_ARG
     assert OP.build_plan(OP.Shape(28, 4, 128, 128, 16, -1.0, 0), None, [0, 1], [5], 4).status == OP.ERR_INVALID_ARG
     assert OP.build_plan(OP.Shape(128, 1, 576, 512, 64, 0.1, 0), None, [0, 1], [5], 4).status == OP.ERR_UNSUPPORTED
+
+
+def test_fused_order_worked_example():
+    """A case small enough to schedule by hand.
+
+    16 CUs -> 2 per XCD; no co-run split -> one prefill CU and one decode CU
+    per XCD. Four 32-token prompts (one tile each, 528 causal pairs, kend 32,
+    tiles in batch order) and 48 one-page decode sequences cut into R =
+    16 * 3 = 48 one-page ranges, two per decode work-group (4 KV heads): 24
+    decode work-groups. Durations: prefill 528 pairs * 7 heads * 512 flop at
+    1 TFLOP/s = 1892.352 ns -> 1893; decode 2 pages * 16 slots * 4 heads *
+    256 * 2 B = 65536 B at 80 GB/s = 819.2 ns -> 820. XCD 0 serves tiles 0
+    and 2 (column 0 -> entries 0 and 8) and decode work-groups 0, 8, 16
+    (entries 16, 24, 32): prefill starts 0, 1893; decode starts 0, 820, 1640;
+    by start time: 0 (prefill first), 16, 24, 32, 8.
+    """
+    sh = OP.Shape(28, 4, 128, 128, 16, 0.088, 0)
+    ns = [1] * 48 + [32] * 4
+    ls = [16] * 48 + [32] * 4
+    qsl = [0]
+    for n in ns:
+        qsl.append(qsl[-1] + n)
+    o = OP.Opts(cus_total=16, wg_per_cu=3, min_split_tokens=16, prefill_tflops_per_cu=1.0, decode_gbps_per_cu=80.0)
+    r = OP.build_plan(sh, o, qsl, ls, 2)
+    assert r.status == OP.OK and r.blob[16] == 48
+    b = r.blob
+    fused = b[b[20]:b[20] + b[21]]
+    assert fused[0::8][:5] == [0, 16, 24, 32, 8]
+    # XCD 4 serves tile 1 and 3 column 0 (entries 4, 12) and decode 4, 12, 20 (entries 20, 28, 36)
+    assert fused[4::8][:5] == [4, 20, 28, 36, 12]
