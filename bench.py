@@ -5,7 +5,9 @@ A step is one pass of the whole path over one synthetic batch: the plan
 (built once, outside the timed region, like the paper's off-path policy
 plane), the prefill kernel and the decode kernel with its split merge, run
 either co-located on two CU-masked streams (the default, the paper's dynamic
-co-location analog) or serially. Inputs are resident in HBM before timing;
+co-location analog) or serially; a third leg times the one-launch form, in
+which one grid holds both phases' work-groups (fused_us). Inputs are
+resident in HBM before timing;
 the KV cache is rotated over several copies so the 256 MB Infinity Cache
 cannot serve repeated steps.
 
@@ -170,6 +172,9 @@ def main():
     ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over steps")
     ap.add_argument("--bm", type=int, default=0, help="prefill rows per tile (0: library default)")
     ap.add_argument("--no-serial", action="store_true", help="skip the serial comparison leg")
+    ap.add_argument("--no-fused", action="store_true", help="skip the one-launch (fused) comparison leg")
+    ap.add_argument("--fused-wg-per-cu", type=int, default=2,
+                    help="decode work-groups per CU the fused leg's plan partitions for")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -276,6 +281,24 @@ def main():
         s_ms, _, s_pre, s_dec = timed(F.FLEX_MODE_SERIAL, args.steps, args.warmup)
         log(f"serial step {s_ms * 1e3:.1f} us (prefill {s_pre * 1e3:.1f} us, decode {s_dec * 1e3:.1f} us)")
     corun.close()
+    f_ms = None
+    if not args.no_fused:
+        # fused leg: both phases in one launch, the work-groups interleaved by the plan
+        pa_f = F.PagedAttention(shape, F.make_opts(cus_decode=0, bm=args.bm, wg_per_cu=args.fused_wg_per_cu),
+                                b.query_start_loc.tolist(), b.seq_lens.tolist(), b.block_table.shape[1])
+        if pa_f.plan.info["n_fused_wgs"] > 0:
+            fargs = [pa_f.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+            for i in range(args.warmup):
+                F.flex_attn_mixed(pa_f.plan, fargs[i % len(fargs)], F.FLEX_MODE_FUSED, stream=caller.cuda_stream)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(caller)
+            for i in range(args.steps):
+                F.flex_attn_mixed(pa_f.plan, fargs[i % len(fargs)], F.FLEX_MODE_FUSED, stream=caller.cuda_stream)
+            e1.record(caller)
+            torch.cuda.synchronize()
+            f_ms = e0.elapsed_time(e1) / args.steps
+            log(f"fused step {f_ms * 1e3:.1f} us ({pa_f.plan.info['n_fused_wgs']} work-groups)")
 
     dec_bytes = work["decode"]["bytes"]
     pre_flops = work["prefill"]["flops"]
@@ -310,6 +333,11 @@ def main():
     if s_ms is not None:
         result["serial_us"] = round(s_ms * 1e3, 2)
         result["corun_speedup_vs_serial"] = round(s_ms / c_ms, 4)
+    if f_ms is not None:
+        result["fused_us"] = round(f_ms * 1e3, 2)
+        result["fused_wg_per_cu"] = args.fused_wg_per_cu
+        if s_ms is not None:
+            result["fused_speedup_vs_serial"] = round(s_ms / f_ms, 4)
         result["phases_us"].update({"serial_prefill": round(s_pre * 1e3, 2), "serial_decode": round(s_dec * 1e3, 2)})
         if dec_bytes:
             result["decode_GBps_all_cus"] = round(dec_bytes / (s_dec * 1e-3) / 1e9, 1)

@@ -4,7 +4,7 @@ The paper evaluates dynamic prefill/decode co-location against static
 co-location and disaggregation by end-to-end serving latency (TTFT, TPOT) on
 1K-input/1K-output and 1K-input/4K-output request mixes (Sec. 4.1; Tables 3
 and 4). This tool replays one synthetic request stream per mix through the
-library on one GPU, step by step, under three policies, and reports the
+library on one GPU, step by step, under four policies, and reports the
 step-time distribution and TTFT / TPOT proxies:
 
 * serial      every step runs prefill then decode on all CUs;
@@ -12,7 +12,9 @@ step-time distribution and TTFT / TPOT proxies:
               co-location), otherwise serial;
 * controller  flex_ctl_* picks each step's mode and split from the step's work
               and queue signals, observing every step's phase times (dynamic
-              co-location; Sec. 3.3, Sec. 3.4).
+              co-location; Sec. 3.3, Sec. 3.4);
+* fused       a step with both phases runs as one launch whose work-groups
+              interleave the phases (no CU masks), otherwise serial.
 
 The stream is defined in steps, not in time: requests arrive at given steps,
 are admitted while there is room, and are prefilled in chunks of at most
@@ -193,15 +195,21 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         both = info["n_decode_items"] > 0 and info["n_prefill_items"] > 0
         if policy == "fixed" and both:
             mode, cd = F.FLEX_MODE_CORUN, args.fixed_decode_cus
+        elif policy == "fused" and both:
+            mode = F.FLEX_MODE_FUSED
         elif policy == "controller":
             d = ctl.decide(info["decode_bytes"], info["prefill_flops"], pending_prefill_tokens=max(0, pend_prefill),
                            pending_decode_seqs=len(waiting), active_decode_seqs=n_dec)
             reasons[d["reason"]] = reasons.get(d["reason"], 0) + 1
             if d["mode"] == F.FLEX_MODE_CORUN:
                 mode, cd = F.FLEX_MODE_CORUN, d["cus_decode"]
-        pa = probe if mode == F.FLEX_MODE_SERIAL else F.PagedAttention(shape, F.make_opts(cus_decode=cd), qsl, ls,
-                                                                          max_pages)
-        key = "serial" if mode == F.FLEX_MODE_SERIAL else f"{256 - cd}:{cd}"
+        if mode == F.FLEX_MODE_SERIAL:
+            pa = probe
+        elif mode == F.FLEX_MODE_FUSED:
+            pa = F.PagedAttention(shape, F.make_opts(wg_per_cu=2), qsl, ls, max_pages)
+        else:
+            pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd), qsl, ls, max_pages)
+        key = {F.FLEX_MODE_SERIAL: "serial", F.FLEX_MODE_FUSED: "fused"}.get(mode, f"{256 - cd}:{cd}")
         splits[key] = splits.get(key, 0) + 1
         d_bt = bt.to(dev)
         d_sl = torch.tensor(ls, dtype=torch.int32, device=dev)
@@ -276,7 +284,7 @@ def main():
     ap.add_argument("--mix", default="all", choices=["1k1k", "1k4k", "long", "all"])
     ap.add_argument("--no-per-mix-limits", dest="per_mix_limits", action="store_false",
                     help="use the flags' batch limits for every mix")
-    ap.add_argument("--policies", default="serial,fixed,controller")
+    ap.add_argument("--policies", default="serial,fixed,controller,fused")
     ap.add_argument("--steps", type=int, default=300)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--warm", type=int, default=224, help="requests already decoding at step 0")

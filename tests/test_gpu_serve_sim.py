@@ -1,5 +1,5 @@
 """GPU run of the step-level serving loop (KV append + mixed attention per step,
-three policies). Every policy must see the same batches: the same decode-token
+four policies). Every policy must see the same batches: the same decode-token
 count and the same number of prompts finishing prefill; the controller's
 co-run steps must be valid candidate splits."""
 import argparse
@@ -17,7 +17,7 @@ def test_policies_replay_the_same_stream():
     args = argparse.Namespace(steps=24, seed=3, warm=40, max_active=48, chunk=2048, burst=8, burst_every=10,
                               rate=0.3, fixed_decode_cus=128, per_mix_limits=False)
     res = {}
-    for pol in ("serial", "fixed", "controller"):
+    for pol in ("serial", "fixed", "controller", "fused"):
         log(f"serve loop: mix long, policy {pol}, 24 steps")
         res[pol] = serve_sim.simulate("long", pol, args, profile=None)
     toks = {p: r["tpot_ms"]["tokens"] for p, r in res.items()}
@@ -27,5 +27,6 @@ def test_policies_replay_the_same_stream():
     assert set(res["serial"]["splits"]) == {"serial"}
     for k in res["controller"]["splits"]:
         assert k == "serial" or k in ("192:64", "128:128", "64:192")
+    assert set(res["fused"]["splits"]) <= {"serial", "fused"} and "fused" in res["fused"]["splits"]
     for r in res.values():
         assert r["total_ms"] > 0 and r["step_ms"]["max"] < 50.0
