@@ -179,6 +179,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run plain copies of known size (for scaling memory counters)")
+    ap.add_argument("--fused-pass", action="store_true",
+                    help="issue warmup + steps one-launch (fused) steps untimed and exit (for kernel tracing)")
     ap.add_argument("--counter-pass", action="store_true",
                     help="only issue the co-run plan's phases one after the other, untimed: the launches a "
                          "co-run step makes, for counter collection (which serialises dispatches and so "
@@ -266,6 +268,18 @@ def main():
         torch.cuda.synchronize()
         corun.close()
         print(json.dumps({"counter_pass": True, "steps": args.warmup + args.steps, "cus_decode_plan": cd}), flush=True)
+        return
+
+    if args.fused_pass:
+        pa_f = F.PagedAttention(shape, F.make_opts(cus_decode=0, bm=args.bm, wg_per_cu=args.fused_wg_per_cu),
+                                b.query_start_loc.tolist(), b.seq_lens.tolist(), b.block_table.shape[1])
+        fargs = [pa_f.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+        for i in range(args.warmup + args.steps):
+            F.flex_attn_mixed(pa_f.plan, fargs[i % len(fargs)], F.FLEX_MODE_FUSED, stream=caller.cuda_stream)
+        torch.cuda.synchronize()
+        corun.close()
+        print(json.dumps({"fused_pass": True, "steps": args.warmup + args.steps,
+                          "fused_wgs": pa_f.plan.info["n_fused_wgs"]}), flush=True)
         return
 
     log(f"co-run: {args.warmup} warmup + {args.steps} timed steps")
