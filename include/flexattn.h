@@ -333,10 +333,17 @@ int flex_attn_kv_append(const flex_attn_shape* shape, const flex_attn_append_arg
  * observed decode rate reached sat_frac of hbm_gbps) or a prefill backlog
  * (pending_prefill_tokens >= backlog_prefill_tokens) takes the smallest;
  * otherwise the best prediction. Serial runs when it is predicted fastest or
- * one phase has no work. Every explore_every-th decision tries a neighbouring
- * split instead, so stale estimates are refreshed. Signal (5), utilisation,
- * enters through the observations: a split whose phases finish unevenly
- * leaves CUs idle and shows up as a slower observed rate.
+ * one phase has no work. When the step has a one-launch form (FLEX_MODE_FUSED)
+ * its prediction is the serial prediction times a running ratio of observed
+ * fused to observed serial step times (prior fused_prior; see
+ * flex_ctl_observation); it is chosen
+ * when strictly below both the serial and the best co-run prediction. Every
+ * explore_every-th decision tries a neighbouring split instead of a co-run
+ * choice, and every fourth such turn tries the one-launch form instead of
+ * the choice when it has one and was not chosen, so stale estimates are
+ * refreshed. Signal (5), utilisation, enters through the observations: a
+ * split whose phases finish unevenly leaves CUs idle and shows up as a
+ * slower observed rate.
  * ---------------------------------------------------------------------- */
 typedef struct flex_ctl flex_ctl_t;
 
@@ -355,6 +362,7 @@ typedef struct flex_ctl_opts {
   double corun_overhead_us;     /* fork/join cost added to co-run predictions [10] */
   double decode_gbps_per_cu;    /* prior when no profile is set [60] */
   double prefill_tflops_per_cu; /* prior when no profile is set [5] */
+  double fused_prior;           /* prior of (one-launch step time) / (serial step time) [0.9] */
 } flex_ctl_opts;
 
 /* Signals describing the step about to run and the queues behind it. */
@@ -364,13 +372,23 @@ typedef struct flex_ctl_signals {
   int32_t pending_prefill_tokens; /* (1) prompt tokens still waiting for prefill */
   int32_t pending_decode_seqs;  /* (1)/(4) sequences waiting to decode beyond this step */
   int32_t active_decode_seqs;   /* (4) sequences decoding in this step */
+  int32_t fused_available;      /* the step's plan has a one-launch form (n_fused_wgs > 0) */
 } flex_ctl_signals;
 
-/* What the last step measured (e.g. flex_attn_corun_timing_read). */
+/* What the last step measured (e.g. flex_attn_corun_timing_read). A
+ * one-launch (FUSED) step has no separate phase times: set fused = 1 and
+ * step_ms to its duration (cus_decode, decode_ms and prefill_ms are then
+ * ignored). The controller keeps the ratio of such steps' durations to its
+ * serial prediction for the same work, and the same ratio for serial steps
+ * that report step_ms (0: not reported), and predicts a fused step as the
+ * serial prediction times the first ratio over the second, so that launch
+ * and gap costs outside the phase times weigh on both alike. */
 typedef struct flex_ctl_observation {
   int32_t cus_decode;           /* split it ran with; 0 or cus_total = serial */
   double decode_bytes, prefill_flops;
   double decode_ms, prefill_ms; /* phase durations (0 for a phase with no work) */
+  int32_t fused;                /* 1: the step ran as one launch */
+  double step_ms;               /* its duration (fused steps only) */
 } flex_ctl_observation;
 
 #define FLEX_CTL_ONE_PHASE 0      /* one phase has no work: serial */
@@ -380,9 +398,10 @@ typedef struct flex_ctl_observation {
 #define FLEX_CTL_BW_SATURATED 4   /* bandwidth pressure: smallest decode share in the band */
 #define FLEX_CTL_EXPLORE 5        /* neighbour of the choice, to refresh its estimate */
 #define FLEX_CTL_PREFILL_BACKLOG 6 /* prefill backlog: smallest decode share in the band */
+#define FLEX_CTL_FUSED_FASTER 7   /* the one-launch form predicted fastest */
 
 typedef struct flex_ctl_decision {
-  int32_t mode;                 /* FLEX_MODE_SERIAL or FLEX_MODE_CORUN */
+  int32_t mode;                 /* FLEX_MODE_SERIAL, FLEX_MODE_CORUN or FLEX_MODE_FUSED */
   int32_t cus_decode;           /* co-run: decode CUs (plan opts cus_decode); serial: cus_total */
   int32_t cus_prefill;
   int32_t reason;               /* FLEX_CTL_* */

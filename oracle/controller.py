@@ -28,15 +28,27 @@ library with it exactly:
   else the smallest under bandwidth pressure (last observed decode rate >=
   sat_frac * hbm) or a prefill backlog, else the best; every explore_every-th
   decision moves to a neighbour (+1 on odd multiples, -1 on even ones, the
-  other way at the ends).
+  other way at the ends);
+* one-launch (fused) form, when the step has one: predicted as the serial
+  prediction times fused_ratio / serial_ratio, two running ratios of whole
+  step times to the serial prediction from the current serial estimates
+  (before the observation updates them): fused steps feed fused_ratio (prior
+  fused_prior), serial steps that report their step time feed serial_ratio
+  (prior 1), each first observation replacing the prior; a profile resets
+  both. It is chosen
+  when its prediction is strictly below serial's (if serial beats every
+  co-run split) or the best co-run split's (otherwise). On an explore turn
+  whose index (decisions // explore_every) is 3 mod 4, a step that has the
+  form and did not choose it runs it instead (reason EXPLORE), before any
+  neighbour move; a serial choice makes no neighbour move.
 """
 from __future__ import annotations
 
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence
 
-ONE_PHASE, BEST, SERIAL_FASTER, BACKLOG, BW_SATURATED, EXPLORE, PREFILL_BACKLOG = range(7)
-MODE_SERIAL, MODE_CORUN = 0, 1
+ONE_PHASE, BEST, SERIAL_FASTER, BACKLOG, BW_SATURATED, EXPLORE, PREFILL_BACKLOG, FUSED_FASTER = range(8)
+MODE_SERIAL, MODE_CORUN, MODE_FUSED = 0, 1, 2
 
 
 @dataclass
@@ -53,6 +65,7 @@ class CtlOpts:
     corun_overhead_us: float = 10.0
     decode_gbps_per_cu: float = 60.0
     prefill_tflops_per_cu: float = 5.0
+    fused_prior: float = 0.9
 
 
 OC_DEFAULTS = CtlOpts()
@@ -67,6 +80,10 @@ class Controller:
     n_pre: List[int] = field(default_factory=list)
     last_bw: float = 0.0
     decisions: int = 0
+    fused_ratio: float = 0.0
+    n_fused: int = 0
+    serial_ratio: float = 1.0
+    n_serial_steps: int = 0
 
     @property
     def K(self) -> int:
@@ -94,6 +111,8 @@ class Controller:
             self.pre[k] = cp * self.o.prefill_tflops_per_cu
         self.n_dec = [0] * (K + 1)
         self.n_pre = [0] * (K + 1)
+        self.fused_ratio, self.n_fused = self.o.fused_prior, 0
+        self.serial_ratio, self.n_serial_steps = 1.0, 0
 
     def set_profile(self, cus: Sequence[int], dgbps: Sequence[float], ptflops: Sequence[float]):
         def curve(ys, c):
@@ -111,14 +130,32 @@ class Controller:
         self.n_dec = [0] * (self.K + 1)
         self.n_pre = [0] * (self.K + 1)
         self.last_bw = 0.0
+        self.fused_ratio, self.n_fused = self.o.fused_prior, 0
+        self.serial_ratio, self.n_serial_steps = 1.0, 0
 
     def _blend(self, table, counts, k, value):
         table[k] = value if counts[k] == 0 else (1.0 - self.o.alpha) * table[k] + self.o.alpha * value
         counts[k] += 1
 
+    def serial_prediction_us(self, B: float, F: float) -> float:
+        K = self.K
+        return (B / (self.dec[K] * 1e3) if B > 0 else 0.0) + (F / (self.pre[K] * 1e6) if F > 0 else 0.0)
+
     def observe(self, cus_decode: int, decode_bytes: float, prefill_flops: float,
-                decode_ms: float, prefill_ms: float):
+                decode_ms: float, prefill_ms: float, fused: bool = False, step_ms: float = 0.0):
+        base = self.serial_prediction_us(decode_bytes, prefill_flops)
+        if fused:
+            if step_ms > 0 and base > 0:
+                r = step_ms * 1e3 / base
+                self.fused_ratio = r if self.n_fused == 0 else (1.0 - self.o.alpha) * self.fused_ratio + self.o.alpha * r
+                self.n_fused += 1
+            return
         k = self.K if cus_decode in (0, self.o.cus_total) else cus_decode // self.o.granule
+        if k == self.K and step_ms > 0 and base > 0:
+            r = step_ms * 1e3 / base
+            self.serial_ratio = r if self.n_serial_steps == 0 else \
+                (1.0 - self.o.alpha) * self.serial_ratio + self.o.alpha * r
+            self.n_serial_steps += 1
         if decode_ms > 0 and decode_bytes > 0:
             r = decode_bytes / (decode_ms * 1e-3) / 1e9
             self._blend(self.dec, self.n_dec, k, r)
@@ -127,7 +164,7 @@ class Controller:
             self._blend(self.pre, self.n_pre, k, prefill_flops / (prefill_ms * 1e-3) / 1e12)
 
     def decide(self, decode_bytes: float, prefill_flops: float, pending_prefill_tokens: int = 0,
-               pending_decode_seqs: int = 0, active_decode_seqs: int = 1) -> dict:
+               pending_decode_seqs: int = 0, active_decode_seqs: int = 1, fused_available: bool = False) -> dict:
         o, K = self.o, self.K
         self.decisions += 1
         B, F = decode_bytes, prefill_flops
@@ -152,7 +189,19 @@ class Controller:
         for k in range(2, K + 1):
             if pred[k] < pred[best]:
                 best = k
+        t_fused = self.fused_ratio / self.serial_ratio * pred[K] if fused_available else None
+        explore = o.explore_every > 0 and self.decisions % o.explore_every == 0
+        explore_fused = explore and fused_available and (self.decisions // o.explore_every) % 4 == 3
+
+        def fused(reason):
+            return dict(mode=MODE_FUSED, cus_decode=o.cus_total, cus_prefill=o.cus_total, reason=reason,
+                        predicted_us=t_fused)
+
         if best == K:
+            if t_fused is not None and t_fused < pred[K]:
+                return fused(FUSED_FASTER)
+            if explore_fused:
+                return fused(EXPLORE)
             return serial(SERIAL_FASTER)
         band = [k for k in range(1, K) if pred[k] <= pred[best] * (1.0 + o.tolerance)]
         choice, reason = best, BEST
@@ -162,7 +211,12 @@ class Controller:
             choice, reason = min(band), BW_SATURATED
         elif pending_prefill_tokens >= o.backlog_prefill_tokens:
             choice, reason = min(band), PREFILL_BACKLOG
-        if o.explore_every > 0 and self.decisions % o.explore_every == 0:
+        fused_wins = t_fused is not None and t_fused < pred[best]
+        if explore_fused and not fused_wins:
+            return fused(EXPLORE)
+        if fused_wins:
+            return fused(FUSED_FASTER)
+        if explore:
             step = 1 if (self.decisions // o.explore_every) % 2 else -1
             k = choice + step
             if not 1 <= k < K:

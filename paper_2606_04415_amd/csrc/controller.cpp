@@ -5,9 +5,10 @@
 //
 // State: for every candidate co-run split k (decode on k * granule CUs,
 // prefill on the rest) the decode rate (GB/s) and prefill rate (TFLOP/s)
-// observed in that split, and the two rates of serial execution. Estimates
-// start from a prior and move by exponential weighting toward each observed
-// step; the first observation of an entry replaces its prior.
+// observed in that split, the two rates of serial execution, and the ratio
+// of one-launch (fused) step times to the serial prediction. Estimates start
+// from a prior and move by exponential weighting toward each observed step;
+// the first observation of an entry replaces its prior.
 #include <algorithm>
 #include <cmath>
 #include <new>
@@ -20,6 +21,10 @@ struct flex_ctl {
   int32_t K;                     // cus_total / granule; index K = serial
   std::vector<double> dec, pre;  // [K + 1], index 0 unused
   std::vector<int64_t> n_dec, n_pre;
+  double fused_ratio = 0.0;      // fused step time / serial prediction
+  int64_t n_fused = 0;
+  double serial_ratio = 1.0;     // serial step time / serial prediction
+  int64_t n_serial_steps = 0;
   double last_decode_gbps = 0.0;
   int64_t decisions = 0;
 };
@@ -44,6 +49,10 @@ double interp(const std::vector<int32_t>& x, const std::vector<double>& y, doubl
 void reset_counts(flex_ctl* c) {
   std::fill(c->n_dec.begin(), c->n_dec.end(), 0);
   std::fill(c->n_pre.begin(), c->n_pre.end(), 0);
+  c->fused_ratio = c->o.fused_prior;
+  c->n_fused = 0;
+  c->serial_ratio = 1.0;
+  c->n_serial_steps = 0;
   c->last_decode_gbps = 0.0;
 }
 
@@ -83,11 +92,13 @@ extern "C" int flex_ctl_create(const flex_ctl_opts* opts, flex_ctl_t** out) {
   if (o.corun_overhead_us == 0.0) o.corun_overhead_us = 10.0;
   if (o.decode_gbps_per_cu == 0.0) o.decode_gbps_per_cu = 60.0;
   if (o.prefill_tflops_per_cu == 0.0) o.prefill_tflops_per_cu = 5.0;
+  if (o.fused_prior == 0.0) o.fused_prior = 0.9;
   if (o.cus_total < 2 || o.granule < 1 || o.cus_total % o.granule || o.cus_total / o.granule < 2)
     return set_error(FLEX_ERR_INVALID_ARG, "granule must divide cus_total into at least two parts");
   if (!(o.alpha > 0.0 && o.alpha <= 1.0) || !(o.tolerance >= 0.0) || !(o.sat_frac > 0.0) ||
       !(o.hbm_gbps > 0.0) || !(o.corun_overhead_us >= 0.0) || !(o.decode_gbps_per_cu > 0.0) ||
-      !(o.prefill_tflops_per_cu > 0.0) || o.backlog_seqs < 0 || o.backlog_prefill_tokens < 0)
+      !(o.prefill_tflops_per_cu > 0.0) || !(o.fused_prior > 0.0) || o.backlog_seqs < 0 ||
+      o.backlog_prefill_tokens < 0)
     return set_error(FLEX_ERR_INVALID_ARG, "controller options out of range");
   flex_ctl* c = new (std::nothrow) flex_ctl();
   if (!c) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
@@ -127,6 +138,13 @@ extern "C" int flex_ctl_set_profile(flex_ctl_t* c, int32_t n, const int32_t* cus
 extern "C" int flex_ctl_observe(flex_ctl_t* c, const flex_ctl_observation* ob) {
   flexattn::clear_error();
   if (!c || !ob) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  // the serial prediction for the same work, from the current estimates (us)
+  const double pred = (ob->decode_bytes > 0.0 ? ob->decode_bytes / (c->dec[c->K] * 1e3) : 0.0) +
+                      (ob->prefill_flops > 0.0 ? ob->prefill_flops / (c->pre[c->K] * 1e6) : 0.0);
+  if (ob->fused) {
+    if (ob->step_ms > 0.0 && pred > 0.0) ewma(c->fused_ratio, c->n_fused, ob->step_ms * 1e3 / pred, c->o.alpha);
+    return FLEX_OK;
+  }
   int32_t k;
   if (ob->cus_decode == 0 || ob->cus_decode == c->o.cus_total) {
     k = c->K;
@@ -135,6 +153,8 @@ extern "C" int flex_ctl_observe(flex_ctl_t* c, const flex_ctl_observation* ob) {
       return set_error(FLEX_ERR_INVALID_ARG, "cus_decode is not a candidate split");
     k = ob->cus_decode / c->o.granule;
   }
+  if (k == c->K && ob->step_ms > 0.0 && pred > 0.0)
+    ewma(c->serial_ratio, c->n_serial_steps, ob->step_ms * 1e3 / pred, c->o.alpha);
   if (ob->decode_ms > 0.0 && ob->decode_bytes > 0.0) {
     const double r = ob->decode_bytes / (ob->decode_ms * 1e-3) / 1e9;
     ewma(c->dec[k], c->n_dec[k], r, c->o.alpha);
@@ -173,7 +193,25 @@ extern "C" int flex_ctl_decide(flex_ctl_t* c, const flex_ctl_signals* sg, flex_c
     T[k] = k < K ? std::max(t_dec(k), t_pre(k)) + o.corun_overhead_us : t_dec(k) + t_pre(k);
     if (T[k] < T[best]) best = k;
   }
-  if (best == K) return serial(FLEX_CTL_SERIAL_FASTER);
+  // One-launch form: the serial prediction times the ratio of observed fused
+  // to observed serial step times (both against the serial prediction).
+  const bool has_fused = sg->fused_available != 0;
+  const double Tf = has_fused ? c->fused_ratio / c->serial_ratio * T[K] : 0.0;
+  const bool explore_turn = o.explore_every > 0 && c->decisions % o.explore_every == 0;
+  const bool fused_turn = explore_turn && has_fused && (c->decisions / o.explore_every) % 4 == 3;
+  auto fused = [&](int32_t reason) {
+    out->mode = FLEX_MODE_FUSED;
+    out->cus_decode = o.cus_total;
+    out->cus_prefill = o.cus_total;
+    out->reason = reason;
+    out->predicted_us = Tf;
+    return FLEX_OK;
+  };
+  if (best == K) {
+    if (has_fused && Tf < T[K]) return fused(FLEX_CTL_FUSED_FASTER);
+    if (fused_turn) return fused(FLEX_CTL_EXPLORE);
+    return serial(FLEX_CTL_SERIAL_FASTER);
+  }
 
   int32_t lo = best, hi = best;   // co-run splits within the band
   for (int32_t k = 1; k < K; ++k) {
@@ -193,7 +231,10 @@ extern "C" int flex_ctl_decide(flex_ctl_t* c, const flex_ctl_signals* sg, flex_c
     choice = lo;
     reason = FLEX_CTL_PREFILL_BACKLOG;
   }
-  if (o.explore_every > 0 && c->decisions % o.explore_every == 0) {
+  const bool fused_best = has_fused && Tf < T[best];
+  if (fused_turn && !fused_best) return fused(FLEX_CTL_EXPLORE);
+  if (fused_best) return fused(FLEX_CTL_FUSED_FASTER);
+  if (explore_turn) {
     const int32_t step = (c->decisions / o.explore_every) % 2 ? 1 : -1;
     int32_t k = choice + step;
     if (k < 1 || k >= K) k = choice - step;

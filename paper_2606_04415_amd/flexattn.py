@@ -42,6 +42,7 @@ FLEX_CTL_BACKLOG = 3
 FLEX_CTL_BW_SATURATED = 4
 FLEX_CTL_EXPLORE = 5
 FLEX_CTL_PREFILL_BACKLOG = 6
+FLEX_CTL_FUSED_FASTER = 7
 FLEX_TIMING_RING = 1024
 
 
@@ -97,18 +98,20 @@ class CtlOpts(ctypes.Structure):
                 ("backlog_seqs", ctypes.c_int32), ("backlog_prefill_tokens", ctypes.c_int32),
                 ("alpha", ctypes.c_double), ("tolerance", ctypes.c_double), ("sat_frac", ctypes.c_double),
                 ("hbm_gbps", ctypes.c_double), ("corun_overhead_us", ctypes.c_double),
-                ("decode_gbps_per_cu", ctypes.c_double), ("prefill_tflops_per_cu", ctypes.c_double)]
+                ("decode_gbps_per_cu", ctypes.c_double), ("prefill_tflops_per_cu", ctypes.c_double),
+                ("fused_prior", ctypes.c_double)]
 
 
 class CtlSignals(ctypes.Structure):
     _fields_ = [("decode_bytes", ctypes.c_double), ("prefill_flops", ctypes.c_double),
                 ("pending_prefill_tokens", ctypes.c_int32), ("pending_decode_seqs", ctypes.c_int32),
-                ("active_decode_seqs", ctypes.c_int32)]
+                ("active_decode_seqs", ctypes.c_int32), ("fused_available", ctypes.c_int32)]
 
 
 class CtlObservation(ctypes.Structure):
     _fields_ = [("cus_decode", ctypes.c_int32), ("decode_bytes", ctypes.c_double),
-                ("prefill_flops", ctypes.c_double), ("decode_ms", ctypes.c_double), ("prefill_ms", ctypes.c_double)]
+                ("prefill_flops", ctypes.c_double), ("decode_ms", ctypes.c_double), ("prefill_ms", ctypes.c_double),
+                ("fused", ctypes.c_int32), ("step_ms", ctypes.c_double)]
 
 
 class CtlDecision(ctypes.Structure):
@@ -389,13 +392,14 @@ class Controller:
                                          (ctypes.c_double * n)(*decode_gbps), (ctypes.c_double * n)(*prefill_tflops)),
               "flex_ctl_set_profile")
 
-    def observe(self, cus_decode, decode_bytes, prefill_flops, decode_ms, prefill_ms):
-        ob = CtlObservation(cus_decode, decode_bytes, prefill_flops, decode_ms, prefill_ms)
+    def observe(self, cus_decode, decode_bytes, prefill_flops, decode_ms, prefill_ms, fused=False, step_ms=0.0):
+        ob = CtlObservation(cus_decode, decode_bytes, prefill_flops, decode_ms, prefill_ms, 1 if fused else 0, step_ms)
         check(lib().flex_ctl_observe(self.handle, ctypes.byref(ob)), "flex_ctl_observe")
 
     def decide(self, decode_bytes, prefill_flops, pending_prefill_tokens=0, pending_decode_seqs=0,
-               active_decode_seqs=1) -> dict:
-        sg = CtlSignals(decode_bytes, prefill_flops, pending_prefill_tokens, pending_decode_seqs, active_decode_seqs)
+               active_decode_seqs=1, fused_available=False) -> dict:
+        sg = CtlSignals(decode_bytes, prefill_flops, pending_prefill_tokens, pending_decode_seqs, active_decode_seqs,
+                        1 if fused_available else 0)
         d = CtlDecision()
         check(lib().flex_ctl_decide(self.handle, ctypes.byref(sg), ctypes.byref(d)), "flex_ctl_decide")
         return {"mode": d.mode, "cus_decode": d.cus_decode, "cus_prefill": d.cus_prefill, "reason": d.reason,

@@ -10,9 +10,10 @@ step-time distribution and TTFT / TPOT proxies:
 * serial      every step runs prefill then decode on all CUs;
 * fixed       a step with both phases co-runs on a fixed CU split (static
               co-location), otherwise serial;
-* controller  flex_ctl_* picks each step's mode and split from the step's work
-              and queue signals, observing every step's phase times (dynamic
-              co-location; Sec. 3.3, Sec. 3.4);
+* controller  flex_ctl_* picks each step's mode (serial, a co-run split, or
+              the one-launch form) from the step's work and queue signals,
+              observing every step's phase times (dynamic co-location;
+              Sec. 3.3, Sec. 3.4);
 * fused       a step with both phases runs as one launch whose work-groups
               interleave the phases (no CU masks), otherwise serial.
 
@@ -21,8 +22,10 @@ are admitted while there is room, and are prefilled in chunks of at most
 `chunk` tokens per step (oldest first) before they decode one token per step.
 So every policy runs exactly the same sequence of batches; only the time
 each step takes differs. A step is the KV append of its new tokens plus the
-attention of the mixed batch (GPU time, HIP events on the issuing stream);
-plan building and upload are host work outside it. Request time stamps use
+attention of the mixed batch (GPU time, HIP events on the issuing stream,
+with no per-phase events inside: the controller's phase times come from an
+untimed repeat of the step's attention); plan building and upload are host
+work outside it. Request time stamps use
 the running sum of step times: TTFT = end of the step that finishes a
 request's prompt minus the time it arrived; TPOT = the time of the step that
 produced each decode token, over all decode tokens of the run (every decoding
@@ -119,8 +122,6 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
     shape = F.make_shape(HQ, HKV, D, D, P, 1.0 / math.sqrt(D), False)
     caller = torch.cuda.Stream()
     coruns = {cd: F.Corun(256 - cd, cd) for cd in (64, 128, 192)}
-    for c in coruns.values():
-        c.set_timing(True)
     serial_timer = coruns[128]
     ctl = None
     if policy == "controller":
@@ -142,6 +143,7 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
     reasons: Dict[int, int] = {}
     done: List[Req] = []
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e_mid = torch.cuda.Event(enable_timing=True)   # after the append: the attention alone follows
 
     for step in range(args.steps):
         while nxt < len(reqs) and reqs[nxt].arrival_step <= step:
@@ -199,10 +201,13 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
             mode = F.FLEX_MODE_FUSED
         elif policy == "controller":
             d = ctl.decide(info["decode_bytes"], info["prefill_flops"], pending_prefill_tokens=max(0, pend_prefill),
-                           pending_decode_seqs=len(waiting), active_decode_seqs=n_dec)
+                           pending_decode_seqs=len(waiting), active_decode_seqs=n_dec,
+                           fused_available=getattr(args, "controller_fused", True) and info["n_fused_wgs"] > 0)
             reasons[d["reason"]] = reasons.get(d["reason"], 0) + 1
             if d["mode"] == F.FLEX_MODE_CORUN:
                 mode, cd = F.FLEX_MODE_CORUN, d["cus_decode"]
+            elif d["mode"] == F.FLEX_MODE_FUSED:
+                mode = F.FLEX_MODE_FUSED
         if mode == F.FLEX_MODE_SERIAL:
             pa = probe
         elif mode == F.FLEX_MODE_FUSED:
@@ -220,17 +225,27 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         app = F.make_append_args(kn_pool[:T], vn_pool[:T], d_slots, k_cache, v_cache)
         corun = coruns[cd] if mode == F.FLEX_MODE_CORUN else serial_timer
         torch.cuda.synchronize()
+        # the step, timed with no phase events (recording them adds ~10 us)
         e0.record(caller)
         F.flex_attn_kv_append(shape, app, stream=caller.cuda_stream)
+        e_mid.record(caller)
         F.flex_attn_mixed(pa.plan, args_, mode, stream=caller.cuda_stream, corun=corun)
         e1.record(caller)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1)
-        pre_ms, dec_ms = corun.timing_read()
-        corun.set_timing(True)
-        if ctl is not None:
+        attn_ms = e_mid.elapsed_time(e1)
+        if ctl is not None and mode == F.FLEX_MODE_FUSED:
+            ctl.observe(0, info["decode_bytes"], info["prefill_flops"], 0.0, 0.0, fused=True, step_ms=attn_ms)
+        elif ctl is not None:
+            # the controller's phase times: the same attention once more, untimed,
+            # with phase events (it recomputes the same outputs)
+            corun.set_timing(True)
+            F.flex_attn_mixed(pa.plan, args_, mode, stream=caller.cuda_stream, corun=corun)
+            pre_ms, dec_ms = corun.timing_read()
+            corun.set_timing(False)
             ctl.observe(cd if mode == F.FLEX_MODE_CORUN else 0, info["decode_bytes"], info["prefill_flops"],
-                        dec_ms[-1] if dec_ms else 0.0, pre_ms[-1] if pre_ms else 0.0)
+                        dec_ms[-1] if dec_ms else 0.0, pre_ms[-1] if pre_ms else 0.0,
+                        step_ms=attn_ms if mode == F.FLEX_MODE_SERIAL else 0.0)
         clock += ms
         step_ms.append(ms)
         tok_ms.extend([ms] * sum(1 for r, n in members if n == 1 and r.prefilled == r.prompt))
@@ -295,6 +310,8 @@ def main():
     ap.add_argument("--rate", type=float, default=0.2, help="Poisson arrivals per step")
     ap.add_argument("--fixed-decode-cus", type=int, default=128)
     ap.add_argument("--no-profile", action="store_true", help="controller starts from its prior only")
+    ap.add_argument("--no-controller-fused", dest="controller_fused", action="store_false",
+                    help="the controller chooses between serial and co-run only")
     args = ap.parse_args()
     profile = None if args.no_profile else measure_profile()
     if profile:

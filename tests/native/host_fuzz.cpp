@@ -67,11 +67,12 @@ int main(int argc, char** argv) {
     }
     for (int s = 0; s < 200; ++s) {
       flex_ctl_signals sg{double(pick(0, 3000)) * 1e6, double(pick(0, 3000)) * 1e9, pick(0, 20000), pick(0, 500),
-                          pick(0, 300)};
+                          pick(0, 300), pick(0, 1)};
       flex_ctl_decision d;
       if (flex_ctl_decide(ctl, &sg, &d) != FLEX_OK) return 6;
       flex_ctl_observation ob{d.mode == FLEX_MODE_CORUN ? d.cus_decode : 0, sg.decode_bytes, sg.prefill_flops,
-                              pick(0, 1000) * 1e-3, pick(0, 5000) * 1e-3};
+                              pick(0, 1000) * 1e-3, pick(0, 5000) * 1e-3,
+                              d.mode == FLEX_MODE_FUSED ? 1 : 0, pick(0, 5000) * 1e-3};
       if (flex_ctl_observe(ctl, &ob) != FLEX_OK) return 7;
     }
     double dg[64], pt[64];

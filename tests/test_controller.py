@@ -2,11 +2,12 @@
 
 Parity: every decision of the library's controller equals the re-derivation
 in oracle/controller.py on long random observe/decide sequences (exact float
-equality of the predicted time). Pins, independent of both: the rule's
-directions from the paper (Sec. 3.4: bandwidth saturation cedes CUs to
-prefill, decode backlog takes more), monotonicity in the step's work, the
-argmin on a profile whose optimum is known in closed form, convergence of the
-estimates, the exploration pattern, and one planted mistake.
+equality of the predicted time), one-launch steps included. Pins, independent
+of both: the rule's directions from the paper (Sec. 3.4: bandwidth saturation
+cedes CUs to prefill, decode backlog takes more), monotonicity in the step's
+work, the argmin on a profile whose optimum is known in closed form,
+convergence of the estimates, the exploration pattern, the one-launch form's
+ratio rule in closed form, and one planted mistake.
 """
 import random
 
@@ -37,19 +38,26 @@ def test_decisions_match_the_re_derivation(seed):
         lib.set_profile(*prof)
         ref.set_profile(*prof)
     K = 256 // opts["granule"]
+    modes = set()
     for step in range(400):
         B = rng.choice([0.0, rng.uniform(1e8, 3e9)])
         Fl = rng.choice([0.0, rng.uniform(1e10, 3e12)])
         sig = dict(pending_prefill_tokens=rng.randrange(0, 20000), pending_decode_seqs=rng.randrange(0, 400),
-                   active_decode_seqs=rng.randrange(0, 300))
+                   active_decode_seqs=rng.randrange(0, 300), fused_available=rng.random() < 0.7)
         a = lib.decide(B, Fl, **sig)
         b = ref.decide(B, Fl, **sig)
         same(a, b)
-        cd = a["cus_decode"] if a["mode"] == F.FLEX_MODE_CORUN else rng.choice([0, 256])
-        obs = (cd, B, Fl, rng.uniform(0.05, 3.0) if B else 0.0, rng.uniform(0.05, 9.0) if Fl else 0.0)
+        modes.add(a["mode"])
+        if a["mode"] == F.FLEX_MODE_FUSED:
+            obs = (256, B, Fl, 0.0, 0.0, True, rng.uniform(0.05, 6.0))
+        else:
+            cd = a["cus_decode"] if a["mode"] == F.FLEX_MODE_CORUN else rng.choice([0, 256])
+            obs = (cd, B, Fl, rng.uniform(0.05, 3.0) if B else 0.0, rng.uniform(0.05, 9.0) if Fl else 0.0,
+                   False, rng.choice([0.0, rng.uniform(0.05, 6.0)]))
         lib.observe(*obs)
         ref.observe(*obs)
     assert lib.estimates() == ref.estimates()
+    assert F.FLEX_MODE_FUSED in modes
 
 
 def profile_linear(ctl, bw_per_cu, sat_gbps, tf_per_cu):
@@ -179,3 +187,60 @@ def test_invalid_options_rejected():
         ctl.observe(100, 1e9, 1e11, 0.1, 0.1)   # not a candidate split
     with pytest.raises(F.FlexAttnError):
         ctl.set_profile([64, 32], [1.0, 2.0], [1.0, 2.0])
+
+
+def test_fused_form_follows_its_observed_ratio():
+    # serial beats every split on this profile (no co-run gain): the one-launch
+    # form is chosen while its ratio to the serial prediction is below 1
+    ctl = F.Controller(granule=64, explore_every=4, tolerance=1e-12, corun_overhead_us=1000.0, fused_prior=0.8)
+    profile_linear(ctl, 40.0, 5120.0, 4.0)
+    B, Fl = 1.0e9, 1.5e11
+    d1 = ctl.decide(B, Fl, active_decode_seqs=8, fused_available=True)
+    serial_us = B / 5120e9 * 1e6 + Fl / 1024e12 * 1e6                 # 195.3 + 146.5 us
+    assert d1["mode"] == F.FLEX_MODE_FUSED and d1["reason"] == F.FLEX_CTL_FUSED_FASTER
+    assert abs(d1["predicted_us"] - 0.8 * serial_us) < 1e-9
+    # without a one-launch form the same step runs serial
+    d2 = ctl.decide(B, Fl, active_decode_seqs=8)
+    assert d2["mode"] == F.FLEX_MODE_SERIAL and d2["reason"] == F.FLEX_CTL_SERIAL_FASTER
+    # a fused step observed at 1.25 x the serial prediction: the first
+    # observation replaces the prior, so serial wins from now on ...
+    ctl.observe(256, B, Fl, 0.0, 0.0, fused=True, step_ms=1.25 * serial_us * 1e-3)
+    # ... except on the explore turn that tries the form (decision 12: 12 // 4 = 3 mod 4)
+    picks = [ctl.decide(B, Fl, active_decode_seqs=8, fused_available=True) for _ in range(14)]   # decisions 3..16
+    turns = {i: d for i, d in enumerate(picks, start=3)}
+    assert turns[12]["mode"] == F.FLEX_MODE_FUSED and turns[12]["reason"] == F.FLEX_CTL_EXPLORE
+    assert abs(turns[12]["predicted_us"] - 1.25 * serial_us) < 1e-6
+    for i, d in turns.items():
+        if i != 12:
+            assert d["mode"] == F.FLEX_MODE_SERIAL, (i, d)
+
+
+def test_fused_must_beat_the_best_split():
+    # co-run predicted 293 us, serial 341 us (saturating decode profile);
+    # ratio 0.9 -> 307 us: the split stays; ratio 0.8 -> 273 us: fused
+    def ctl(prior):
+        c = F.Controller(granule=64, explore_every=-1, tolerance=1e-12, corun_overhead_us=1e-9, fused_prior=prior)
+        profile_linear(c, 40.0, 5120.0, 4.0)
+        return c
+    B, Fl = 1.0e9, 1.5e11
+    d = ctl(0.9).decide(B, Fl, active_decode_seqs=8, fused_available=True)
+    assert d["mode"] == F.FLEX_MODE_CORUN and d["cus_decode"] == 128
+    d = ctl(0.8).decide(B, Fl, active_decode_seqs=8, fused_available=True)
+    assert d["mode"] == F.FLEX_MODE_FUSED and d["reason"] == F.FLEX_CTL_FUSED_FASTER
+
+
+def test_fused_ratio_is_relative_to_observed_serial_steps():
+    # launch gaps outside the phase times: a serial step observed at 1.5 x its
+    # prediction and a fused step at 1.2 x make the fused form 0.8 x serial
+    ctl = F.Controller(granule=64, explore_every=-1, tolerance=1e-12, corun_overhead_us=1000.0, fused_prior=2.0)
+    profile_linear(ctl, 40.0, 5120.0, 4.0)
+    B, Fl = 1.0e9, 1.5e11
+    serial_us = B / 5120e9 * 1e6 + Fl / 1024e12 * 1e6
+    assert ctl.decide(B, Fl, active_decode_seqs=8, fused_available=True)["mode"] == F.FLEX_MODE_SERIAL
+    ctl.observe(0, B, Fl, 0.0, 0.0, step_ms=1.5 * serial_us * 1e-3)            # step time only
+    ctl.observe(0, B, Fl, 0.0, 0.0, fused=True, step_ms=1.2 * serial_us * 1e-3)
+    d = ctl.decide(B, Fl, active_decode_seqs=8, fused_available=True)
+    assert d["mode"] == F.FLEX_MODE_FUSED and d["reason"] == F.FLEX_CTL_FUSED_FASTER
+    assert abs(d["predicted_us"] - 0.8 * serial_us) < 1e-9
+    # step-time-only observations leave the phase-rate estimates alone
+    assert abs(ctl.decide(B, Fl, active_decode_seqs=8)["predicted_us"] - serial_us) < 1e-9
