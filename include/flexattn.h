@@ -215,11 +215,13 @@ int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, 
  * paper's dynamic co-location (Sec. 3.4). FLEX_MODE_FUSED runs both phases
  * in one launch on stream (then the split-K merge): each work-group of the
  * launch serves one prefill work-group's tile and column or one or two
- * decode ranges, in the plan's fused order, which interleaves the phases so
- * they progress together; the device's dispatcher hands work-groups to
- * compute units as they free up, so the phases share the device without CU
- * masks (the alternative to two streams; an analog of the paper's temporal
- * sharing, Sec. 3.4). FUSED needs a plan with n_fused_wgs > 0: grouped-query
+ * decode ranges, in the plan's fused order (the phases interleaved by a
+ * simulated dispatch onto a prefill and a decode share of each XCD); the
+ * device's dispatcher hands work-groups to compute units as they free up, so
+ * the phases share the device without CU masks (the alternative to two
+ * streams; an analog of the dispatch-controlled sharing the paper relies on
+ * where the device offers no spatial partitioning, Sec. 3 and Sec. 3.4).
+ * FUSED needs a plan with n_fused_wgs > 0: grouped-query
  * heads with G = Hq / Hkv > 4, 3 <= Hkv <= 8 and 32-row tiles; otherwise it
  * returns FLEX_ERR_UNSUPPORTED. Outputs are bit-identical between the three
  * modes for the same plan. corun is ignored by FUSED. For SERIAL, corun may
@@ -388,7 +390,8 @@ typedef struct flex_ctl_observation {
   double decode_bytes, prefill_flops;
   double decode_ms, prefill_ms; /* phase durations (0 for a phase with no work) */
   int32_t fused;                /* 1: the step ran as one launch */
-  double step_ms;               /* its duration (fused steps only) */
+  double step_ms;               /* the step's duration: required for fused steps, optional
+                                   for serial ones (0 = not reported) */
 } flex_ctl_observation;
 
 #define FLEX_CTL_ONE_PHASE 0      /* one phase has no work: serial */
