@@ -172,6 +172,17 @@ def test_run_calls_reject_bad_args_without_gpu():
     assert F.lib().flex_attn_decode(plan.handle, ctypes.byref(a), None) == F.FLEX_ERR_WORKSPACE
     assert F.lib().flex_attn_workspace_init(ctypes.c_void_p(0x3001), 64, None) == F.FLEX_ERR_INVALID_ARG
     assert F.lib().flex_attn_corun_create(100, 50, ctypes.byref(ctypes.c_void_p())) != F.FLEX_OK
+    # the one-launch mode: checked like the others, and refused (before any launch)
+    # for a plan whose shape has no one-launch form
+    assert F.lib().flex_attn_mixed(plan.handle, ctypes.byref(F.Args()), F.FLEX_MODE_FUSED, None, None) == \
+        F.FLEX_ERR_INVALID_ARG
+    narrow = F.flex_attn_plan(F.make_shape(16, 4, 128, 128, 16, 0.088), None, [0, 1, 3], [40, 50], 4)
+    assert narrow.info["n_fused_wgs"] == 0 and plan.info["n_fused_wgs"] > 0
+    a.workspace_bytes = 1 << 20
+    a.d_plan_bytes = narrow.info["device_plan_bytes"]
+    assert F.lib().flex_attn_mixed(narrow.handle, ctypes.byref(a), F.FLEX_MODE_FUSED, None, None) == \
+        F.FLEX_ERR_UNSUPPORTED
+    assert "one-launch" in F.last_error()
 
 
 def test_status_strings():
