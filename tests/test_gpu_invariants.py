@@ -4,7 +4,10 @@ V2: equal scores (q = 0) give the mean of the visible value rows and
     lse = ln(visible keys).
 V8: changing keys and values after a row's causal limit leaves that row
     bit-identical (a masked key must contribute exactly nothing).
-Both through the C ABI on ragged grouped-query and latent batches, so the
+V3: constant value rows give that constant, whatever the weights.
+V7: the decode kernel at position t agrees with the prefill kernel's row t;
+V6: a chunk over cached keys agrees with the same rows of a one-shot prompt.
+All through the C ABI on ragged grouped-query and latent batches, so the
 decode kernel, the split merge and the prefill kernels are all exercised.
 """
 import numpy as np
@@ -80,3 +83,55 @@ def test_future_keys_do_not_matter(base):
     assert torch.equal(o1[other].view(torch.int16), o2[other].view(torch.int16))
     # and later rows of the chunk do change
     assert not torch.equal(o1[q0 + 60], o2[q0 + 60])
+
+
+def close(a, b, what):
+    a, b = a.double().numpy(), b.double().numpy()
+    err = np.abs(a - b)
+    assert (err <= ATOL_REL * np.maximum(1.0, np.abs(b))).all() and err.mean() <= MEAN_TOL, what
+
+
+@pytest.mark.parametrize("base", ["decode", "mla"])
+def test_constant_values_give_that_constant(base):
+    # V3: every visible value row equal to c (per KV head) -> out = c whatever the weights
+    w = WORKLOADS[base]
+    ns, ls = ([1, 1, 70, 1], [700, 9, 300, 2100]) if base == "decode" else ([1, 70, 1], [300, 200, 1500])
+    b = custom_batch(w, ns, ls, seed=13)
+    c = torch.linspace(-2.0, 2.0, w.num_kv_heads * w.head_dim_v).view(w.num_kv_heads, w.head_dim_v)
+    c = c.to(torch.bfloat16)
+    if w.v_aliases_k:
+        b.k_cache[..., :w.head_dim_v] = c          # V is the first 512 columns of the key row
+    else:
+        b.v_cache[...] = c
+    log(f"V3 on device: {base}, constant value rows")
+    out, _, _ = run(b)
+    G = w.num_q_heads // w.num_kv_heads
+    ref = c.double().repeat_interleave(G, 0)         # [Hq, d_v]
+    for r in range(out.shape[0]):
+        close(out[r], ref, f"row {r}")
+
+
+def test_decode_row_equals_prefill_row():
+    # V7: the decode kernel at position t and the prefill kernel's row t agree;
+    # V6: a chunk on top of cached keys equals the same rows of a one-shot prompt
+    w = QW
+    ns, ls = [300, 1, 1, 32, 64], [300, 1, 1, 64, 64]
+    b = custom_batch(w, ns, ls, seed=14)
+    P = w.page_size
+    qsl = b.query_start_loc.tolist()
+    for s, t in ((1, 137), (2, 255)):              # decodes at positions 137 and 255 of prompt 0
+        L = t + 1
+        b.seq_lens[s] = L
+        npg = -(-L // P)
+        b.block_table[s, :npg] = b.block_table[0, :npg]
+        b.q[qsl[s]] = b.q[qsl[0] + t]
+    # sequence 3: rows 32..63 of the 64-token prompt 4, as a chunk over its first 32 keys
+    b.block_table[3] = b.block_table[4]
+    b.q[qsl[3]:qsl[3] + 32] = b.q[qsl[4] + 32:qsl[4] + 64]
+    log("V7 / V6 on device: decode vs prefill rows, chunked vs one-shot prefill")
+    out, lse, _ = run(b)
+    close(out[qsl[1]], out[qsl[0] + 137], "decode at 137 vs prefill row 137")
+    close(out[qsl[2]], out[qsl[0] + 255], "decode at 255 vs prefill row 255")
+    assert np.allclose(lse[qsl[1]].numpy(), lse[qsl[0] + 137].numpy(), atol=1e-3)
+    close(out[qsl[3]:qsl[3] + 32], out[qsl[4] + 32:qsl[4] + 64], "chunk vs one-shot")
+    assert np.allclose(lse[qsl[3]:qsl[3] + 32].numpy(), lse[qsl[4] + 32:qsl[4] + 64].numpy(), atol=1e-3)
