@@ -242,3 +242,18 @@ def test_split_head_latent_prefill_ragged():
 
 def test_full_split_head_latent_sampled():
     sampled_check("mla_split", n_pre_rows=8)
+
+
+@pytest.mark.parametrize("mode", ["serial", "corun", "fused"])
+def test_batch_without_query_tokens(mode):
+    """Every sequence has context but no new token: each mode returns at once
+    with an empty output and nothing launched."""
+    b = custom_batch(QW, [0, 0, 0], [40, 0, 7], seed=11)
+    corun = F.Corun(128, 128) if mode == "corun" else None
+    m = {"serial": F.FLEX_MODE_SERIAL, "corun": F.FLEX_MODE_CORUN, "fused": F.FLEX_MODE_FUSED}[mode]
+    log(f"batch with no query tokens, mode {mode}")
+    out, lse, pa = run(b, mode=m, corun=corun)
+    assert out.shape == (0, QW.num_q_heads, QW.head_dim_v) and lse.shape == (0, QW.num_q_heads)
+    assert pa.plan.info["n_decode_items"] == 0 and pa.plan.info["n_prefill_items"] == 0
+    if corun is not None:
+        corun.close()
