@@ -427,6 +427,46 @@ int flex_ctl_decide(flex_ctl_t* ctl, const flex_ctl_signals* sig, flex_ctl_decis
  * split, then the serial pair; K entries each, capacity >= K. */
 int flex_ctl_estimates(const flex_ctl_t* ctl, double* decode_gbps, double* prefill_tflops, int32_t capacity);
 
+/* ------------------------------------------------------------------------
+ * Time-slice scheduler: temporal multiplexing of the phases instead of CU
+ * partitioning (Sec. 3 and Sec. 3.4: when the device offers no spatial
+ * partitioning, each phase's execution share is enforced by dispatch control
+ * and phase-aware temporal multiplexing; Sec. 4: the prefill/decode
+ * time-slice ratio is the knob of the serving experiments).
+ *
+ * Each step runs one phase alone on the whole device (flex_attn_decode or
+ * flex_attn_prefill on a batch holding only that phase). The scheduler keeps
+ * the device time spent in each phase, both totals multiplied by `decay`
+ * before every new observation is added (a window of about 1 / (1 - decay)
+ * steps; decay 1 keeps the whole history), and picks the next step's phase:
+ * the only ready phase if one is ready; with both ready, decode when
+ * decode_ms * (1 - decode_share) <= prefill_ms * decode_share (decode's
+ * share of the windowed time is at or below its target, ties to decode),
+ * else prefill. Over a run with both phases always ready and decay 1, decode's
+ * share of the total time stays within one step's duration of decode_share.
+ * Host-only; no HIP call.
+ * ---------------------------------------------------------------------- */
+typedef struct flex_ts flex_ts_t;
+
+/* A zero field takes the default in brackets. */
+typedef struct flex_ts_opts {
+  double decode_share;          /* target fraction of device time for decode, in (0, 1) [0.5] */
+  double decay;                 /* weight kept by past time at each observation, in (0, 1] [1] */
+} flex_ts_opts;
+
+#define FLEX_TS_DECODE 0
+#define FLEX_TS_PREFILL 1
+
+int flex_ts_create(const flex_ts_opts* opts, flex_ts_t** out);
+void flex_ts_destroy(flex_ts_t* ts);
+/* Next step's phase (FLEX_TS_DECODE or FLEX_TS_PREFILL) into *phase.
+ * FLEX_ERR_INVALID_ARG when neither phase is ready. */
+int flex_ts_next(const flex_ts_t* ts, int32_t decode_ready, int32_t prefill_ready, int32_t* phase);
+/* A finished step: its phase and duration (ms, >= 0). */
+int flex_ts_observe(flex_ts_t* ts, int32_t phase, double ms);
+/* The windowed device time of each phase (ms). */
+int flex_ts_totals(const flex_ts_t* ts, double* decode_ms, double* prefill_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -228,3 +228,42 @@ class Controller:
 
     def estimates(self):
         return self.dec[1:], self.pre[1:]
+
+
+# ---------------------------------------------------------------------------
+# Time-slice scheduler (temporal multiplexing of the phases; Sec. 3, Sec. 3.4;
+# the time-slice ratio of Sec. 4). The paper fixes no rule; the library's is a
+# deficit rule, restated here: each step runs one phase on the whole device;
+# with both phases ready, decode runs when its share of the windowed device
+# time is at most decode_share, i.e. t_dec * (1 - share) <= t_pre * share in
+# double precision (ties to decode), else prefill; with one ready, that one.
+# Before each observation both totals are multiplied by decay.
+
+TS_DECODE, TS_PREFILL = 0, 1
+
+
+class TimeSlice:
+    def __init__(self, decode_share: float = 0.0, decay: float = 0.0):
+        self.share = decode_share if decode_share != 0.0 else 0.5
+        self.decay = decay if decay != 0.0 else 1.0
+        if not (0.0 < self.share < 1.0) or not (0.0 < self.decay <= 1.0):
+            raise ValueError("decode_share in (0, 1), decay in (0, 1]")
+        self.t_dec = 0.0
+        self.t_pre = 0.0
+
+    def next(self, decode_ready: bool, prefill_ready: bool) -> int:
+        if not decode_ready and not prefill_ready:
+            raise ValueError("neither phase has work")
+        if not prefill_ready:
+            return TS_DECODE
+        if not decode_ready:
+            return TS_PREFILL
+        return TS_DECODE if self.t_dec * (1.0 - self.share) <= self.t_pre * self.share else TS_PREFILL
+
+    def observe(self, phase: int, ms: float):
+        self.t_dec *= self.decay
+        self.t_pre *= self.decay
+        if phase == TS_DECODE:
+            self.t_dec += ms
+        else:
+            self.t_pre += ms

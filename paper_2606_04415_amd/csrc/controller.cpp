@@ -261,3 +261,66 @@ extern "C" int flex_ctl_estimates(const flex_ctl_t* c, double* dg, double* pt, i
   }
   return FLEX_OK;
 }
+
+// ---------------------------------------------------------------------------
+// Time-slice scheduler (temporal multiplexing, Sec. 3 and Sec. 3.4; the
+// time-slice ratio of Sec. 4): one phase per step on the whole device, the
+// phase chosen so that decode's share of the windowed device time tracks
+// decode_share. A deficit rule: whichever phase is below its share runs next.
+
+struct flex_ts {
+  double share;
+  double decay;
+  double t_dec = 0.0;
+  double t_pre = 0.0;
+};
+
+extern "C" int flex_ts_create(const flex_ts_opts* opts, flex_ts_t** out) {
+  flexattn::clear_error();
+  if (!out) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  *out = nullptr;
+  flex_ts_opts o{};
+  if (opts) o = *opts;
+  if (o.decode_share == 0.0) o.decode_share = 0.5;
+  if (o.decay == 0.0) o.decay = 1.0;
+  if (!(o.decode_share > 0.0 && o.decode_share < 1.0))
+    return set_error(FLEX_ERR_INVALID_ARG, "decode_share must lie in (0, 1)");
+  if (!(o.decay > 0.0 && o.decay <= 1.0)) return set_error(FLEX_ERR_INVALID_ARG, "decay must lie in (0, 1]");
+  flex_ts* t = new (std::nothrow) flex_ts;
+  if (!t) return set_error(FLEX_ERR_INTERNAL, "out of host memory");
+  t->share = o.decode_share;
+  t->decay = o.decay;
+  *out = t;
+  return FLEX_OK;
+}
+
+extern "C" void flex_ts_destroy(flex_ts_t* t) { delete t; }
+
+extern "C" int flex_ts_next(const flex_ts_t* t, int32_t decode_ready, int32_t prefill_ready, int32_t* phase) {
+  flexattn::clear_error();
+  if (!t || !phase) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  if (!decode_ready && !prefill_ready) return set_error(FLEX_ERR_INVALID_ARG, "neither phase has work");
+  if (!prefill_ready) *phase = FLEX_TS_DECODE;
+  else if (!decode_ready) *phase = FLEX_TS_PREFILL;
+  else *phase = t->t_dec * (1.0 - t->share) <= t->t_pre * t->share ? FLEX_TS_DECODE : FLEX_TS_PREFILL;
+  return FLEX_OK;
+}
+
+extern "C" int flex_ts_observe(flex_ts_t* t, int32_t phase, double ms) {
+  flexattn::clear_error();
+  if (!t) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  if (phase != FLEX_TS_DECODE && phase != FLEX_TS_PREFILL) return set_error(FLEX_ERR_INVALID_ARG, "unknown phase");
+  if (!(ms >= 0.0) || !std::isfinite(ms)) return set_error(FLEX_ERR_INVALID_ARG, "duration must be finite and >= 0");
+  t->t_dec *= t->decay;
+  t->t_pre *= t->decay;
+  (phase == FLEX_TS_DECODE ? t->t_dec : t->t_pre) += ms;
+  return FLEX_OK;
+}
+
+extern "C" int flex_ts_totals(const flex_ts_t* t, double* decode_ms, double* prefill_ms) {
+  flexattn::clear_error();
+  if (!t || !decode_ms || !prefill_ms) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  *decode_ms = t->t_dec;
+  *prefill_ms = t->t_pre;
+  return FLEX_OK;
+}

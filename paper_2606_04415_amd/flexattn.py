@@ -33,7 +33,7 @@ EXPORTED = [
     "flex_attn_corun_streams", "flex_attn_corun_set_timing", "flex_attn_corun_timing_read",
     "flex_attn_debug_gather", "flex_attn_workspace_init", "flex_attn_kv_append",
     "flex_ctl_create", "flex_ctl_destroy", "flex_ctl_set_profile", "flex_ctl_observe", "flex_ctl_decide",
-    "flex_ctl_estimates",
+    "flex_ctl_estimates", "flex_ts_create", "flex_ts_destroy", "flex_ts_next", "flex_ts_observe", "flex_ts_totals",
 ]
 FLEX_CTL_ONE_PHASE = 0
 FLEX_CTL_BEST = 1
@@ -43,6 +43,8 @@ FLEX_CTL_BW_SATURATED = 4
 FLEX_CTL_EXPLORE = 5
 FLEX_CTL_PREFILL_BACKLOG = 6
 FLEX_CTL_FUSED_FASTER = 7
+FLEX_TS_DECODE = 0
+FLEX_TS_PREFILL = 1
 FLEX_TIMING_RING = 1024
 
 
@@ -119,6 +121,10 @@ class CtlDecision(ctypes.Structure):
                 ("reason", ctypes.c_int32), ("predicted_us", ctypes.c_double)]
 
 
+class TsOpts(ctypes.Structure):
+    _fields_ = [("decode_share", ctypes.c_double), ("decay", ctypes.c_double)]
+
+
 class FlexAttnError(RuntimeError):
     def __init__(self, status: int, what: str, detail: str):
         super().__init__(f"{what}: status {status} ({detail})")
@@ -170,9 +176,15 @@ def lib():
     L.flex_ctl_observe.argtypes = [vp, ctypes.POINTER(CtlObservation)]
     L.flex_ctl_decide.argtypes = [vp, ctypes.POINTER(CtlSignals), ctypes.POINTER(CtlDecision)]
     L.flex_ctl_estimates.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i32]
+    L.flex_ts_create.argtypes = [ctypes.POINTER(TsOpts), ctypes.POINTER(vp)]
+    L.flex_ts_destroy.argtypes = [vp]
+    L.flex_ts_destroy.restype = None
+    L.flex_ts_next.argtypes = [vp, i32, i32, ctypes.POINTER(i32)]
+    L.flex_ts_observe.argtypes = [vp, i32, ctypes.c_double]
+    L.flex_ts_totals.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     for f in EXPORTED:
         if f not in ("flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan_destroy",
-                     "flex_attn_corun_destroy"):
+                     "flex_attn_corun_destroy", "flex_ctl_destroy", "flex_ts_destroy"):
             getattr(L, f).restype = ctypes.c_int
     _lib = L
     return L
@@ -409,6 +421,41 @@ class Controller:
         dg, pt = (ctypes.c_double * self.K)(), (ctypes.c_double * self.K)()
         check(lib().flex_ctl_estimates(self.handle, dg, pt, self.K), "flex_ctl_estimates")
         return list(dg), list(pt)
+
+
+class TimeSlice:
+    """The time-slice scheduler (flex_ts_*): one phase per step, decode's share
+    of the device time held near decode_share."""
+
+    def __init__(self, decode_share=0.5, decay=1.0):
+        h = ctypes.c_void_p()
+        check(lib().flex_ts_create(ctypes.byref(TsOpts(decode_share, decay)), ctypes.byref(h)), "flex_ts_create")
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            lib().flex_ts_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def next(self, decode_ready: bool, prefill_ready: bool) -> int:
+        ph = ctypes.c_int32()
+        check(lib().flex_ts_next(self.handle, int(bool(decode_ready)), int(bool(prefill_ready)), ctypes.byref(ph)),
+              "flex_ts_next")
+        return ph.value
+
+    def observe(self, phase: int, ms: float):
+        check(lib().flex_ts_observe(self.handle, int(phase), float(ms)), "flex_ts_observe")
+
+    def totals(self):
+        d, p = ctypes.c_double(), ctypes.c_double()
+        check(lib().flex_ts_totals(self.handle, ctypes.byref(d), ctypes.byref(p)), "flex_ts_totals")
+        return d.value, p.value
 
 
 class Corun:

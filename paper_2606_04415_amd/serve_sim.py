@@ -15,21 +15,29 @@ step-time distribution and TTFT / TPOT proxies:
               observing every step's phase times (dynamic co-location;
               Sec. 3.3, Sec. 3.4);
 * fused       a step with both phases runs as one launch whose work-groups
-              interleave the phases (no CU masks), otherwise serial.
+              interleave the phases (no CU masks), otherwise serial;
+* timeslice   temporal multiplexing instead of co-location inside a step:
+              each step runs one phase alone on all CUs (all decodes, or
+              prompt chunks), flex_ts_* choosing the phase so that decode's
+              share of the recent device time tracks a target
+              (`timeslice:0.3` = 30%; Sec. 3 and Sec. 3.4, and the time-slice
+              ratio of Sec. 4).
 
 The stream is defined in steps, not in time: requests arrive at given steps,
 are admitted while there is room, and are prefilled in chunks of at most
 `chunk` tokens per step (oldest first) before they decode one token per step.
-So every policy runs exactly the same sequence of batches; only the time
-each step takes differs. A step is the KV append of its new tokens plus the
+So every co-location policy runs exactly the same sequence of batches; only
+the time each step takes differs (timeslice splits each such batch's phases
+over separate steps). A step is the KV append of its new tokens plus the
 attention of the mixed batch (GPU time, HIP events on the issuing stream,
 with no per-phase events inside: the controller's phase times come from an
 untimed repeat of the step's attention); plan building and upload are host
 work outside it. Request time stamps use
 the running sum of step times: TTFT = end of the step that finishes a
-request's prompt minus the time it arrived; TPOT = the time of the step that
-produced each decode token, over all decode tokens of the run (every decoding
-request gets one token per step). Synthetic: random K/V contents, Qwen2.5-7B attention
+request's prompt minus the time it arrived; TPOT = the time from a request's
+previous token (or the end of its prompt) to each of its decode tokens, over
+all decode tokens of the run (under the co-location policies every decoding
+request gets one token per step, so this is that step's time). Synthetic: random K/V contents, Qwen2.5-7B attention
 geometry (28/4 heads x 128, page 16), lengths drawn from a seeded generator.
 
     python -m paper_2606_04415_amd.serve_sim --mix 1k1k --steps 300
@@ -68,6 +76,7 @@ class Req:
     prefilled: int = 0
     generated: int = 0
     pages: List[int] = field(default_factory=list)
+    last_tok_ms: float = 0.0
     first_ms: Optional[float] = None
     finish_ms: Optional[float] = None
 
@@ -124,6 +133,12 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
     coruns = {cd: F.Corun(256 - cd, cd) for cd in (64, 128, 192)}
     serial_timer = coruns[128]
     ctl = None
+    ts = None
+    if policy.startswith("timeslice"):
+        share = float(policy.split(":")[1]) if ":" in policy else args.decode_share
+        ts = F.TimeSlice(share, getattr(args, "ts_decay", 0.9))
+    phase_ms: Dict[str, float] = {}   # device time of decode-only, prefill-only and mixed steps
+    prefill_tokens = 0
     if policy == "controller":
         ctl = F.Controller()
         if profile:
@@ -138,7 +153,7 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
     nxt = 0
     clock = 0.0
     step_ms: List[float] = []
-    tok_ms: List[float] = []   # step time of every decode token
+    tok_ms: List[float] = []   # time since the previous token, for every decode token
     splits: Dict[str, int] = {}
     reasons: Dict[int, int] = {}
     done: List[Req] = []
@@ -168,6 +183,15 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
                 ns.append(c)
                 ls.append(r.prefilled + c)
                 members.append((r, c))
+        if ts is not None and members:
+            has_dec = any(n == 1 and r.prefilled == r.prompt for r, n in members)
+            has_pre = len(members) > sum(1 for r, n in members if n == 1 and r.prefilled == r.prompt)
+            phase = ts.next(has_dec, has_pre)
+            keep = [i for i, (r, n) in enumerate(members)
+                    if (n == 1 and r.prefilled == r.prompt) == (phase == F.FLEX_TS_DECODE)]
+            if phase == F.FLEX_TS_DECODE:
+                budget = args.chunk                      # no prompt tokens run this step
+            ns, ls, members = [ns[i] for i in keep], [ls[i] for i in keep], [members[i] for i in keep]
         if not members:
             step_ms.append(0.0)
             continue
@@ -215,6 +239,8 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         else:
             pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd), qsl, ls, max_pages)
         key = {F.FLEX_MODE_SERIAL: "serial", F.FLEX_MODE_FUSED: "fused"}.get(mode, f"{256 - cd}:{cd}")
+        if ts is not None:
+            key = "decode" if phase == F.FLEX_TS_DECODE else "prefill"
         splits[key] = splits.get(key, 0) + 1
         d_bt = bt.to(dev)
         d_sl = torch.tensor(ls, dtype=torch.int32, device=dev)
@@ -246,18 +272,26 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
             ctl.observe(cd if mode == F.FLEX_MODE_CORUN else 0, info["decode_bytes"], info["prefill_flops"],
                         dec_ms[-1] if dec_ms else 0.0, pre_ms[-1] if pre_ms else 0.0,
                         step_ms=attn_ms if mode == F.FLEX_MODE_SERIAL else 0.0)
+        if ts is not None:
+            ts.observe(phase, ms)
+        n_dec_tok = sum(1 for r, n in members if n == 1 and r.prefilled == r.prompt)
+        kind = "decode" if n_dec_tok == len(members) else "prefill" if n_dec_tok == 0 else "mixed"
+        phase_ms[kind] = phase_ms.get(kind, 0.0) + ms
         clock += ms
         step_ms.append(ms)
-        tok_ms.extend([ms] * sum(1 for r, n in members if n == 1 and r.prefilled == r.prompt))
         # advance the requests
         for r, n in members:
             if n == 1 and r.prefilled == r.prompt:
                 r.generated += 1
+                tok_ms.append(clock - r.last_tok_ms)
+                r.last_tok_ms = clock
             else:
                 r.prefilled += n
+                prefill_tokens += n
                 if r.prefilled == r.prompt:
                     r.generated = 1
                     r.first_ms = clock
+                    r.last_tok_ms = clock
             if r.generated >= r.out:
                 r.finish_ms = clock
                 free_pages.extend(r.pages)
@@ -266,6 +300,8 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         active = [r for r in active if r.finish_ms is None]
     for c in coruns.values():
         c.close()
+    if ts is not None:
+        ts.close()
 
     def pct(xs, p):
         xs = sorted(xs)
@@ -280,6 +316,9 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
                        "mean": round(sum(ttft) / len(ttft), 3) if ttft else None},
            "tpot_ms": {"tokens": len(tok_ms), "mean": round(sum(tok_ms) / len(tok_ms), 4) if tok_ms else None,
                        "p90": pct(tok_ms, 0.9)},
+           "throughput": {"decode_tok_per_s": round(len(tok_ms) / clock * 1e3, 1) if clock else None,
+                          "prefill_tok_per_s": round(prefill_tokens / clock * 1e3, 1) if clock else None},
+           "device_ms": {k: round(v, 3) for k, v in phase_ms.items()},
            "splits": splits}
     if ctl is not None:
         res["reasons"] = {str(k): v for k, v in sorted(reasons.items())}
@@ -310,6 +349,10 @@ def main():
     ap.add_argument("--rate", type=float, default=0.2, help="Poisson arrivals per step")
     ap.add_argument("--fixed-decode-cus", type=int, default=128)
     ap.add_argument("--no-profile", action="store_true", help="controller starts from its prior only")
+    ap.add_argument("--decode-share", type=float, default=0.5,
+                    help="timeslice policy: target decode share of device time (or name it: timeslice:0.3)")
+    ap.add_argument("--ts-decay", type=float, default=0.9,
+                    help="timeslice policy: weight kept by past device time per step (window ~ 1 / (1 - decay))")
     ap.add_argument("--no-controller-fused", dest="controller_fused", action="store_false",
                     help="the controller chooses between serial and co-run only")
     args = ap.parse_args()

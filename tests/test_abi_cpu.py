@@ -25,7 +25,7 @@ HEADER = os.path.join(ROOT, "include", "flexattn.h")
 def header_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(flex_(?:attn|ctl)_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(flex_(?:attn|ctl|ts)_\w+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol():

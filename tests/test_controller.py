@@ -244,3 +244,93 @@ def test_fused_ratio_is_relative_to_observed_serial_steps():
     assert abs(d["predicted_us"] - 0.8 * serial_us) < 1e-9
     # step-time-only observations leave the phase-rate estimates alone
     assert abs(ctl.decide(B, Fl, active_decode_seqs=8)["predicted_us"] - serial_us) < 1e-9
+
+
+# ---------------------------------------------------------------------------
+# Time-slice scheduler (flex_ts_*)
+
+def test_timeslice_worked_example():
+    """share 1/4 (decode when 3 * t_dec <= t_pre), decode steps 1 ms, prefill
+    steps 2 ms, whole history; worked by hand, (t_dec, t_pre) after each step:
+    D (1,0), P (1,2), P (1,4), D (2,4), P (2,6), D (3,6), P (3,8), P (3,10)."""
+    ts = F.TimeSlice(decode_share=0.25)
+    seq = []
+    for _ in range(8):
+        ph = ts.next(True, True)
+        seq.append("D" if ph == F.FLEX_TS_DECODE else "P")
+        ts.observe(ph, 1.0 if ph == F.FLEX_TS_DECODE else 2.0)
+    assert "".join(seq) == "DPPDPDPP"
+    assert ts.totals() == (3.0, 10.0)
+    ts.close()
+
+
+@pytest.mark.parametrize("share", [0.2, 0.5, 0.8])
+@pytest.mark.parametrize("dur", [(0.1, 0.25), (0.3, 0.07), (1.0, 1.0)])
+def test_timeslice_share_converges(share, dur):
+    """Both phases always ready, whole history: after every step decode's share of
+    the total time is within one step's duration (relative to the total) of the target."""
+    ts = F.TimeSlice(decode_share=share)
+    td = tp = 0.0
+    for i in range(400):
+        ph = ts.next(True, True)
+        ts.observe(ph, dur[ph])
+        if ph == F.FLEX_TS_DECODE:
+            td += dur[0]
+        else:
+            tp += dur[1]
+        if i > 10:
+            assert abs(td / (td + tp) - share) <= max(dur) / (td + tp) + 1e-12
+    ts.close()
+
+
+def test_timeslice_one_ready_phase_and_errors():
+    ts = F.TimeSlice(decode_share=0.9)
+    for _ in range(5):
+        assert ts.next(False, True) == F.FLEX_TS_PREFILL
+        ts.observe(F.FLEX_TS_PREFILL, 1.0)
+    assert ts.next(True, False) == F.FLEX_TS_DECODE
+    with pytest.raises(F.FlexAttnError):
+        ts.next(False, False)
+    with pytest.raises(F.FlexAttnError):
+        ts.observe(7, 1.0)
+    with pytest.raises(F.FlexAttnError):
+        ts.observe(F.FLEX_TS_DECODE, -1.0)
+    with pytest.raises(F.FlexAttnError):
+        F.TimeSlice(decode_share=1.0)
+    with pytest.raises(F.FlexAttnError):
+        F.TimeSlice(decode_share=0.5, decay=1.5)
+    ts.close()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_timeslice_matches_rederivation(seed):
+    """Random readiness and durations, a decaying window: every choice and the
+    final totals equal the re-derivation's, exactly."""
+    rng = random.Random(seed)
+    share, decay = rng.uniform(0.05, 0.95), rng.choice([1.0, 0.9, 0.5])
+    a, b = F.TimeSlice(share, decay), OC.TimeSlice(share, decay)
+    for _ in range(500):
+        dr, pr = bool(rng.random() < 0.9), bool(rng.random() < 0.7)
+        if not (dr or pr):
+            continue
+        pa, pb = a.next(dr, pr), b.next(dr, pr)
+        assert pa == pb
+        ms = rng.expovariate(1.0 / (0.2 if pa == OC.TS_DECODE else 0.5))
+        a.observe(pa, ms)
+        b.observe(pb, ms)
+    assert a.totals() == (b.t_dec, b.t_pre)
+    a.close()
+
+
+def test_timeslice_decay_forgets():
+    """decay 0.5: after a long prefill-only stretch the decode total has decayed
+    to nothing, so decode runs first when both become ready again."""
+    ts = F.TimeSlice(decode_share=0.1, decay=0.5)
+    for _ in range(3):
+        ts.observe(F.FLEX_TS_DECODE, 10.0)
+    for _ in range(60):
+        ts.observe(F.FLEX_TS_PREFILL, 0.01)
+    d, p = ts.totals()
+    assert d < 1e-15 and p > 0
+    assert ts.next(True, True) == F.FLEX_TS_DECODE
+    ts.close()

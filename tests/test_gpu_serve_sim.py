@@ -30,3 +30,15 @@ def test_policies_replay_the_same_stream():
     assert set(res["fused"]["splits"]) <= {"serial", "fused"} and "fused" in res["fused"]["splits"]
     for r in res.values():
         assert r["total_ms"] > 0 and r["step_ms"]["max"] < 50.0
+
+
+def test_timeslice_policy_runs_one_phase_per_step():
+    args = argparse.Namespace(steps=24, seed=3, warm=40, max_active=48, chunk=2048, burst=8, burst_every=10,
+                              rate=0.3, fixed_decode_cus=128, per_mix_limits=False, decode_share=0.5, ts_decay=0.9)
+    log("serve loop: mix long, time-sliced at 40% decode, 24 steps")
+    r = serve_sim.simulate("long", "timeslice:0.4", args, profile=None)
+    assert set(r["splits"]) == {"decode", "prefill"}, r["splits"]
+    assert set(r["device_ms"]) == {"decode", "prefill"}, r["device_ms"]
+    assert r["tpot_ms"]["tokens"] > 0 and r["ttft_ms"]["n"] > 0
+    # a time-sliced decode token waits for the prefill steps in between
+    assert r["tpot_ms"]["p90"] >= r["step_ms"]["p50"] * 0.5
