@@ -79,6 +79,26 @@ int main(int argc, char** argv) {
     if (flex_ctl_estimates(ctl, dg, pt, 64) != FLEX_OK) return 8;
     flex_ctl_destroy(ctl);
   }
+  // time-slice scheduler: random targets, windows, readiness and durations
+  for (int it = 0; it < iters / 10 + 1; ++it) {
+    flex_ts_opts to{std::uniform_real_distribution<double>(0.01, 0.99)(rng), pick(0, 1) ? 1.0 : 0.9};
+    flex_ts_t* ts = nullptr;
+    if (flex_ts_create(&to, &ts) != FLEX_OK) return 10;
+    for (int s = 0; s < 50; ++s) {
+      const int dr = pick(0, 1), pr = pick(0, 1);
+      int32_t ph = -1;
+      const int st = flex_ts_next(ts, dr, pr, &ph);
+      if (!dr && !pr) {
+        if (st != FLEX_ERR_INVALID_ARG) return 11;
+        continue;
+      }
+      if (st != FLEX_OK || (ph == FLEX_TS_DECODE ? !dr : !pr)) return 12;
+      if (flex_ts_observe(ts, ph, pick(0, 1000) * 1e-3) != FLEX_OK) return 13;
+    }
+    double d = -1, p = -1;
+    if (flex_ts_totals(ts, &d, &p) != FLEX_OK || d < 0 || p < 0) return 14;
+    flex_ts_destroy(ts);
+  }
   std::printf("plans ok %d rejected %d\n", ok, rejected);
   return ok > 0 && rejected > 0 ? 0 : 9;
 }
