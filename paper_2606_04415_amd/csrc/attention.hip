@@ -1232,16 +1232,17 @@ static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 gr
     if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(q, g1, stream);
     if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(q, g1, stream);
     if constexpr (P == 64) {
-      if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 64, false, kPrefillPerHead, 64, 3>(q, g1, stream);
+      if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 32, false, kPrefillPerHead, 64, 3>(q, g1, stream);
     }
     return hipErrorInvalidValue;
   }
   if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
   // Heads split out (keys 192, values 128): one work-group per (128-token
-  // tile, query head); 64-key tiles, each inside one 64-slot page.
+  // tile, query head); 32-key tiles (three stages in 74 KB of LDS, 122
+  // VGPRs), so two work-groups share a CU.
   if constexpr (P == 64) {
-    if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 64, false, kPrefillPerHead, 64, 3>(p, grid, stream);
+    if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 32, false, kPrefillPerHead, 64, 3>(p, grid, stream);
   }
   return hipErrorInvalidValue;
 }
