@@ -1196,18 +1196,21 @@ hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStrea
 }
 
 // Grouped-query prefill: one wave per query head of a KV head (4 waves when
-// the group has at most 4 heads, else 8), bm/16 token blocks per wave.
+// the group has at most 4 heads, else 8), bm/16 token blocks per wave. The
+// 16-wave form takes 64-key tiles (one work-group per CU); the smaller forms
+// take 32-key tiles in three stages (50 KB of LDS at d = 128), so that two or
+// more work-groups share a CU and their barriers do not line up.
 template <int D, int P>
 static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid, hipStream_t stream) {
   constexpr int BN = 64;
   constexpr int NS = D == 128 ? 3 : 4;
   const bool narrow = p.G <= 4;
   if (bm == 32)
-    return narrow ? launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, NS, 2>(p, grid, stream)
+    return narrow ? launch_rowpar<D, D, 8, 1, 32, false, kPrefillGrouped, P, 3, 2>(p, grid, stream)
                   : launch_rowpar<D, D, 16, 1, BN, false, kPrefillGrouped, P, NS, 2>(p, grid, stream);
   if (bm == 16)
-    return narrow ? launch_rowpar<D, D, 4, 1, BN, false, kPrefillGrouped, P, NS>(p, grid, stream)
-                  : launch_rowpar<D, D, 8, 1, BN, false, kPrefillGrouped, P, NS>(p, grid, stream);
+    return narrow ? launch_rowpar<D, D, 4, 1, 32, false, kPrefillGrouped, P, 3>(p, grid, stream)
+                  : launch_rowpar<D, D, 8, 1, 32, false, kPrefillGrouped, P, 3>(p, grid, stream);
   return hipErrorInvalidValue;
 }
 

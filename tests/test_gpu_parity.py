@@ -257,3 +257,15 @@ def test_batch_without_query_tokens(mode):
     assert pa.plan.info["n_decode_items"] == 0 and pa.plan.info["n_prefill_items"] == 0
     if corun is not None:
         corun.close()
+
+
+@pytest.mark.parametrize("bm", [32, 16])
+@pytest.mark.parametrize("d", [128, 64])
+def test_narrow_group_prefill_tiles(bm, d):
+    """Four query heads per KV head (the 4- and 8-wave prefill forms, 32-key
+    tiles) over ragged chunks, both head sizes and tile heights."""
+    ns, ls = [1, 77, 1, 150, 33], [500, 77, 40, 300, 1000]
+    b = custom_batch(QW, ns, ls, seed=12, num_q_heads=16, num_kv_heads=4, head_dim_qk=d, head_dim_v=d,
+                     sm_scale=d ** -0.5)
+    log(f"narrow GQA 16/4 d{d} page16, bm {bm}")
+    full_check(b, F.make_opts(bm=bm), f"narrow-d{d}-bm{bm}")
