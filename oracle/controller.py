@@ -1,4 +1,6 @@
-"""Re-derivation of the online co-location controller's decisions (host policy).
+"""Re-derivations of the host policies: the online co-location controller's
+decisions and, at the end of the module, the time-slice scheduler's phase
+choices (``TimeSlice``).
 
 TEST INFRASTRUCTURE. Only ``tests/`` may import this module. The library never
 does, and this module imports nothing from the library.
