@@ -443,8 +443,9 @@ int flex_ctl_estimates(const flex_ctl_t* ctl, double* decode_gbps, double* prefi
  * decode_ms * (1 - decode_share) <= prefill_ms * decode_share (decode's
  * share of the windowed time is at or below its target, ties to decode),
  * else prefill. Over a run with both phases always ready and decay 1, decode's
- * share of the total time stays within one step's duration of decode_share.
- * Host-only; no HIP call.
+ * time stays within one longest step of decode_share times the total time
+ * (so its share is within that step's duration over the total of the
+ * target). Host-only; no HIP call.
  * ---------------------------------------------------------------------- */
 typedef struct flex_ts flex_ts_t;
 
