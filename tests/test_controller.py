@@ -116,6 +116,11 @@ def test_saturated_decode_cedes_cus_and_backlog_takes_them():
     assert d_sat["cus_decode"] < d_back["cus_decode"]
     # saturated decode never gets more CUs than saturation needs (within the band)
     assert d_sat["cus_decode"] <= 192
+    # a prefill backlog (no bandwidth pressure observed) also takes the smallest
+    # decode share of the band, the same choice as bandwidth pressure
+    d_pre = fresh().decide(B, Fl, pending_prefill_tokens=100000, active_decode_seqs=128)
+    assert d_pre["reason"] == F.FLEX_CTL_PREFILL_BACKLOG
+    assert d_pre["cus_decode"] == d_sat["cus_decode"] <= base["cus_decode"]
 
 
 def test_one_phase_runs_serial():
