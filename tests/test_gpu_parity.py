@@ -6,6 +6,8 @@ rows the oracle computes one by one. Unused pages hold NaN and tail slots
 hold +/-1e4 (see workloads.make_batch), so a wrong page index or an unmasked
 tail read breaks parity.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -173,8 +175,8 @@ def test_corun_bitwise_equals_serial(split):
     corun.close()
 
 
-def sampled_check(name, n_dec=6, n_pre_rows=12, mode=F.FLEX_MODE_SERIAL, split=None):
-    w = WORKLOADS[name]
+def sampled_check(name, n_dec=6, n_pre_rows=12, mode=F.FLEX_MODE_SERIAL, split=None, w=None):
+    w = w or WORKLOADS[name]
     log(f"{name}: drawing the full-size batch")
     b = make_batch(w, seed=0)
     d = device_inputs(b)
@@ -269,3 +271,10 @@ def test_narrow_group_prefill_tiles(bm, d):
                      sm_scale=d ** -0.5)
     log(f"narrow GQA 16/4 d{d} page16, bm {bm}")
     full_check(b, F.make_opts(bm=bm), f"narrow-d{d}-bm{bm}")
+
+
+def test_full_prefill_narrow_group_sampled():
+    """The 8 x 2048 causal prefill with 16 query heads on the 4 KV heads (the
+    8-wave, 32-key-tile form) at full size, on sampled rows."""
+    w = dataclasses.replace(WORKLOADS["prefill"], num_q_heads=16)
+    sampled_check("prefill-16/4", w=w)
