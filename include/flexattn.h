@@ -262,9 +262,13 @@ int flex_attn_corun_timing_read(flex_attn_corun_t* corun, float* prefill_ms, flo
                                 int32_t max_steps, int32_t* n_steps);
 
 /* Test aid: copy the L_s key rows (and value rows unless v_aliases_k) of
- * sequence seq, gathered through block_table by the same page-address
- * arithmetic the attention kernels use, into contiguous k_out [L_s, Hkv, d_qk]
- * and v_out [L_s, Hkv, d_v] (bf16). seq_len is L_s on the host. */
+ * sequence seq, gathered through block_table with a plain per-element page
+ * lookup (row t from page block_table[seq][t / P], slot t % P, the paging
+ * contract above), into contiguous k_out [L_s, Hkv, d_qk] and
+ * v_out [L_s, Hkv, d_v] (bf16). It checks the caller's block table and
+ * strides against the contract; it does not run the attention kernels' own
+ * address paths (those load through page windows staged in LDS and buffer
+ * resources per page). seq_len is L_s on the host. */
 int flex_attn_debug_gather(const flex_attn_plan_t* plan, const flex_attn_args* args, int32_t seq,
                            int32_t seq_len, void* k_out, void* v_out, void* stream);
 

@@ -91,31 +91,36 @@ def softmax_rows(z: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 def sequence_attention(q_s: np.ndarray, K: np.ndarray, V: np.ndarray, L: int,
                        num_kv_heads: int, sm_scale: float,
                        rows: Optional[Sequence[int]] = None,
-                       row_block: int = 256) -> Tuple[np.ndarray, np.ndarray]:
+                       block: int = 2048) -> Tuple[np.ndarray, np.ndarray]:
     """Attention of one sequence's n queries over its L gathered keys.
 
     q_s [n, Hq, d_qk] fp64, K [L, Hkv, d_qk], V [L, Hkv, d_v]. ``rows`` selects
-    a subset of the n queries (sampled checks at large sizes). Rows are done in
-    blocks of ``row_block`` to bound memory; each row is independent.
+    a subset of the n queries (sampled checks at large sizes). Every (row,
+    query head) pair is independent; the pairs whose head reads KV head g are
+    stacked into one product with that head's keys, a block of about
+    ``block`` pairs at a time to bound memory.
     """
     n, Hq, _ = q_s.shape
     dv = V.shape[-1]
     idx = np.arange(n) if rows is None else np.asarray(list(rows), dtype=np.int64)
     out = np.empty((len(idx), Hq, dv), dtype=np.float64)
     lse = np.empty((len(idx), Hq), dtype=np.float64)
-    for h in range(Hq):
-        g = kv_head_of(h, Hq, num_kv_heads)
+    for g in range(num_kv_heads):
+        heads = np.array([h for h in range(Hq) if kv_head_of(h, Hq, num_kv_heads) == g])
         Kg = K[:, g, :]          # [L, d_qk]
         Vg = V[:, g, :]          # [L, d_v]
-        for b0 in range(0, len(idx), row_block):
-            rb = idx[b0:b0 + row_block]
-            z = sm_scale * (q_s[rb, h, :] @ Kg.T)          # [rows, L]
-            limits = np.array([causal_limit(int(i), n, L) for i in rb])
+        rows_per_block = max(1, block // len(heads))
+        for b0 in range(0, len(idx), rows_per_block):
+            rb = idx[b0:b0 + rows_per_block]
+            Qb = q_s[rb][:, heads, :].reshape(len(rb) * len(heads), -1)   # (row, head) pairs
+            z = sm_scale * (Qb @ Kg.T)                                    # [pairs, L]
+            limits = np.repeat([causal_limit(int(i), n, L) for i in rb], len(heads))
             visible = np.arange(L)[None, :] < limits[:, None]
             z = np.where(visible, z, -np.inf)
             w, ls = softmax_rows(z)
-            out[b0:b0 + len(rb), h, :] = w @ Vg
-            lse[b0:b0 + len(rb), h] = ls
+            o = w @ Vg
+            out[b0:b0 + len(rb), heads, :] = o.reshape(len(rb), len(heads), dv)
+            lse[b0:b0 + len(rb), heads] = ls.reshape(len(rb), len(heads))
     return out, lse
 
 

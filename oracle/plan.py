@@ -34,10 +34,17 @@ the contract is:
   piece launches lists them by key count descending, ties by slot, and a
   merge list gives the first piece of every sequence cut into several pieces
   (batch order). max_splits is accepted and ignored.
-* prefill tiles of BM rows (BM 32 by default for grouped-query heads, 128 for
-  the latent layout, which also takes 64): rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end;
-  ordered by key_end descending, then sequence, then tile. Each tile is served
-  by Hkv * ceil(G / 8) work-groups (grouped-query) or Hq (latent layouts).
+* prefill tiles of BM rows (128 for the latent layout, which also takes 64):
+  rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end; ordered by
+  key_end descending, then sequence, then tile. Each tile is served by
+  Hkv * ceil(G / 8) work-groups (grouped-query) or Hq (latent layouts).
+  Grouped-query BM is 16, 32 or 128; BM = 128 makes flat tiles: a row is a
+  (token, query head) pair of one KV head, r = token * G + head, so a
+  sequence has n * G rows; tile rows [t*BM, min(n*G, (t+1)*BM)), key_end =
+  L - n + (row_end - 1) // G + 1 (the causal limit of the last row's token);
+  one work-group per (tile, KV head), Hkv of them. With BM unset the
+  grouped-query default is 128 when sum over prefill sequences of
+  ceil(n * G / 128) * Hkv >= 4 * cus_prefill, else 32.
 * co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
@@ -101,7 +108,7 @@ class Shape:
 class Opts:
     cus_total: int = 0           # 0 -> 256
     cus_decode: int = 0          # 0 -> all; -1 -> cost model
-    bm: int = 0                  # 0 -> 32 (128 for the 576/512 layout)
+    bm: int = 0                  # 0 -> 32 or 128 by batch size (128 for the latent layouts)
     min_split_tokens: int = 0    # 0 -> 256
     max_splits: int = 0          # 0 -> 32
     wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 2 (576/512 latent layout)
@@ -159,12 +166,13 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     granule = o.split_granule or 32
     mla = sh.head_dim_qk == 576
     split = sh.head_dim_qk == 192     # heads split out: prefill only, one tile per query head
-    bm = o.bm or (128 if mla or split else 32)
+    bm = o.bm or (128 if mla or split else 0)      # grouped-query default chosen after the CU split
     if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:
         return PlanResult(ERR_INVALID_ARG)
     if o.cus_decode < -1 or o.cus_decode > cus_total:
         return PlanResult(ERR_INVALID_ARG)
-    if (mla and bm not in (64, 128)) or (split and bm != 128) or (not mla and not split and bm not in (16, 32)):
+    if (mla and bm not in (64, 128)) or (split and bm != 128) or (
+            not mla and not split and bm not in (0, 16, 32, 128)):
         return PlanResult(ERR_UNSUPPORTED)
     # --- integer metadata checks
     if max_pages_per_seq < 0:
@@ -214,6 +222,14 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         cus_decode = best if best is not None else cus_total
     cus_prefill = cus_total - cus_decode if (dec and pre and cus_decode < cus_total) else cus_total
 
+    # --- grouped-query tile height: 128 flat rows when every prefill CU gets at least
+    # four such work-groups, else 32 tokens
+    G = sh.num_q_heads // sh.num_kv_heads
+    if bm == 0:
+        flat_wgs = sum(cdiv((qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads for s in pre)
+        bm = 128 if flat_wgs >= 4 * cus_prefill else 32
+    flat = not mla and not split and bm == 128   # rows are (token, query head) pairs of one KV head
+
     # --- decode partition: balanced page ranges over the concatenated decode sequences
     min_pps = cdiv(min_tokens, P)
     pages = [cdiv(seq_lens[s], P) for s in dec]
@@ -247,9 +263,13 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     tiles = []
     for s in pre:
         n, L = qsl[s + 1] - qsl[s], seq_lens[s]
-        for t in range(cdiv(n, bm)):
-            r0, r1 = t * bm, min(n, (t + 1) * bm)
-            tiles.append([s, t, r0, r1, L - n + r1, 0, 0, 0])
+        rows = n * G if flat else n          # flat: row r is (token r // G, query head r % G)
+        if rows > 2**31 - 1:
+            return PlanResult(ERR_INVALID_ARG)
+        for t in range(cdiv(rows, bm)):
+            r0, r1 = t * bm, min(rows, (t + 1) * bm)
+            last_token = (r1 - 1) // G if flat else r1 - 1
+            tiles.append([s, t, r0, r1, L - n + last_token + 1, 0, 0, 0])
     tiles.sort(key=lambda it: (-it[4], it[0], it[1]))
 
     nd_, np_ = len(dec_items), len(tiles)
@@ -261,8 +281,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     off_merge = off_order + nd_
     off_pre = off_merge + len(merge)
     total = off_pre + ITEM * np_
-    G = sh.num_q_heads // sh.num_kv_heads
-    pre_height = sh.num_q_heads if mla or split else sh.num_kv_heads * cdiv(G, 8)
+    pre_height = sh.num_q_heads if mla or split else sh.num_kv_heads * (1 if flat else cdiv(G, 8))
     fused = fused_order(tiles, pre_height, R, T, heads_per_wg,
                         not mla and not split and G > 4 and W == 1 and heads_per_wg >= 3 and bm == 32,
                         G=G, sh=sh, o=o, cus_total=cus_total, cus_decode=cus_decode)

@@ -467,11 +467,16 @@ void decode_gqa_kernel(AttnParams p) {
 //                    query head of the KV head.
 //   kPrefillPerHead  work-group = (tile of NW*RB*16 tokens, query head).
 //   kDecodeLatent    work-group = (decode item, group of NW*RB*16 heads).
+//   kPrefillFlat     work-group = (tile of NW*RB*16 query rows, KV head): the
+//                    rows of one KV head are (token, query head) pairs taken
+//                    token-major, r = token * G + head, so every wave holds
+//                    whole 16-row blocks whatever G is; wave w owns rows
+//                    r0 + w*RB*16 .. +RB*16 of the tile.
 // LDS rows: grouped-query K/V rows are unpadded and XOR-swizzled by 16-byte
 // chunk so the MFMA operand reads are bank-conflict free; latent rows
 // (576 wide) are padded by one chunk instead.
 // ---------------------------------------------------------------------------
-enum RowMode { kPrefillGrouped = 0, kPrefillPerHead = 1, kDecodeLatent = 2 };
+enum RowMode { kPrefillGrouped = 0, kPrefillPerHead = 1, kDecodeLatent = 2, kPrefillFlat = 3 };
 
 typedef __attribute__((address_space(3))) uint8_t* lds_byte_ptr;
 
@@ -485,6 +490,31 @@ typedef __attribute__((address_space(3))) uint8_t* lds_byte_ptr;
 __device__ __forceinline__ void dma16(const void* src, void* lds_wave_base) {
   const uint32_t m0 = uint32_t(reinterpret_cast<uintptr_t>((lds_byte_ptr)(lds_wave_base)));
   asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(__builtin_amdgcn_readfirstlane(m0)) : "memory");
+}
+
+// 16-byte buffer -> LDS copy per lane: lane i writes lds_wave_base + 16 i,
+// reading rsrc base + voffset. The resource (page base, in SGPRs) is
+// wave-uniform and the per-lane offset fixed for the launch, so a tile's
+// loads cost scalar work only. Inline assembly for the same reason as dma16.
+// The resource words often come straight from v_readfirstlane: a vector
+// instruction writing an SGPR that a vector-memory instruction then reads
+// needs 5 wait states, and the compiler's hazard check does not look inside
+// inline assembly, so the block opens with them (s_nop 5: 6 wait states,
+// which also covers the M0 write before an LDS DMA).
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void dma16_buf(const i32x4& rsrc, uint32_t voffset, void* lds_wave_base) {
+  const uint32_t m0 = uint32_t(reinterpret_cast<uintptr_t>((lds_byte_ptr)(lds_wave_base)));
+  asm volatile("s_nop 5\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voffset), "s"(rsrc),
+               "{m0}"(__builtin_amdgcn_readfirstlane(m0))
+               : "memory");
+}
+
+// Raw buffer resource over [base, base + bytes) from a wave-uniform address.
+__device__ __forceinline__ i32x4 uniform_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{__builtin_amdgcn_readfirstlane(int32_t(uint32_t(a))),
+               __builtin_amdgcn_readfirstlane(int32_t(uint32_t(a >> 32) & 0xFFFFu)),
+               __builtin_amdgcn_readfirstlane(int32_t(bytes)), kBufferFlags};
 }
 
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int NS>
@@ -601,6 +631,27 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
     }
     wave_limit = wave_on ? L - nq + min(r1, wr0 + RB * 16) : 0;
     wave_full = L - nq + wr0 + 1;
+  } else if constexpr (MODE == kPrefillFlat) {
+    const int r0 = it[2], r1 = it[3];
+    key_begin = 0;
+    key_end = it[4];
+    head_kv = col;
+    const int G = p.G;
+    const int base = L - nq;                 // keys before the chunk's first token
+    const int wr0 = r0 + w * RB * 16;        // first row of the wave
+    wave_on = wr0 < r1;
+    const int rfirst = wave_on ? wr0 : r0;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int local = rfirst + rb * 16 + n;
+      const int lr = local < r1 ? local : rfirst;
+      const int tok = lr / G;
+      row_tok[rb] = q0 + tok;
+      row_head[rb] = head_kv * G + (lr - tok * G);
+      row_limit[rb] = base + tok + 1;
+    }
+    wave_limit = wave_on ? base + (min(r1, wr0 + RB * 16) - 1) / G + 1 : 0;
+    wave_full = base + rfirst / G + 1;
   } else {
     const int r0 = it[2], r1 = it[3];
     key_begin = 0;
@@ -709,9 +760,41 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
   // Issue this wave's loads of the key tile starting at kb into stage st.
   // Keys past key_end read the last key's row (masked later); padding slots
   // read a dummy row.
+  // A whole tile whose load instructions each stay in one page (every row
+  // layout but the padded latent rows with pages of at most BN keys): the
+  // tile's pages are read once into scalar registers and every load goes
+  // through a buffer resource on its page, with the launch-fixed per-lane
+  // offsets; no per-tile vector address arithmetic.
+  constexpr bool kUniformPage = !(VALIAS && P <= BN);
+  constexpr int PPT = P <= BN ? BN / P : 1;   // pages per tile
+  auto issue_whole = [&](int kb, int st, int pt_base) {
+    uint8_t* sbase = lds + st * C::STAGE;
+    int pg[PPT];
+#pragma unroll
+    for (int t = 0; t < PPT; ++t) pg[t] = __builtin_amdgcn_readfirstlane(s_pt[kb / P - pt_base + t]);
+    const uint32_t in_page = P > BN ? uint32_t(kb % P) : 0u;   // first slot of the tile in its page
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
+      const uint8_t* base = isv ? vbase : kbase;
+      const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
+      const int tp = tile_page(j, 0);
+      int page = pg[0];
+#pragma unroll
+      for (int t = 1; t < PPT; ++t) page = tp == t ? pg[t] : page;
+      const i32x4 r = uniform_rsrc(base + (uint64_t(uint32_t(page)) * sp + in_page * ss), uint32_t(min(P, BN)) * ss);
+      dma16_buf(r, ld_lane_off[j], sbase + (w * C::NI + j) * 1024);
+    }
+  };
   auto issue = [&](int kb, int st, int pt_base) {
     uint8_t* sbase = lds + st * C::STAGE;
     const bool whole = kb + BN <= key_end;
+    if constexpr (kUniformPage) {
+      if (whole) {
+        issue_whole(kb, st, pt_base);
+        return;
+      }
+    }
 #pragma unroll
     for (int j = 0; j < C::NI; ++j) {
       const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
@@ -944,7 +1027,7 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
     const int r0 = it[2], r1 = it[3];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int blk = MODE == kPrefillPerHead ? (w * RB + rb) : ((w % TB) * RB + rb);
+      const int blk = MODE == kPrefillGrouped ? ((w % TB) * RB + rb) : (w * RB + rb);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int local = r0 + blk * 16 + 4 * gq + r;
@@ -952,11 +1035,19 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
         const float lr = kValuSum ? shfl_f(ltot[rb], 4 * gq + r) : lsum[rb][r];
         if (local < r1) {
           const float inv = 1.f / lr;
-          uint16_t* dst = p.out + (int64_t(q0 + local) * p.Hq + row_head[rb]) * DV + n;
+          // output row (token, query head) of this accumulator row
+          int64_t orow;
+          if constexpr (MODE == kPrefillFlat) {
+            const int tok = local / p.G;
+            orow = int64_t(q0 + tok) * p.Hq + head_kv * p.G + (local - tok * p.G);
+          } else {
+            orow = int64_t(q0 + local) * p.Hq + row_head[rb];
+          }
+          uint16_t* dst = p.out + orow * DV + n;
 #pragma unroll
           for (int cv = 0; cv < C::NACC; ++cv)
             dst[16 * cv] = __builtin_bit_cast(uint16_t, (__bf16)(o[rb][cv][r] * inv));
-          if (n == 0 && p.lse) p.lse[int64_t(q0 + local) * p.Hq + row_head[rb]] = (mr + log2f(lr)) * kLn2;
+          if (n == 0 && p.lse) p.lse[orow] = (mr + log2f(lr)) * kLn2;
         }
       }
     }
@@ -1005,7 +1096,7 @@ void rowpar_kernel(AttnParams p) {
   // then reads the K/V of one KV head only, which its L2 can hold, instead
   // of every head's.
   int item = int(blockIdx.x), col = int(blockIdx.y);
-  if (MODE == kPrefillGrouped && p.xcd_remap) {
+  if ((MODE == kPrefillGrouped || MODE == kPrefillFlat) && p.xcd_remap) {
     const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
     col = x % p.grid_y;
     item = j * (8 / p.grid_y) + x / p.grid_y;
@@ -1020,6 +1111,23 @@ void rowpar_kernel(AttnParams p) {
     col = (j % hp8) * 8 + x;
   }
   rowpar_body<DQK, DV, NW, RB, BN, VALIAS, MODE, P, NS, TB>(p, item, col);
+}
+
+// Grouped-query prefill over flattened (token, query head) rows: WPE waves
+// per SIMD are the register budget the compiler is held to, so that
+// 4 * WPE / NW work-groups share a compute unit and their barriers drift
+// apart. 1-D XCD-aware grid as for kPrefillGrouped.
+template <int D, int NW, int RB, int BN, int P, int NS, int WPE>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
+void flat_prefill_kernel(AttnParams p) {
+  int item = int(blockIdx.x), col = int(blockIdx.y);
+  if (p.xcd_remap) {
+    const int x = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
+    col = x % p.grid_y;
+    item = j * (8 / p.grid_y) + x / p.grid_y;
+    if (item >= p.n_items) return;
+  }
+  rowpar_body<D, D, NW, RB, BN, false, kPrefillFlat, P, NS, 1>(p, item, col);
 }
 
 // ---------------------------------------------------------------------------
@@ -1120,12 +1228,18 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t words) {
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
+// Allow a kernel the dynamic LDS it launches with. The attribute is set on
+// every launch (it is a cheap host-side call), so it holds on whichever device
+// is current and a transient failure is not remembered.
+static hipError_t set_dynamic_lds(const void* kern, size_t bytes) {
+  return hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
+}
+
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB = 1>
 static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stream) {
   using C = RowParCfg<DQK, DV, NW, RB, BN, VALIAS, NS>;
   auto kern = rowpar_kernel<DQK, DV, NW, RB, BN, VALIAS, MODE, P, NS, TB>;
-  static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, int(C::LDS_BYTES));
+  const hipError_t attr = set_dynamic_lds(reinterpret_cast<const void*>(kern), C::LDS_BYTES);
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(kern, grid, dim3(C::NT), C::LDS_BYTES, stream, p);
   return hipGetLastError();
@@ -1214,8 +1328,37 @@ static hipError_t launch_prefill_grouped(const AttnParams& p, int bm, dim3 grid,
   return hipErrorInvalidValue;
 }
 
+template <int D, int NW, int RB, int BN, int P, int NS, int WPE>
+static hipError_t launch_flat_t(const AttnParams& p, dim3 grid, hipStream_t stream) {
+  using C = RowParCfg<D, D, NW, RB, BN, false, NS>;
+  auto kern = flat_prefill_kernel<D, NW, RB, BN, P, NS, WPE>;
+  const hipError_t attr = set_dynamic_lds(reinterpret_cast<const void*>(kern), C::LDS_BYTES);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kern, grid, dim3(C::NT), C::LDS_BYTES, stream, p);
+  return hipGetLastError();
+}
+
+// Flattened-row prefill: tiles of 128 (token, query head) rows, four waves
+// of 32 rows (two 16-row blocks each, so every K/V operand read from LDS
+// feeds two products), 32-key tiles in three stages (50 KB of LDS at head
+// dim 128) and at most 168 registers, so that three work-groups share a
+// compute unit and their barriers drift apart.
+template <int D, int P>
+static hipError_t launch_prefill_flat(const AttnParams& p, int bm, dim3 grid, hipStream_t stream) {
+  if (bm == 128) return launch_flat_t<D, 4, 2, 32, P, 3, 3>(p, grid, stream);
+  return hipErrorInvalidValue;
+}
+
 template <int P>
 static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 grid, hipStream_t stream) {
+  if ((dqk == 128 || dqk == 64) && bm >= 64) {
+    AttnParams q = p;
+    if (8 % p.grid_y == 0) {
+      q.xcd_remap = 1;
+      grid = dim3((p.n_items * p.grid_y + 7) / 8 * 8, 1);
+    }
+    return dqk == 128 ? launch_prefill_flat<128, P>(q, bm, grid, stream) : launch_prefill_flat<64, P>(q, bm, grid, stream);
+  }
   if (dqk == 128 || dqk == 64) {
     // XCD-aware 1-D grid when the column count divides 8 (see rowpar_kernel).
     AttnParams q = p;

@@ -108,14 +108,14 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
   const int64_t granule = o.split_granule ? o.split_granule : 32;
-  const int32_t bm = o.bm ? o.bm : (latent || split ? 128 : 32);
+  int32_t bm = o.bm ? o.bm : (latent || split ? 128 : 0);   // grouped-query default: chosen below
   if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
   if (o.cus_decode < -1 || o.cus_decode > cus_total)
     return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
-  if (latent ? (bm != 64 && bm != 128) : split ? bm != 128 : (bm != 16 && bm != 32))
+  if (latent ? (bm != 64 && bm != 128) : split ? bm != 128 : (bm != 0 && bm != 16 && bm != 32 && bm != 128))
     return set_error(FLEX_ERR_UNSUPPORTED,
-                     "bm must be 16 or 32 (grouped-query), 64 or 128 (latent layout), 128 (192/128 layout)");
+                     "bm must be 16, 32 or 128 (grouped-query), 64 or 128 (latent layout), 128 (192/128 layout)");
   if (max_pages_per_seq < 0) return set_error(FLEX_ERR_INVALID_ARG, "max_pages_per_seq < 0");
   if (num_seqs > 0 && qsl[0] != 0) return set_error(FLEX_ERR_INVALID_ARG, "query_start_loc[0] != 0");
 
@@ -141,7 +141,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   // Prefill work-groups per tile: one per query head (latent layout), or one per
   // KV head and group of up to 8 of its query heads (grouped-query layout).
   const int32_t G = sh.num_q_heads / sh.num_kv_heads;
-  const int32_t pre_grid_y = latent || split ? sh.num_q_heads : sh.num_kv_heads * ((G + 7) / 8);
+
   const int32_t rows_per_wg = latent ? latent_rows : heads_per_wg * (sh.num_q_heads / sh.num_kv_heads);
   std::vector<int32_t> dec, pre;
   for (int32_t s = 0; s < num_seqs; ++s) {
@@ -184,6 +184,21 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   }
   const int64_t cus_prefill =
       (!dec.empty() && !pre.empty() && cus_decode < cus_total) ? cus_total - cus_decode : cus_total;
+
+  // Grouped-query prefill tiles: 128 flattened rows (a row is a (token,
+  // query head) pair of one KV head, token-major: every 16-row block of a
+  // wave is full whatever the group size) when the batch gives every
+  // prefill CU at least four such work-groups; else 32 tokens, whose larger
+  // work-groups fill a CU one at a time and leave no ragged last round on
+  // small batches.
+  if (bm == 0) {
+    int64_t flat_wgs = 0;
+    for (int32_t s : pre) flat_wgs += cdiv(int64_t(qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads;
+    bm = flat_wgs >= 4 * cus_prefill ? 128 : 32;
+  }
+  const bool flat = !latent && !split && bm == 128;
+  const int32_t pre_grid_y =
+      latent || split ? sh.num_q_heads : flat ? sh.num_kv_heads : sh.num_kv_heads * ((G + 7) / 8);
 
   // Decode partition (balanced split-K): the pages of all decode sequences,
   // concatenated in batch order, are cut into R near-equal ranges, one
@@ -235,14 +250,19 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   }
   const int32_t n_dec_items = int32_t(pieces.size());
 
-  // Prefill tiles of bm rows, the longest causal key range first.
+  // Prefill tiles of bm rows, the longest causal key range first. A row is
+  // a token, or with flat tiles a (token, query head) pair of one KV head,
+  // r = token * G + head; a tile's key range ends at the causal limit of its
+  // last row's token.
   struct Tile { int32_t s, t, r0, r1, kend; };
   std::vector<Tile> tiles;
   for (int32_t s : pre) {
     const int32_t n = qsl[s + 1] - qsl[s], L = seq_lens[s];
-    for (int32_t t = 0; int64_t(t) * bm < n; ++t) {
-      const int32_t r0 = t * bm, r1 = std::min(n, (t + 1) * bm);
-      tiles.push_back({s, t, r0, r1, L - n + r1});
+    const int64_t rows = flat ? int64_t(n) * G : n;
+    if (rows > INT32_MAX) return set_error(FLEX_ERR_INVALID_ARG, "prefill chunk too long for flat row tiles");
+    for (int32_t t = 0; int64_t(t) * bm < rows; ++t) {
+      const int32_t r0 = t * bm, r1 = int32_t(std::min<int64_t>(rows, int64_t(t + 1) * bm));
+      tiles.push_back({s, t, r0, r1, L - n + (flat ? (r1 - 1) / G + 1 : r1)});
     }
   }
   std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& a, const Tile& b) {

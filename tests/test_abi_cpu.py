@@ -100,8 +100,9 @@ def test_plan_matches_rederivation_fuzz():
         maxp = max([1] + [-(-L // P) for L in ls]) + rng.randint(0, 3)
         opts = OP.Opts(cus_decode=rng.choice([0, 64, 192, -1]), max_splits=rng.choice([0, 1, 3]),
                        wg_per_cu=rng.choice([0, 2]), min_split_tokens=rng.choice([0, 16, 1000]),
-                       bm=rng.choice([0, 16]) if sh.head_dim_qk != 576 else rng.choice([0, 64]),
-                       cus_total=rng.choice([0, 256, 240]),
+                       bm=(rng.choice([0, 0, 16, 32, 128]) if sh.head_dim_qk in (64, 128)
+                           else rng.choice([0, 64]) if sh.head_dim_qk == 576 else rng.choice([0, 128])),
+                       cus_total=rng.choice([0, 256, 240, 16]),
                        hbm_gbps=rng.choice([0.0, 5000.0]), decode_gbps_per_cu=rng.choice([0.0, 25.0]))
         compare(sh, opts, qsl, ls, maxp)
 

@@ -94,18 +94,28 @@ def check_invariants(sh, opts, qsl, ls, maxp):
             assert k0 == pos and k1 > k0 and k0 % P == 0
             pos = k1
         assert pos == ls[s]
-    # prefill tiles tile [0, n) and carry the causal key end
+    # prefill tiles tile [0, n) (flat tiles: [0, n * G), rows being (token, query
+    # head) pairs) and carry the causal key end of their last row's token
     bm = b[14]
+    G = sh.num_q_heads // sh.num_kv_heads
+    flat = sh.head_dim_qk in (64, 128) and bm == 128
+    if sh.head_dim_qk in (64, 128) and not (o.bm or 0):   # default tile height
+        flat_wgs = sum(-(-(qsl[s + 1] - qsl[s]) * G // 128) * sh.num_kv_heads for s in pre)
+        assert bm == (128 if flat_wgs >= 4 * b[13] else 32)
+    assert b[8] == (sh.num_kv_heads if flat else b[8])
     rows = {}
     for it in pre_items:
         s, t, r0, r1, kend = it[:5]
         n, L = qsl[s + 1] - qsl[s], ls[s]
-        assert r0 == t * bm and r1 == min(n, (t + 1) * bm) and kend == L - n + r1
+        nrows = n * G if flat else n
+        last_token = (r1 - 1) // G if flat else r1 - 1
+        assert r0 == t * bm and r1 == min(nrows, (t + 1) * bm) and kend == L - n + last_token + 1
         rows.setdefault(s, []).append((r0, r1))
     assert sorted(rows) == pre
     for s, rr in rows.items():
         rr.sort()
-        assert rr[0][0] == 0 and rr[-1][1] == qsl[s + 1] - qsl[s]
+        n = qsl[s + 1] - qsl[s]
+        assert rr[0][0] == 0 and rr[-1][1] == (n * G if flat else n)
         assert all(a[1] == b_[0] for a, b_ in zip(rr, rr[1:]))
     kends = [it[4] for it in pre_items]
     assert kends == sorted(kends, reverse=True)
@@ -154,8 +164,11 @@ def test_fuzz_invariants():
         if sh.num_q_heads % sh.num_kv_heads or sh.num_q_heads // sh.num_kv_heads > 16:
             continue
         qsl, ls, maxp = random_batch(rng, sh.page_size, rng.randint(0, 40), rng.randint(0, 4))
-        opts = OP.Opts(cus_decode=rng.choice([0, 64, 128, -1]), max_splits=rng.choice([0, 2, 8]),
-                       wg_per_cu=rng.choice([0, 1, 8]))
+        cus_total = rng.choice([0, 0, 16])
+        opts = OP.Opts(cus_decode=rng.choice([0, 8, -1] if cus_total else [0, 64, 128, -1]),
+                       max_splits=rng.choice([0, 2, 8]), wg_per_cu=rng.choice([0, 1, 8]),
+                       bm=0 if mla else rng.choice([0, 0, 16, 32, 128]), cus_total=cus_total,
+                       split_granule=8 if cus_total else 0)
         check_invariants(sh, opts, qsl, ls, maxp)
 
 
