@@ -233,6 +233,27 @@ int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, 
 int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode,
                     void* stream, flex_attn_corun_t* corun);
 
+/* Allocation-free form of flex_attn_mixed, for callers that cannot allocate
+ * device memory or let a library call do so: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation. Same arguments,
+ * modes, kernels and results (bit-identical to flex_attn_mixed for the same
+ * plan and inputs), except that the decode phase's split-K partials go to a
+ * fixed scratch array the library holds in device memory (one per device it
+ * runs on, kept until the process ends) instead of args->workspace, whose two
+ * fields are ignored. The call itself allocates nothing.
+ * Limit: the plan's workspace_bytes must not exceed
+ * flex_attn_static_scratch_bytes() (32 MiB), else FLEX_ERR_WORKSPACE with the
+ * sizes in flex_attn_last_error(). The scratch needs no initialisation and
+ * keeps the last call's contents. Every call on one device shares that
+ * device's scratch: two calls whose work can overlap on one GPU (different
+ * streams, or a co-run step still running) race; issue them in order on one
+ * stream. The first call on a device resolves the scratch address
+ * (hipGetSymbolAddress); a failure there is FLEX_ERR_HIP. */
+int flex_attn_mixed_static(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode,
+                           void* stream, flex_attn_corun_t* corun);
+/* Bytes of the allocation-free call's scratch array. */
+size_t flex_attn_static_scratch_bytes(void);
+
 /* Create two streams on the current device, restricted by CU masks to
  * cus_prefill and cus_decode compute units (disjoint; each eighth of the
  * device holds one CU of every shader engine of every XCD, so any split keeps

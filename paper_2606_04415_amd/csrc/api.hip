@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -46,8 +47,10 @@ int hip_fail(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Checks shared by every run call; fills the kernel parameter block.
-int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p) {
+// Checks shared by every run call; fills the kernel parameter block. A
+// non-NULL ws_override (of at least the plan's workspace_bytes) replaces the
+// caller's workspace, whose fields are then ignored.
+int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p, void* ws_override = nullptr) {
   if (!plan || !a) return set_error(FLEX_ERR_INVALID_ARG, "plan or args is NULL");
   const flex_attn_shape& sh = plan->shape;
   const flex_attn_plan_info& info = plan->info;
@@ -76,7 +79,7 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
   if (a->block_table_stride < 1) return set_error(FLEX_ERR_INVALID_ARG, "block_table_stride < 1");
   if (a->d_plan_bytes < info.device_plan_bytes)
     return set_error(FLEX_ERR_WORKSPACE, "d_plan_bytes smaller than the plan's device_plan_bytes");
-  if (info.workspace_bytes > 0) {
+  if (info.workspace_bytes > 0 && !ws_override) {
     if (!a->workspace) return set_error(FLEX_ERR_INVALID_ARG, "workspace is NULL");
     if (!aligned16(a->workspace)) return set_error(FLEX_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
     if (a->workspace_bytes < info.workspace_bytes)
@@ -100,7 +103,7 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
   if (info.workspace_bytes > 0) {
     const int32_t W = info.decode_wg_width;
     const size_t stats = size_t(info.n_decode_items) * W * plan->rows_per_wg * 2 * 4;
-    char* ws = static_cast<char*>(a->workspace);
+    char* ws = static_cast<char*>(ws_override ? ws_override : a->workspace);
     p->ws_stats = reinterpret_cast<float*>(ws);
     p->ws_o = reinterpret_cast<float*>(ws + ((stats + 255) / 256) * 256);
   }
@@ -232,13 +235,14 @@ extern "C" int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_a
   return run_prefill(plan, p, args, static_cast<hipStream_t>(stream));
 }
 
-extern "C" int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode, void* stream,
-                               flex_attn_corun_t* corun) {
-  clear_error();
+namespace {
+
+int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode, void* stream,
+              flex_attn_corun_t* corun, void* ws_override) {
   if (mode != FLEX_MODE_SERIAL && mode != FLEX_MODE_CORUN && mode != FLEX_MODE_FUSED)
     return set_error(FLEX_ERR_INVALID_ARG, "unknown mode");
   AttnParams p;
-  int st = prepare(plan, args, &p);
+  int st = prepare(plan, args, &p, ws_override);
   if (st != FLEX_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (mode == FLEX_MODE_FUSED) return run_fused(plan, p, args, s);
@@ -284,6 +288,59 @@ extern "C" int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_arg
     return hip_fail(e, "join wait");
   return FLEX_OK;
 }
+
+// Scratch of the allocation-free entry point: split-K partials of the
+// decode phase, one array per device the library runs on (each device holds
+// its own copy at its own address), resolved once per device with
+// hipGetSymbolAddress. Host code uses only the resolved address: the array's
+// name is a host-side stand-in, not a device address.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return set_error(FLEX_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch))) != hipSuccess)
+      return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return FLEX_OK;
+}
+
+}  // namespace
+
+extern "C" int flex_attn_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode, void* stream,
+                               flex_attn_corun_t* corun) {
+  clear_error();
+  return run_mixed(plan, args, mode, stream, corun, nullptr);
+}
+
+extern "C" int flex_attn_mixed_static(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode,
+                                      void* stream, flex_attn_corun_t* corun) {
+  clear_error();
+  if (!plan || !args) return set_error(FLEX_ERR_INVALID_ARG, "plan or args is NULL");
+  if (plan->info.workspace_bytes > kStaticScratchBytes)
+    return set_error(FLEX_ERR_WORKSPACE, "the plan needs " + std::to_string(plan->info.workspace_bytes) +
+                                             " bytes of split-K scratch; the allocation-free call holds " +
+                                             std::to_string(kStaticScratchBytes));
+  void* ws = nullptr;
+  if (plan->info.workspace_bytes > 0) {
+    const int st = static_scratch(&ws);
+    if (st != FLEX_OK) return st;
+  }
+  return run_mixed(plan, args, mode, stream, corun, ws);
+}
+
+extern "C" size_t flex_attn_static_scratch_bytes(void) { return kStaticScratchBytes; }
 
 extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, flex_attn_corun_t** out) {
   clear_error();

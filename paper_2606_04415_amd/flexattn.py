@@ -32,6 +32,7 @@ EXPORTED = [
     "flex_attn_prefill", "flex_attn_mixed", "flex_attn_corun_create", "flex_attn_corun_destroy",
     "flex_attn_corun_streams", "flex_attn_corun_set_timing", "flex_attn_corun_timing_read",
     "flex_attn_debug_gather", "flex_attn_workspace_init", "flex_attn_kv_append",
+    "flex_attn_mixed_static", "flex_attn_static_scratch_bytes",
     "flex_ctl_create", "flex_ctl_destroy", "flex_ctl_set_profile", "flex_ctl_observe", "flex_ctl_decide",
     "flex_ctl_estimates", "flex_ts_create", "flex_ts_destroy", "flex_ts_next", "flex_ts_observe", "flex_ts_totals",
 ]
@@ -158,6 +159,9 @@ def lib():
     for f in ("flex_attn_decode", "flex_attn_prefill"):
         getattr(L, f).argtypes = [vp, ctypes.POINTER(Args), vp]
     L.flex_attn_mixed.argtypes = [vp, ctypes.POINTER(Args), ctypes.c_int, vp, vp]
+    L.flex_attn_mixed_static.argtypes = [vp, ctypes.POINTER(Args), ctypes.c_int, vp, vp]
+    L.flex_attn_static_scratch_bytes.argtypes = []
+    L.flex_attn_static_scratch_bytes.restype = ctypes.c_size_t
     L.flex_attn_corun_create.argtypes = [i32, i32, ctypes.POINTER(vp)]
     L.flex_attn_corun_destroy.argtypes = [vp]
     L.flex_attn_corun_destroy.restype = None
@@ -184,7 +188,8 @@ def lib():
     L.flex_ts_totals.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     for f in EXPORTED:
         if f not in ("flex_attn_status_string", "flex_attn_last_error", "flex_attn_plan_destroy",
-                     "flex_attn_corun_destroy", "flex_ctl_destroy", "flex_ts_destroy"):
+                     "flex_attn_corun_destroy", "flex_ctl_destroy", "flex_ts_destroy",
+                     "flex_attn_static_scratch_bytes"):
             getattr(L, f).restype = ctypes.c_int
     _lib = L
     return L
@@ -332,6 +337,17 @@ def flex_attn_mixed(plan: Plan, args: Args, mode: int, stream=None, corun: "Coru
     s = stream if stream is not None else current_stream()
     check(lib().flex_attn_mixed(plan.handle, ctypes.byref(args), mode, s,
                                 corun.handle if corun is not None else None), "flex_attn_mixed")
+
+
+def flex_attn_mixed_static(plan: Plan, args: Args, mode: int, stream=None, corun: "Corun" = None):
+    """flex_attn_mixed with the split-K partials in the library's fixed scratch (allocates nothing)."""
+    s = stream if stream is not None else current_stream()
+    check(lib().flex_attn_mixed_static(plan.handle, ctypes.byref(args), mode, s,
+                                       corun.handle if corun is not None else None), "flex_attn_mixed_static")
+
+
+def static_scratch_bytes() -> int:
+    return int(lib().flex_attn_static_scratch_bytes())
 
 
 def flex_attn_debug_gather(plan: Plan, args: Args, seq: int, seq_len: int, k_out, v_out=None, stream=None):
