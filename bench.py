@@ -1,30 +1,38 @@
 #!/usr/bin/env python3
-"""Benchmark one mixed prefill/decode attention step on one MI355X.
+"""Benchmark one mixed prefill/decode attention step on one MI355X, plus the
+single-phase workloads, each against its roofline.
 
 A step is one pass of the whole path over one synthetic batch: the plan
 (built once, outside the timed region, like the paper's off-path policy
 plane), the prefill kernel and the decode kernel with its split merge, run
-either co-located on two CU-masked streams (the default, the paper's dynamic
-co-location analog) or serially; a third leg times the one-launch form, in
-which one grid holds both phases' work-groups (fused_us). Inputs are
-resident in HBM before timing;
-the KV cache is rotated over several copies so the 256 MB Infinity Cache
-cannot serve repeated steps.
+co-located on two CU-masked streams (the headline, the paper's dynamic
+co-location analog), serially on one stream, or as one launch holding both
+phases' work-groups. Inputs are resident in HBM before timing; KV caches
+that the 256 MB Infinity Cache could hold are rotated over several copies.
 
-Default workload: the Qwen2.5-7B-shaped mixed step (one 2048-token chunk on
+Headline workload: the Qwen2.5-7B-shaped mixed step (one 2048-token chunk on
 4096 cached tokens plus 128 decodes with context U[1024, 8192], GQA 28/4,
-head_dim 128, page 16). Prints one JSON line on stdout.
+head_dim 128, page 16). Also timed: the 64-sequence decode batch (decode
+GB/s), the 8 x 2048 causal prefill (prefill TFLOP/s) and the absorbed-MLA
+step (decode, prefill, serial step). Prints one JSON line on stdout.
 
-Each mode runs W warm-up steps, K timed steps (the step time: HIP events on
-the issuing stream around the K steps), then K more steps with HIP events
-around each phase's kernel on the stream it runs on (the phase durations and
-the roofline's kernel duration), kept apart because recording those events
-adds about 10 us to a step.
+Protocol. The device raises its clock over the first ~100-200 MFMA-heavy
+launches after it has been idle (prefill 219 -> 181 us; again after one
+second idle); decode is flat. So the setup runs untimed steps of every leg
+until about `--settle-ms` of work has passed ("settle" in the line), after
+the W warm-up steps; the K co-run steps right after the warm-up, before the
+settle, are reported as `cold_corun_us`. The legs are then timed
+interleaved: blocks of steps of each mode in rotating order, an event after
+every step (p10/p50/p90 from those), each block bracketed by
+synchronisations; `value` is the co-run blocks' time over K. A second pass
+with HIP events around each phase's kernel (on the stream it runs on) gives
+the phase durations for the roofline.
 """
 from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -36,6 +44,42 @@ BF16_PEAK_TFLOPS = 2516.6   # 256 CUs x 2.4 GHz x 4096 dense bf16 flop/clk
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def pct(xs, q):
+    ys = sorted(xs)
+    if not ys:
+        return None
+    k = (len(ys) - 1) * q
+    lo, hi = math.floor(k), math.ceil(k)
+    return ys[lo] + (ys[hi] - ys[lo]) * (k - lo)
+
+
+def dist(us):
+    return {"mean": round(sum(us) / len(us), 2), "p10": round(pct(us, 0.1), 2), "p50": round(pct(us, 0.5), 2),
+            "p90": round(pct(us, 0.9), 2), "n": len(us)}
+
+
+def host_info():
+    info = {"cpu_count": os.cpu_count()}
+    try:
+        info["affinity"] = len(os.sched_getaffinity(0))
+    except Exception:
+        info["affinity"] = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        info["blas_threads"] = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
+    except Exception:
+        info["blas_threads"] = None
+    return info
 
 
 def cpu_baseline(b, seconds_target=15.0):
@@ -86,12 +130,9 @@ def cpu_baseline(b, seconds_target=15.0):
         est += t_dec * keys_dec_all / keys_dec_sample
     if keys_pre_sample:
         est += t_pre * keys_pre_all / keys_pre_sample
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
-    except Exception:
-        cores = os.cpu_count() or 1
-    return {"value": est * 1e6, "unit": "us", "cores": cores, "kind": "oracle",
+    hi = host_info()
+    cores = hi.get("blas_threads") or hi.get("affinity") or os.cpu_count() or 1
+    return {"value": est * 1e6, "unit": "us", "cores": cores, "kind": "oracle", "host": hi,
             "sample": f"{n_dec_sample} of {len(dec)} decode sequences ({keys_dec_sample} keys) + "
                       f"{n_pre_rows} prefill query rows x {w.num_q_heads} heads ({keys_pre_sample} causal keys); "
                       f"{t_dec + t_pre:.1f} s of fp64 numpy, scaled by causal key count to the whole step",
@@ -161,18 +202,107 @@ def time_kv_append(b, kv, shape, steps, stream):
     return {"tokens": int(sm.numel()), "us": round(us, 2), "GBps": round(nbytes / (us * 1e-6) / 1e9, 1)}
 
 
+def launch_timer(stream, fn, n, settle_ms, warmup):
+    """Settle, then time n launches back to back with an event after each
+    (per-launch microseconds)."""
+    import torch
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    i = 0
+    while time.perf_counter() - t0 < settle_ms * 1e-3:
+        for _ in range(10):
+            fn(i)
+            i += 1
+        torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record(stream)
+    for j in range(n):
+        fn(j)
+        ev[j + 1].record(stream)
+    torch.cuda.synchronize()
+    return [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)], i
+
+
+def roof(bound, achieved, unit):
+    peak = HBM_PEAK_GBPS if bound == "hbm" else BF16_PEAK_TFLOPS
+    return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit, "frac": round(achieved / peak, 4)}
+
+
+def bench_config(name, steps, warmup, settle_ms, pools):
+    """Single-phase workloads and the latent step, on all CUs, plans with
+    library defaults; per-launch times and roofline fractions."""
+    import torch
+    from paper_2606_04415_amd import flexattn as F
+    from paper_2606_04415_amd.workloads import WORKLOADS, algorithmic_work, make_batch
+    w = WORKLOADS[name]
+    b = make_batch(w, seed=0, poison=False, device="cuda")
+    work = algorithmic_work(w, b.extra["ns"], b.extra["ls"])
+    dev = torch.device("cuda:0")
+    kv = [(b.k_cache, b.v_cache)] + [(b.k_cache.clone(), None if b.v_cache is None else b.v_cache.clone())
+                                     for _ in range(pools - 1)]
+    bt, sl, qsl = b.block_table.to(dev), b.seq_lens.to(dev), b.query_start_loc.to(dev)
+    shape = F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v, w.page_size,
+                         w.sm_scale, w.v_aliases_k)
+    pa = F.PagedAttention(shape, None, b.query_start_loc.tolist(), b.seq_lens.tolist(), b.block_table.shape[1])
+    out, _ = pa.alloc_out(b.q)
+    args = [pa.args(b.q, k, v, bt, sl, qsl, out) for k, v in kv]
+    st = torch.cuda.Stream()
+    cs = st.cuda_stream
+    res = {"workload": f"{w.name}: {w.description}", "kv_pools": pools, "bm": pa.plan.info["bm"],
+           "inputs": "q/k/v drawn on the device (seeded), ~N(0,1) in bf16"}
+    dec_b, pre_f = work["decode"]["bytes"], work["prefill"]["flops"]
+    legs = []
+    if dec_b:
+        legs.append(("decode", lambda i: F.flex_attn_decode(pa.plan, args[i % len(args)], stream=cs)))
+    if pre_f:
+        legs.append(("prefill", lambda i: F.flex_attn_prefill(pa.plan, args[i % len(args)], stream=cs)))
+    if dec_b and pre_f:
+        legs.append(("serial_step", lambda i: F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_SERIAL,
+                                                                stream=cs)))
+    for leg, fn in legs:
+        us, settled = launch_timer(st, fn, steps, settle_ms, warmup)
+        d = dist(us)
+        r = {"us": d, "settle_launches": settled}
+        if leg == "decode":
+            r["GBps"] = round(dec_b / (d["mean"] * 1e-6) / 1e9, 1)
+            r["roofline"] = roof("hbm", r["GBps"], "GB/s")
+            r["algorithmic_bytes"] = dec_b
+            if w.head_dim_qk == 576:   # latent decode sits near the ridge: its MFMA side too
+                fl = work["decode"]["flops"]
+                r["TFLOPs"] = round(fl / (d["mean"] * 1e-6) / 1e12, 1)
+                r["bound_us"] = round(max(dec_b / (HBM_PEAK_GBPS * 1e3), fl / (BF16_PEAK_TFLOPS * 1e6)), 1)
+        elif leg == "prefill":
+            r["TFLOPs"] = round(pre_f / (d["mean"] * 1e-6) / 1e12, 1)
+            r["roofline"] = roof("mfma", r["TFLOPs"], "TFLOP/s")
+            r["algorithmic_flops"] = pre_f
+        else:
+            r["bound_us"] = round(max((dec_b + work["prefill"]["bytes"]) / (HBM_PEAK_GBPS * 1e3),
+                                      (pre_f + work["decode"]["flops"]) / (BF16_PEAK_TFLOPS * 1e6)), 1)
+            r["frac_of_bound"] = round(r["bound_us"] / d["mean"], 4)
+        res[leg] = r
+        log(f"{name} {leg}: {d['mean']:.1f} us (p10 {d['p10']:.1f}, p90 {d['p90']:.1f})")
+    del kv, args, b
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=200,
-                    help="untimed steps first: the first passes over the rotated KV copies pay for TLB and clock warm-up")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle-ms", type=float, default=400.0,
+                    help="untimed steps of every leg after the warm-up, until this much time has passed")
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--split", default="128:128", help="prefill:decode CUs for co-run")
     ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over steps")
     ap.add_argument("--bm", type=int, default=0, help="prefill rows per tile (0: library default)")
+    ap.add_argument("--blocks", type=int, default=5, help="interleaved timing blocks per leg")
     ap.add_argument("--no-serial", action="store_true", help="skip the serial comparison leg")
     ap.add_argument("--no-fused", action="store_true", help="skip the one-launch (fused) comparison leg")
+    ap.add_argument("--no-configs", action="store_true", help="skip the single-phase and latent workloads")
     ap.add_argument("--fused-wg-per-cu", type=int, default=2,
                     help="decode work-groups per CU the fused leg's plan partitions for")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -185,6 +315,9 @@ def main():
                     help="only issue the co-run plan's phases one after the other, untimed: the launches a "
                          "co-run step makes, for counter collection (which serialises dispatches and so "
                          "cannot pass the co-run streams' value waits)")
+    ap.add_argument("--config-pass", default="",
+                    help="only issue warmup + steps serial steps of this workload (library defaults), untimed "
+                         "(for kernel tracing and counters of the single-phase and latent workloads)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -200,6 +333,24 @@ def main():
     import torch
     from paper_2606_04415_amd import flexattn as F
     from paper_2606_04415_amd.workloads import WORKLOADS, algorithmic_work, make_batch
+
+    if args.config_pass:
+        w = WORKLOADS[args.config_pass]
+        b = make_batch(w, seed=0, poison=False, device="cuda")
+        dev = torch.device("cuda:0")
+        bt, sl, qsl = b.block_table.to(dev), b.seq_lens.to(dev), b.query_start_loc.to(dev)
+        shape = F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v, w.page_size,
+                             w.sm_scale, w.v_aliases_k)
+        pa = F.PagedAttention(shape, F.make_opts(bm=args.bm), b.query_start_loc.tolist(), b.seq_lens.tolist(),
+                              b.block_table.shape[1])
+        out, _ = pa.alloc_out(b.q)
+        a = pa.args(b.q, b.k_cache, b.v_cache, bt, sl, qsl, out)
+        for i in range(args.warmup + args.steps):
+            F.flex_attn_mixed(pa.plan, a, F.FLEX_MODE_SERIAL)
+        torch.cuda.synchronize()
+        print(json.dumps({"config_pass": args.config_pass, "steps": args.warmup + args.steps,
+                          "bm": pa.plan.info["bm"]}), flush=True)
+        return
 
     w = WORKLOADS[args.workload]
     log(f"drawing workload '{w.name}': {w.description}")
@@ -220,119 +371,126 @@ def main():
     cp, cd = (int(x) for x in args.split.split(":"))
     shape = F.make_shape(w.num_q_heads, w.num_kv_heads, w.head_dim_qk, w.head_dim_v, w.page_size,
                          w.sm_scale, w.v_aliases_k)
-    t0 = time.perf_counter()
-    pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd, bm=args.bm), b.query_start_loc.tolist(), b.seq_lens.tolist(),
-                          b.block_table.shape[1])
-    plan_us = (time.perf_counter() - t0) * 1e6
-    info = pa.plan.info
-    out, lse = pa.alloc_out(q)
-    arglist = [pa.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+    plan_us = []
+    def plan(**kw):
+        t0 = time.perf_counter()
+        pa = F.PagedAttention(shape, F.make_opts(bm=args.bm, **kw), b.query_start_loc.tolist(), b.seq_lens.tolist(),
+                              b.block_table.shape[1])
+        plan_us.append((time.perf_counter() - t0) * 1e6)
+        return pa
+    pa_c = plan(cus_decode=cd)
+    pa_s = plan(cus_decode=0)
+    pa_f = plan(cus_decode=0, wg_per_cu=args.fused_wg_per_cu)
+    out, lse = pa_c.alloc_out(q)
+    arg_c = [pa_c.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+    arg_s = [pa_s.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+    arg_f = [pa_f.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
     corun = F.Corun(cp, cd)
+    info = pa_c.plan.info
     log(f"plan: {info['n_decode_items']} decode items x {info['decode_wg_width']}, "
-        f"{info['n_prefill_items']} prefill tiles x {info['prefill_grid_y']}; co-run {cp}/{cd} CUs")
+        f"{info['n_prefill_items']} prefill tiles x {info['prefill_grid_y']} (bm {info['bm']}); co-run {cp}/{cd} CUs")
 
     # The caller issues steps on a stream of its own: HIP's legacy default
-    # stream synchronizes implicitly with the co-run pair's streams, which
-    # would hold the host at every step.
+    # stream synchronizes implicitly with the co-run pair's streams.
     caller = torch.cuda.Stream()
-
-    def timed(mode, steps, warmup):
-        """K timed steps with nothing but the step in the stream (the step time),
-        then K more with HIP events around each phase's kernel on the stream it
-        runs on (the phase and kernel durations): recording those events costs
-        about 10 us per step, so they stay out of the step time."""
-        corun.set_timing(False)
-        for i in range(warmup):
-            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t_wall = time.perf_counter()
-        e0.record(caller)
-        for i in range(steps):
-            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
-        e1.record(caller)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t_wall
-        ms = e0.elapsed_time(e1) / steps
-        corun.set_timing(True)
-        for i in range(steps):
-            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], mode, stream=caller.cuda_stream, corun=corun)
-        torch.cuda.synchronize()
-        pre, dec = corun.timing_read()
-        corun.set_timing(False)
-        return ms, wall, sum(pre) / len(pre), sum(dec) / len(dec)
+    cs = caller.cuda_stream
+    step = {
+        "corun": lambda i: F.flex_attn_mixed(pa_c.plan, arg_c[i % len(arg_c)], F.FLEX_MODE_CORUN, stream=cs,
+                                             corun=corun),
+        "serial": lambda i: F.flex_attn_mixed(pa_s.plan, arg_s[i % len(arg_s)], F.FLEX_MODE_SERIAL, stream=cs),
+        "fused": lambda i: F.flex_attn_mixed(pa_f.plan, arg_f[i % len(arg_f)], F.FLEX_MODE_FUSED, stream=cs),
+    }
+    legs = ["corun"] + ([] if args.no_serial else ["serial"]) + \
+           ([] if args.no_fused or pa_f.plan.info["n_fused_wgs"] == 0 else ["fused"])
 
     if args.counter_pass:
         for i in range(args.warmup + args.steps):
-            F.flex_attn_mixed(pa.plan, arglist[i % len(arglist)], F.FLEX_MODE_SERIAL, stream=caller.cuda_stream)
+            F.flex_attn_mixed(pa_c.plan, arg_c[i % len(arg_c)], F.FLEX_MODE_SERIAL, stream=cs)
         torch.cuda.synchronize()
         corun.close()
         print(json.dumps({"counter_pass": True, "steps": args.warmup + args.steps, "cus_decode_plan": cd}), flush=True)
         return
-
     if args.fused_pass:
-        pa_f = F.PagedAttention(shape, F.make_opts(cus_decode=0, bm=args.bm, wg_per_cu=args.fused_wg_per_cu),
-                                b.query_start_loc.tolist(), b.seq_lens.tolist(), b.block_table.shape[1])
-        fargs = [pa_f.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
         for i in range(args.warmup + args.steps):
-            F.flex_attn_mixed(pa_f.plan, fargs[i % len(fargs)], F.FLEX_MODE_FUSED, stream=caller.cuda_stream)
+            step["fused"](i)
         torch.cuda.synchronize()
         corun.close()
         print(json.dumps({"fused_pass": True, "steps": args.warmup + args.steps,
                           "fused_wgs": pa_f.plan.info["n_fused_wgs"]}), flush=True)
         return
 
-    log(f"co-run: {args.warmup} warmup + {args.steps} timed steps")
-    c_ms, c_wall, c_pre, c_dec = timed(F.FLEX_MODE_CORUN, args.steps, args.warmup)
-    log(f"co-run step {c_ms * 1e3:.1f} us (prefill {c_pre * 1e3:.1f} us, decode {c_dec * 1e3:.1f} us)")
-    s_ms = s_pre = s_dec = None
-    if not args.no_serial:
-        # serial leg: the same batch planned for the whole device
-        pa_s = F.PagedAttention(shape, F.make_opts(cus_decode=0, bm=args.bm), b.query_start_loc.tolist(),
-                                b.seq_lens.tolist(), b.block_table.shape[1])
-        arglist = [pa_s.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
-        pa = pa_s
-        s_ms, _, s_pre, s_dec = timed(F.FLEX_MODE_SERIAL, args.steps, args.warmup)
-        log(f"serial step {s_ms * 1e3:.1f} us (prefill {s_pre * 1e3:.1f} us, decode {s_dec * 1e3:.1f} us)")
+    def block(mode, n, start):
+        """n steps of one mode back to back; per-step times and the block's time (us)."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(caller)
+        for j in range(n):
+            step[mode](start + j)
+            ev[j + 1].record(caller)
+        torch.cuda.synchronize()
+        return [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)], ev[0].elapsed_time(ev[n]) * 1e3
+
+    # W warm-up steps, then K co-run steps before settling (the cold figure)
+    log(f"warm-up: {args.warmup} steps; cold co-run: {args.steps} steps")
+    for i in range(args.warmup):
+        step["corun"](i)
+    _, cold_total = block("corun", args.steps, args.warmup)
+    # settle: rotate the legs until settle_ms have passed
+    t0 = time.perf_counter()
+    n_settle = 0
+    while time.perf_counter() - t0 < args.settle_ms * 1e-3:
+        for mode in legs:
+            for _ in range(5):
+                step[mode](n_settle)
+                n_settle += 1
+        torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t0) * 1e3
+    log(f"settle: {n_settle} steps in {settle_ms:.0f} ms; timing {args.steps} steps per leg in "
+        f"{args.blocks} interleaved blocks")
+    per = {m: [] for m in legs}
+    total = {m: 0.0 for m in legs}
+    nb = max(1, min(args.blocks, args.steps))
+    sizes = [args.steps // nb + (1 if r < args.steps % nb else 0) for r in range(nb)]
+    for r in range(nb):
+        order = legs[r % len(legs):] + legs[:r % len(legs)]
+        for mode in order:
+            us, t = block(mode, sizes[r], r * 1000)
+            per[mode] += us
+            total[mode] += t
+    c_ms = total["corun"] / args.steps / 1e3
+
+    # phase durations (events on each kernel's own stream), a separate pass
+    def phases(mode, pa_, arg_):
+        corun.set_timing(True)
+        for i in range(args.steps):
+            F.flex_attn_mixed(pa_.plan, arg_[i % len(arg_)], mode, stream=cs, corun=corun)
+        torch.cuda.synchronize()
+        pre, dec = corun.timing_read()
+        corun.set_timing(False)
+        return sum(pre) / len(pre), sum(dec) / len(dec), pre, dec
+    c_pre, c_dec, c_pre_l, c_dec_l = phases(F.FLEX_MODE_CORUN, pa_c, arg_c)
+    s_pre = s_dec = None
+    if "serial" in legs:
+        s_pre, s_dec, _, _ = phases(F.FLEX_MODE_SERIAL, pa_s, arg_s)
     corun.close()
-    f_ms = None
-    if not args.no_fused:
-        # fused leg: both phases in one launch, the work-groups interleaved by the plan
-        pa_f = F.PagedAttention(shape, F.make_opts(cus_decode=0, bm=args.bm, wg_per_cu=args.fused_wg_per_cu),
-                                b.query_start_loc.tolist(), b.seq_lens.tolist(), b.block_table.shape[1])
-        if pa_f.plan.info["n_fused_wgs"] > 0:
-            fargs = [pa_f.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
-            for i in range(args.warmup):
-                F.flex_attn_mixed(pa_f.plan, fargs[i % len(fargs)], F.FLEX_MODE_FUSED, stream=caller.cuda_stream)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(caller)
-            for i in range(args.steps):
-                F.flex_attn_mixed(pa_f.plan, fargs[i % len(fargs)], F.FLEX_MODE_FUSED, stream=caller.cuda_stream)
-            e1.record(caller)
-            torch.cuda.synchronize()
-            f_ms = e0.elapsed_time(e1) / args.steps
-            log(f"fused step {f_ms * 1e3:.1f} us ({pa_f.plan.info['n_fused_wgs']} work-groups)")
 
     dec_bytes = work["decode"]["bytes"]
     pre_flops = work["prefill"]["flops"]
-    # dominant kernel: the one with the larger share of the co-run step;
-    # frac_of_cu_share prices it against the peak of the CUs its stream holds
     n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    # dominant kernel: the phase with the larger share of the co-run step
     if dec_bytes and (not pre_flops or c_dec >= c_pre):
         achieved = dec_bytes / (c_dec * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode"),
-                "kernel": "decode_gqa_kernel" if w.head_dim_qk != 576 else "rowpar_kernel (latent decode)",
-                "algorithmic_bytes_per_launch": dec_bytes, "avg_launch_us": round(c_dec * 1e3, 2),
-                "cus": cd}
+        roof_ = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode"),
+                 "kernel": "decode_gqa_kernel" if w.head_dim_qk != 576 else "rowpar_kernel (latent decode)",
+                 "algorithmic_bytes_per_launch": dec_bytes, "avg_launch_us": round(c_dec * 1e3, 2), "cus": cd}
     else:
         achieved = pre_flops / (c_pre * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(w.name, "prefill"),
-                "kernel": "rowpar_kernel (prefill)", "algorithmic_flops_per_launch": pre_flops,
-                "avg_launch_us": round(c_pre * 1e3, 2), "cus": cp,
-                "frac_of_cu_share": round(achieved / (BF16_PEAK_TFLOPS * cp / n_cus), 4)}
+        roof_ = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(w.name, "prefill"),
+                 "kernel": "rowpar_kernel (prefill)", "algorithmic_flops_per_launch": pre_flops,
+                 "avg_launch_us": round(c_pre * 1e3, 2), "cus": cp,
+                 "frac_of_cu_share": round(achieved / (BF16_PEAK_TFLOPS * cp / n_cus), 4)}
 
     result = {
         "metric": METRIC, "value": round(c_ms * 1e3, 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
@@ -340,14 +498,17 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.description}", "batch": len(ls), "query_tokens": sum(ns),
                    "kv_tokens": sum(ls), "mode": "corun", "cus_prefill": cp, "cus_decode": cd,
-                   "kv_pools": len(kv), "plan_host_us": round(plan_us, 1)},
+                   "kv_pools": len(kv), "prefill_bm": info["bm"], "plan_host_us": [round(x, 1) for x in plan_us]},
+        "settle": {"steps": n_settle, "ms": round(settle_ms, 1),
+                   "why": "untimed steps of every leg after the warm-up: the device raises its clock over the first "
+                          "~100-200 MFMA-heavy launches after idle"},
+        "cold_corun_us": round(cold_total / args.steps, 2),
+        "step_us": {m: dist(per[m]) for m in legs},
         "phases_us": {"corun_prefill": round(c_pre * 1e3, 2), "corun_decode": round(c_dec * 1e3, 2)},
-        "roofline": roof,
+        "roofline": roof_,
     }
-    # the other phase of the co-run step against its own peak (HBM is shared
-    # by the whole device, so a bandwidth-bound phase is priced against all of it)
     if dec_bytes and pre_flops:
-        if roof["bound"] == "mfma":
+        if roof_["bound"] == "mfma":
             a = dec_bytes / (c_dec * 1e-3) / 1e9
             result["roofline_other"] = {"bound": "hbm", "kernel": "decode_gqa_kernel + merge_kernel",
                                         "achieved": round(a, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -360,7 +521,8 @@ def main():
                                         "frac": round(a / BF16_PEAK_TFLOPS, 4), "cus": cp,
                                         "frac_of_cu_share": round(a / (BF16_PEAK_TFLOPS * cp / n_cus), 4),
                                         "avg_phase_us": round(c_pre * 1e3, 2)}
-    if s_ms is not None:
+    if "serial" in legs:
+        s_ms = total["serial"] / args.steps / 1e3
         result["serial_us"] = round(s_ms * 1e3, 2)
         result["corun_speedup_vs_serial"] = round(s_ms / c_ms, 4)
         result["phases_us"].update({"serial_prefill": round(s_pre * 1e3, 2), "serial_decode": round(s_dec * 1e3, 2)})
@@ -368,14 +530,23 @@ def main():
             result["decode_GBps_all_cus"] = round(dec_bytes / (s_dec * 1e-3) / 1e9, 1)
         if pre_flops:
             result["prefill_TFLOPs_all_cus"] = round(pre_flops / (s_pre * 1e-3) / 1e12, 2)
-    if f_ms is not None:
+    if "fused" in legs:
+        f_ms = total["fused"] / args.steps / 1e3
         result["fused_us"] = round(f_ms * 1e3, 2)
         result["fused_wg_per_cu"] = args.fused_wg_per_cu
-        if s_ms is not None:
-            result["fused_speedup_vs_serial"] = round(s_ms / f_ms, 4)
+        if "serial" in legs:
+            result["fused_speedup_vs_serial"] = round(total["serial"] / total["fused"], 4)
     result["bound_us"] = round(max((dec_bytes + work["prefill"]["bytes"]) / (HBM_PEAK_GBPS * 1e3),
                                    (pre_flops + work["decode"]["flops"]) / (BF16_PEAK_TFLOPS * 1e6)), 1)
+    result["max_phase_us"] = round(max(c_pre, c_dec) * 1e3, 2)
     result["kv_append"] = time_kv_append(b, kv, shape, args.steps, caller)
+    del kv, arg_c, arg_s, arg_f, q
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        result["configs"] = {}
+        for name, pools in (("decode", 4), ("prefill", 2), ("mla", 1)):
+            log(f"workload '{name}'")
+            result["configs"][name] = bench_config(name, args.steps, args.warmup, args.settle_ms / 2, pools)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)

@@ -152,8 +152,13 @@ def draw_lengths(w: Workload, gen: torch.Generator) -> Tuple[List[int], List[int
 
 def make_batch(w: Workload, seed: int = 0, poison: bool = True,
                ns: Optional[List[int]] = None, ls: Optional[List[int]] = None,
-               num_pages: Optional[int] = None) -> Batch:
-    """Draw one batch of ``w``. ``ns``/``ls`` override the drawn lengths (tests)."""
+               num_pages: Optional[int] = None, device=None) -> Batch:
+    """Draw one batch of ``w``. ``ns``/``ls`` override the drawn lengths (tests).
+
+    With ``device`` (e.g. "cuda"), steps 3-5 of the draw order run on that
+    device with a generator of its own seeded with ``seed``: the same shapes
+    and distributions, other values than the CPU draw, and the tensors stay
+    on the device (the benchmark draws its large workloads this way)."""
     gen = torch.Generator().manual_seed(seed)
     if ns is None or ls is None:
         ns, ls = draw_lengths(w, gen)
@@ -173,11 +178,16 @@ def make_batch(w: Workload, seed: int = 0, poison: bool = True,
         npages_alloc = npages
     perm = torch.randperm(npages, generator=gen)
     T = sum(ns)
-    q = torch.randn((T, w.num_q_heads, w.head_dim_qk), generator=gen).to(torch.bfloat16)
-    k = torch.randn((npages_alloc, P, w.num_kv_heads, w.head_dim_qk), generator=gen).to(torch.bfloat16)
+    tgen, tdev = gen, None
+    if device is not None:
+        tdev = torch.device(device)
+        tgen = torch.Generator(device=tdev).manual_seed(seed)
+    q = torch.randn((T, w.num_q_heads, w.head_dim_qk), generator=tgen, device=tdev).to(torch.bfloat16)
+    k = torch.randn((npages_alloc, P, w.num_kv_heads, w.head_dim_qk), generator=tgen, device=tdev).to(torch.bfloat16)
     v = None
     if not w.v_aliases_k:
-        v = torch.randn((npages_alloc, P, w.num_kv_heads, w.head_dim_v), generator=gen).to(torch.bfloat16)
+        v = torch.randn((npages_alloc, P, w.num_kv_heads, w.head_dim_v), generator=tgen,
+                        device=tdev).to(torch.bfloat16)
 
     max_pages = max([w.max_pages_per_seq] + pages_per_seq)
     bt = torch.empty((B, max_pages), dtype=torch.int32)
