@@ -27,9 +27,11 @@
  *  - Every call returns an int status (FLEX_OK or a negative FLEX_ERR_*);
  *    nothing throws across this boundary. flex_attn_last_error() returns a
  *    thread-local text describing the last failure on the calling thread.
- *  - Device memory is owned by the caller; the library allocates device
- *    memory only for a co-run pair's 24-byte counter buffer. Host plan objects
- *    and co-run pairs are owned by the library until their destroy call.
+ *  - Device memory is owned by the caller; the library never allocates
+ *    device memory (its only device state is fixed module memory: the step
+ *    counters of co-run pairs, the scratch of flex_attn_mixed_static and the
+ *    debug check's status word). Host plan objects and co-run pairs are
+ *    owned by the library until their destroy call.
  *  - Run calls (decode, prefill, mixed, debug gather, workspace init) only
  *    enqueue work on the given HIP stream (a hipStream_t passed as void*;
  *    NULL is the null stream) and return; they never synchronise.
@@ -60,11 +62,17 @@ extern "C" {
 #define FLEX_MODE_FUSED 2   /* one launch holding both phases' work-groups, interleaved */
 
 /* Attention geometry of one layer.
- * Supported: (head_dim_qk, head_dim_v) in {(64,64), (128,128)} with
- * num_q_heads / num_kv_heads <= 16, or (576, 512) with v_aliases_k = 1,
- * num_kv_heads = 1 and num_q_heads a multiple of 64 (absorbed latent attention:
- * the value row of a key is the first 512 columns of its 576-wide key row);
- * page_size in {16, 64}. sm_scale must be finite and > 0. */
+ * Supported:
+ *  - (head_dim_qk, head_dim_v) in {(64,64), (128,128)} with
+ *    num_q_heads / num_kv_heads <= 16, page_size 16 or 64 (grouped-query);
+ *  - (576, 512) with v_aliases_k = 1, num_kv_heads = 1 and num_q_heads a
+ *    multiple of 64, page_size 16 or 64 (absorbed latent attention: the
+ *    value row of a key is the first 512 columns of its 576-wide key row);
+ *  - (192, 128) with v_aliases_k = 0, num_q_heads / num_kv_heads <= 16 and
+ *    page_size 64 (latent attention with its heads split out: keys 128 + 64
+ *    rope, values 128 per head). This layout is prefill only: every sequence
+ *    with one or more new tokens is a prefill sequence.
+ * sm_scale must be finite and > 0. */
 typedef struct flex_attn_shape {
   int32_t num_q_heads;
   int32_t num_kv_heads;
@@ -82,9 +90,12 @@ typedef struct flex_attn_shape {
 typedef struct flex_attn_plan_opts {
   int32_t cus_total;          /* [256] */
   int32_t cus_decode;         /* [0 = all CUs] */
-  int32_t bm;                 /* prefill rows per tile: 16 or 32 [32]; 64 or 128 [128] for 576/512 */
+  int32_t bm;                 /* prefill rows per tile. Grouped-query: 16 or 32 tokens, or 128
+                                 flattened rows, each a (token, query head) pair of one KV head
+                                 [128 when the batch gives every prefill CU at least four
+                                 such 128-row work-groups, else 32]; 576/512: 64 or 128 tokens
+                                 [128]; 192/128: 128 [128] */
   int32_t min_split_tokens;   /* shortest balanced decode range, in keys [256] */
-  int32_t max_splits;         /* accepted and ignored (must be >= 0) */
   int32_t wg_per_cu;          /* decode work-groups aimed at per CU
                                  [1 grouped-query, 2 for 576/512] */
   int32_t split_granule;      /* co-run split granularity in CUs [32] */
@@ -97,8 +108,8 @@ typedef struct flex_attn_plan_opts {
 /* Summary of a plan. */
 typedef struct flex_attn_plan_info {
   int32_t num_seqs;
-  int32_t n_decode_seqs;     /* sequences with one new token */
-  int32_t n_prefill_seqs;    /* sequences with two or more new tokens */
+  int32_t n_decode_seqs;     /* sequences with one new token (none in the 192/128 layout) */
+  int32_t n_prefill_seqs;    /* sequences with two or more new tokens (one or more: 192/128) */
   int32_t n_decode_items;    /* decode pieces: (sequence, key range) work items */
   int32_t n_prefill_items;   /* (sequence, row tile) work items */
   int32_t n_split_seqs;      /* decode sequences cut into more than one piece */
@@ -119,6 +130,10 @@ typedef struct flex_attn_plan_info {
 } flex_attn_plan_info;
 
 /* Device tensors of one run. Strides are in elements.
+ *  (A run call checks pointers, alignment, strides, block_table_stride >=
+ *  the plan's max_pages_per_seq and buffer sizes; the contents of
+ *  block_table, seq_lens and query_start_loc are checked only in debug mode,
+ *  see flex_attn_set_debug, or on the host by flex_attn_validate_host.)
  *  q        bf16 [T, Hq, d_qk], contiguous (T = query_start_loc[B]).
  *  k_cache  bf16 pages: element (page, slot, kv_head, d) at
  *           page*k_stride[0] + slot*k_stride[1] + kv_head*k_stride[2] + d.
@@ -169,7 +184,8 @@ const char* flex_attn_status_string(int status);
 const char* flex_attn_last_error(void);
 
 /* Build a host plan: validate the integer metadata, classify each sequence by
- * its new-token count (1 -> decode, >= 2 -> prefill, 0 -> nothing), split each
+ * its new-token count (1 -> decode, >= 2 -> prefill, 0 -> nothing; in the
+ * (192, 128) layout every count >= 1 is prefill), split each
  * decode sequence's keys into page-aligned ranges, tile each prefill chunk into
  * rows, longest key range first, and fix the co-run CU split. This mirrors the
  * daemon's validate-then-enqueue step and its per-phase queues (Sec. 3.2;
@@ -184,6 +200,32 @@ int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan_opts* opts
                    const int32_t* h_seq_lens, int32_t max_pages_per_seq,
                    flex_attn_plan_t** out_plan);
 
+/* Check one run's metadata on the host against the plan, before copying it
+ * to the device: block_table_stride >= the plan's max_pages_per_seq, entries
+ * 0 .. ceil(L_s / P) - 1 of every block-table row in [0, num_pages), and
+ * h_seq_lens [B] / h_query_start_loc [B+1] equal to the values the plan was
+ * built from. FLEX_OK, or FLEX_ERR_INVALID_ARG naming the first violation.
+ * Host arrays only; no HIP call. */
+int flex_attn_validate_host(const flex_attn_plan_t* plan, const int32_t* h_block_table,
+                            int32_t block_table_stride, int32_t num_pages, const int32_t* h_seq_lens,
+                            const int32_t* h_query_start_loc);
+
+/* Debug mode of the run calls, the device-side counterpart of
+ * flex_attn_validate_host (the paper's daemon validates each request before
+ * dispatch, Sec. 3.2). With level 1, flex_attn_decode, _prefill, _mixed and
+ * _mixed_static first run a check kernel on the stream that compares the
+ * device seq_lens and query_start_loc with the plan's copy (uploaded with
+ * the plan) and every block-table entry a sequence uses with
+ * [0, num_pages); they wait for it (the call then synchronises the stream,
+ * so debug mode does not suit graph capture) and return
+ * FLEX_ERR_INVALID_ARG naming the sequence without launching attention
+ * when a check fails. Level 0 turns it off. The initial level is 1 when the
+ * environment variable FLEX_ATTN_DEBUG is set to anything but 0 when the
+ * library loads, else 0. Returns the previous level, or FLEX_ERR_INVALID_ARG
+ * for a negative level. FLEX_ATTN_LOG=1 in the environment prints one line
+ * per plan on stderr (2: also every work item). */
+int flex_attn_set_debug(int level);
+
 /* Copy the plan summary into *out. */
 int flex_attn_plan_info_get(const flex_attn_plan_t* plan, flex_attn_plan_info* out);
 
@@ -197,13 +239,15 @@ int flex_attn_plan_upload(const flex_attn_plan_t* plan, void* d_dst, size_t dst_
 
 void flex_attn_plan_destroy(flex_attn_plan_t* plan);
 
-/* Decode phase (sequences with one new token): split-K attention over each
+/* Decode phase (sequences with one new token; the 192/128 layout has none):
+ * split-K attention over each
  * sequence's pages, streamed from HBM, then (when some sequence is split) a
  * second launch that merges the splits in split order:
  * out = sum_j e^{m_j - M} O_j / sum_j e^{m_j - M} l_j, M = max_j m_j. */
 int flex_attn_decode(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream);
 
-/* Prefill phase (sequences with two or more new tokens): causal flash
+/* Prefill phase (sequences with two or more new tokens, or one or more in the
+ * 192/128 layout): causal flash
  * attention over key tiles gathered through block_table into LDS, with QK^T
  * and PV on bf16 matrix cores and fp32 accumulation. */
 int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream);

@@ -33,7 +33,7 @@ the contract is:
   the piece count), a launch order of the pieces for one-work-group-per-
   piece launches lists them by key count descending, ties by slot, and a
   merge list gives the first piece of every sequence cut into several pieces
-  (batch order). max_splits is accepted and ignored.
+  (batch order).
 * prefill tiles of BM rows (128 for the latent layout, which also takes 64):
   rows [t*BM, min(n, (t+1)*BM)), key_end = L - n + row_end; ordered by
   key_end descending, then sequence, then tile. Each tile is served by
@@ -67,10 +67,11 @@ the contract is:
   (decode_gbps_per_cu 1e9). Ties in start time: prefill first, then phase
   order. Entry 8 k + x is the k-th of XCD x's list, -1 past its end.
 
-Blob layout (int32, version 5): 22-word header (word 19: offset of the
-merge list, 20: offset of the fused order, 21: its length), 8 words per
-decode item, the range table, the piece launch order, the merge list, 8
-words per prefill item, the fused order; see ``build_plan``.
+Blob layout (int32, version 6): 23-word header (word 19: offset of the
+merge list, 20: offset of the fused order, 21: its length, 22: offset of the
+lengths), 8 words per decode item, the range table, the piece launch order,
+the merge list, 8 words per prefill item, the fused order, then seq_lens [B]
+and query_start_loc [B+1] as given; see ``build_plan``.
 """
 from __future__ import annotations
 
@@ -80,8 +81,8 @@ from typing import List, Optional, Sequence
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
 MAGIC = 0x46504C58
-VERSION = 5
-HEADER = 22
+VERSION = 6
+HEADER = 23
 ITEM = 8
 # cost-model rates of one CU when the options leave them 0 (the library's
 # defaults: measured with half of an MI355X running one phase alone)
@@ -110,7 +111,6 @@ class Opts:
     cus_decode: int = 0          # 0 -> all; -1 -> cost model
     bm: int = 0                  # 0 -> 32 or 128 by batch size (128 for the latent layouts)
     min_split_tokens: int = 0    # 0 -> 256
-    max_splits: int = 0          # 0 -> 32
     wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 2 (576/512 latent layout)
     split_granule: int = 0       # 0 -> 32
     hbm_gbps: float = 0.0        # 0 -> 8000
@@ -161,13 +161,12 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     # --- option checks / defaults
     cus_total = o.cus_total or 256
     wg_per_cu = o.wg_per_cu or (2 if sh.head_dim_qk == 576 else 1)
-    max_splits = o.max_splits or 32
     min_tokens = o.min_split_tokens or 256
     granule = o.split_granule or 32
     mla = sh.head_dim_qk == 576
     split = sh.head_dim_qk == 192     # heads split out: prefill only, one tile per query head
     bm = o.bm or (128 if mla or split else 0)      # grouped-query default chosen after the CU split
-    if cus_total < 1 or wg_per_cu < 1 or max_splits < 1 or min_tokens < 1 or granule < 1:
+    if cus_total < 1 or wg_per_cu < 1 or min_tokens < 1 or granule < 1:
         return PlanResult(ERR_INVALID_ARG)
     if o.cus_decode < -1 or o.cus_decode > cus_total:
         return PlanResult(ERR_INVALID_ARG)
@@ -287,11 +286,13 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
                         G=G, sh=sh, o=o, cus_total=cus_total, cus_decode=cus_decode)
     off_fused = total
     total += len(fused)
+    off_lens = total
+    total += 2 * B + 1
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
            HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, off_merge,
-           off_fused, len(fused)]
+           off_fused, len(fused), off_lens]
     blob = (hdr + [x for it in dec_items for x in it] + ranges + order + merge + [x for it in tiles for x in it]
-            + fused)
+            + fused + list(seq_lens) + list(qsl))
     # workspace: (max, sum) per decode item, column and row, then the partial outputs;
     # only needed when some decode sequence is split
     if n_split == 0:

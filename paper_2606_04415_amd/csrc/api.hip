@@ -9,7 +9,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -27,7 +29,8 @@ struct flex_attn_corun {
   // Fork/join through stream memory operations on three 64-bit step counters
   // (caller, prefill, decode): far cheaper, on the host and on the device,
   // than event records and event waits across queues.
-  uint64_t* flags = nullptr;   // device memory, zeroed at creation
+  uint64_t* flags = nullptr;   // a slot of the device's counter pool, zeroed at creation
+  int slot = -1;
   uint64_t step = 0;           // last step number issued
   int device = 0;
   int cus_prefill = 0;
@@ -76,7 +79,10 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
   if (a->k_stride[2] < sh.head_dim_qk || vs[2] < (sh.v_aliases_k ? sh.head_dim_qk : sh.head_dim_v))
     return set_error(FLEX_ERR_INVALID_ARG, "cache head stride smaller than the head dimension");
   if (a->num_pages <= 0) return set_error(FLEX_ERR_INVALID_ARG, "num_pages must be positive");
-  if (a->block_table_stride < 1) return set_error(FLEX_ERR_INVALID_ARG, "block_table_stride < 1");
+  if (a->block_table_stride < 1 || a->block_table_stride < plan->max_pages_per_seq)
+    return set_error(FLEX_ERR_INVALID_ARG, "block_table_stride " + std::to_string(a->block_table_stride) +
+                                               " is below the plan's max_pages_per_seq " +
+                                               std::to_string(plan->max_pages_per_seq));
   if (a->d_plan_bytes < info.device_plan_bytes)
     return set_error(FLEX_ERR_WORKSPACE, "d_plan_bytes smaller than the plan's device_plan_bytes");
   if (info.workspace_bytes > 0 && !ws_override) {
@@ -107,6 +113,34 @@ int prepare(const flex_attn_plan_t* plan, const flex_attn_args* a, AttnParams* p
     p->ws_stats = reinterpret_cast<float*>(ws);
     p->ws_o = reinterpret_cast<float*>(ws + ((stats + 255) / 256) * 256);
   }
+  return FLEX_OK;
+}
+
+// Debug mode (flex_attn_set_debug, or FLEX_ATTN_DEBUG=1 in the environment
+// when the library loads): before any attention launch, a check kernel
+// compares the device seq_lens / query_start_loc with the plan's copy and
+// every used block-table entry with [0, num_pages); a violation is
+// FLEX_ERR_INVALID_ARG and nothing is launched.
+std::atomic<int> g_debug{[] {
+  const char* v = std::getenv("FLEX_ATTN_DEBUG");
+  return v && *v && std::strcmp(v, "0") != 0 ? 1 : 0;
+}()};
+
+int debug_validate(const flex_attn_plan_t* plan, const flex_attn_args* a, hipStream_t s) {
+  if (g_debug.load(std::memory_order_relaxed) == 0) return FLEX_OK;
+  const flex_attn_plan_info& info = plan->info;
+  if (info.n_decode_items + info.n_prefill_items == 0) return FLEX_OK;
+  int32_t kind = 0, seq = -1;
+  const hipError_t e =
+      debug_check(a->seq_lens, a->query_start_loc, a->block_table, a->block_table_stride,
+                  static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_LENS], info.num_seqs,
+                  plan->shape.page_size, a->num_pages, &kind, &seq, s);
+  if (e != hipSuccess) return hip_fail(e, "debug check");
+  static const char* what[] = {"", "device seq_lens differs from the plan's", "device query_start_loc differs "
+                               "from the plan's", "a block-table entry lies outside [0, num_pages)"};
+  if (kind != 0)
+    return set_error(FLEX_ERR_INVALID_ARG, "debug check, sequence " + std::to_string(seq) + ": " +
+                                               what[kind >= 1 && kind <= 3 ? kind : 0]);
   return FLEX_OK;
 }
 
@@ -163,6 +197,42 @@ int run_fused(const flex_attn_plan_t* plan, const AttnParams& p, const flex_attn
   const hipError_t e = launch_fused(pp, pd, d + plan->words[H_OFF_FUSED], n, plan->shape.head_dim_qk,
                                     heads_per_wg <= 4 ? 2 : 1, info.n_split_seqs > 0, s);
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "fused launch");
+}
+
+// Step counters of the co-run pairs: a fixed pool of slots (3 counters
+// each, padded to 4) per device in module memory, so creating a pair
+// allocates no device memory. Host code uses the address resolved per device
+// with hipGetSymbolAddress, never the array's name.
+constexpr int kCorunSlots = 64;
+static __device__ __align__(256) uint64_t corun_counters[kCorunSlots * 4];
+std::mutex g_corun_mu;
+uint64_t* g_corun_base[64] = {};
+bool g_corun_used[64][kCorunSlots] = {};
+
+int corun_slot_acquire(int dev, int* slot, uint64_t** flags) {
+  if (dev < 0 || dev >= 64) return set_error(FLEX_ERR_UNSUPPORTED, "device index beyond the counter table");
+  std::lock_guard<std::mutex> lock(g_corun_mu);
+  if (!g_corun_base[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(corun_counters));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(corun_counters)");
+    g_corun_base[dev] = static_cast<uint64_t*>(ptr);
+  }
+  for (int i = 0; i < kCorunSlots; ++i) {
+    if (!g_corun_used[dev][i]) {
+      g_corun_used[dev][i] = true;
+      *slot = i;
+      *flags = g_corun_base[dev] + 4 * i;
+      return FLEX_OK;
+    }
+  }
+  return set_error(FLEX_ERR_UNSUPPORTED, "more than " + std::to_string(kCorunSlots) + " co-run pairs on one device");
+}
+
+void corun_slot_release(int dev, int slot) {
+  if (dev < 0 || dev >= 64 || slot < 0) return;
+  std::lock_guard<std::mutex> lock(g_corun_mu);
+  g_corun_used[dev][slot] = false;
 }
 
 // CU masks in eighths of the device. On MI355X (8 XCDs x 4 shader engines x 8
@@ -222,16 +292,18 @@ extern "C" int flex_attn_plan_upload(const flex_attn_plan_t* plan, void* d_dst, 
 extern "C" int flex_attn_decode(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream) {
   clear_error();
   AttnParams p;
-  const int st = prepare(plan, args, &p);
+  int st = prepare(plan, args, &p);
   if (st != FLEX_OK) return st;
+  if ((st = debug_validate(plan, args, static_cast<hipStream_t>(stream))) != FLEX_OK) return st;
   return run_decode(plan, p, args, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, void* stream) {
   clear_error();
   AttnParams p;
-  const int st = prepare(plan, args, &p);
+  int st = prepare(plan, args, &p);
   if (st != FLEX_OK) return st;
+  if ((st = debug_validate(plan, args, static_cast<hipStream_t>(stream))) != FLEX_OK) return st;
   return run_prefill(plan, p, args, static_cast<hipStream_t>(stream));
 }
 
@@ -245,6 +317,7 @@ int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode
   int st = prepare(plan, args, &p, ws_override);
   if (st != FLEX_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = debug_validate(plan, args, s)) != FLEX_OK) return st;
   if (mode == FLEX_MODE_FUSED) return run_fused(plan, p, args, s);
   const bool has_pre = plan->info.n_prefill_items > 0, has_dec = plan->info.n_decode_items > 0;
   auto pre = [&](hipStream_t ps) { return run_prefill(plan, p, args, ps); };
@@ -259,6 +332,10 @@ int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode
     return FLEX_OK;
   }
   if (!corun) return set_error(FLEX_ERR_INVALID_ARG, "co-run mode needs a co-run stream pair");
+  if (has_pre && has_dec && plan->info.cus_decode != corun->cus_decode)
+    return set_error(FLEX_ERR_INVALID_ARG, "the plan's decode phase is partitioned for " +
+                                               std::to_string(plan->info.cus_decode) + " CUs, the co-run pair gives it " +
+                                               std::to_string(corun->cus_decode));
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -342,6 +419,13 @@ extern "C" int flex_attn_mixed_static(const flex_attn_plan_t* plan, const flex_a
 
 extern "C" size_t flex_attn_static_scratch_bytes(void) { return kStaticScratchBytes; }
 
+extern "C" int flex_attn_set_debug(int level) {
+  clear_error();
+  if (level < 0) return set_error(FLEX_ERR_INVALID_ARG, "debug level < 0");
+  const int prev = g_debug.exchange(level > 0 ? 1 : 0);
+  return prev;
+}
+
 extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, flex_attn_corun_t** out) {
   clear_error();
   if (!out) return set_error(FLEX_ERR_INVALID_ARG, "out is NULL");
@@ -371,11 +455,14 @@ extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, f
   c->device = dev;
   c->cus_prefill = cus_prefill;
   c->cus_decode = cus_decode;
+  if (const int st = corun_slot_acquire(dev, &c->slot, &c->flags); st != FLEX_OK) {
+    delete c;
+    return st;
+  }
   if ((e = hipExtStreamCreateWithCUMask(&c->prefill, words, mask_p)) != hipSuccess ||
       (e = hipExtStreamCreateWithCUMask(&c->decode, words, mask_d)) != hipSuccess ||
-      (e = hipMalloc(reinterpret_cast<void**>(&c->flags), 3 * sizeof(uint64_t))) != hipSuccess ||
       (e = hipMemset(c->flags, 0, 3 * sizeof(uint64_t))) != hipSuccess) {
-    const int st = hip_fail(e, "co-run stream/event creation");
+    const int st = hip_fail(e, "co-run stream creation");
     flex_attn_corun_destroy(c);
     return st;
   }
@@ -388,9 +475,9 @@ extern "C" void flex_attn_corun_destroy(flex_attn_corun_t* c) {
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
   if (c->prefill) (void)hipStreamDestroy(c->prefill);
   if (c->decode) (void)hipStreamDestroy(c->decode);
-  if (c->flags) {
+  if (c->slot >= 0) {
     (void)hipDeviceSynchronize();   // no stream may still wait on the counters
-    (void)hipFree(c->flags);
+    corun_slot_release(c->device, c->slot);
   }
   delete c;
 }

@@ -16,6 +16,7 @@
 //                     atomics).
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "device_common.h"
@@ -1218,6 +1219,65 @@ __global__ void gather_kernel(CacheRef kref, CacheRef vref, int has_v, const int
       for (int d = threadIdx.x; d < dv; d += blockDim.x) v_out[r * dv + d] = vs[d];
     }
   }
+}
+
+// Debug check: one work-group per sequence. The first violation found
+// (kind, sequence) lands in status[0], status[1]; status must start at zero.
+__global__ __launch_bounds__(256) void debug_check_kernel(const int32_t* seq_lens, const int32_t* qsl,
+                                                          const int32_t* bt, int32_t bt_stride,
+                                                          const int32_t* plan_lens, int32_t B, int32_t P,
+                                                          int32_t num_pages, int32_t* status) {
+  const int s = int(blockIdx.x);
+  const int32_t L = plan_lens[s];                 // the length the plan was built for
+  auto flag = [&](int kind) {
+    if (atomicCAS(status, 0, kind) == 0) status[1] = s;
+  };
+  if (threadIdx.x == 0) {
+    if (seq_lens[s] != L) flag(1);
+    if (qsl[s] != plan_lens[B + s] || (s == B - 1 && qsl[B] != plan_lens[2 * B])) flag(2);
+  }
+  const int pages = (L + P - 1) / P;
+  for (int t = int(threadIdx.x); t < pages; t += int(blockDim.x)) {
+    const int32_t pg = bt[int64_t(s) * bt_stride + t];
+    if (pg < 0 || pg >= num_pages) flag(3);
+  }
+}
+
+// Per-device status words of the debug check, resolved once per device.
+static __device__ int32_t debug_status[2];
+static std::mutex g_debug_mu;
+static int32_t* g_debug_ptr[64] = {};
+
+hipError_t debug_check(const int32_t* seq_lens, const int32_t* qsl, const int32_t* bt, int32_t bt_stride,
+                       const int32_t* plan_lens, int32_t num_seqs, int32_t P, int32_t num_pages, int32_t* kind,
+                       int32_t* seq, hipStream_t stream) {
+  *kind = 0;
+  *seq = -1;
+  if (num_seqs == 0) return hipSuccess;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  int32_t* status = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_debug_mu);
+    if (!g_debug_ptr[dev]) {
+      void* ptr = nullptr;
+      if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(debug_status))) != hipSuccess) return e;
+      g_debug_ptr[dev] = static_cast<int32_t*>(ptr);
+    }
+    status = g_debug_ptr[dev];
+  }
+  if ((e = launch_fill_zero(status, 8, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(debug_check_kernel, dim3(num_seqs), dim3(256), 0, stream, seq_lens, qsl, bt, bt_stride,
+                     plan_lens, num_seqs, P, num_pages, status);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  int32_t h[2] = {0, -1};
+  if ((e = hipMemcpyAsync(h, status, sizeof(h), hipMemcpyDeviceToHost, stream)) != hipSuccess) return e;
+  if ((e = hipStreamSynchronize(stream)) != hipSuccess) return e;
+  *kind = h[0];
+  *seq = h[1];
+  return hipSuccess;
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t words) {

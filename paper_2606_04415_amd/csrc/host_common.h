@@ -9,19 +9,21 @@
 
 namespace flexattn {
 
-// Plan word layout: a 22-word header, 8 words per decode item, the range
+// Plan word layout: a 23-word header, 8 words per decode item, the range
 // table, the piece launch order, the merge list, 8 words per prefill item,
-// the fused order.
+// the fused order, then the batch's seq_lens [B] and query_start_loc [B+1]
+// as the plan saw them (the debug check compares the device copies with
+// them).
 constexpr int32_t kPlanMagic = 0x46504C58;
-constexpr int32_t kPlanVersion = 5;
-constexpr int kHeaderWords = 22;
+constexpr int32_t kPlanVersion = 6;
+constexpr int kHeaderWords = 23;
 constexpr int kItemWords = 8;
 
 enum HeaderField {
   H_MAGIC = 0, H_VERSION, H_NUM_SEQS, H_N_DEC_ITEMS, H_N_PRE_ITEMS, H_N_DEC_SEQS,
   H_N_PRE_SEQS, H_DEC_WIDTH, H_PRE_GRID_Y, H_OFF_DEC, H_OFF_PRE, H_PPS, H_CUS_DEC,
   H_CUS_PRE, H_BM, H_TOTAL_WORDS, H_N_RANGES, H_OFF_RANGES, H_OFF_ORDER, H_OFF_MERGE,
-  H_OFF_FUSED, H_N_FUSED
+  H_OFF_FUSED, H_N_FUSED, H_OFF_LENS
 };
 
 // Decode item (one piece: the overlap of a balanced page range with one
@@ -80,6 +82,7 @@ int set_error(int status, const std::string& msg);
 // Validates an attention shape (sets the error text); FLEX_OK if supported.
 int check_shape(const flex_attn_shape& sh);
 void clear_error();
+int log_level();
 
 }  // namespace flexattn
 
@@ -88,5 +91,10 @@ struct flex_attn_plan {
   flex_attn_plan_info info;
   int32_t cus_total;        // the CU count the plan was partitioned against
   int32_t rows_per_wg;      // query rows of one decode work-group
+  int32_t max_pages_per_seq;  // block-table entries a row must hold
   std::vector<int32_t> words;
 };
+
+namespace flexattn {
+void log_plan(const ::flex_attn_plan_t& p);
+}  // namespace flexattn

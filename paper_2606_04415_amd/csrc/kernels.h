@@ -52,6 +52,17 @@ hipError_t launch_gather(const CacheRef& kc, const CacheRef& vc, bool has_v, con
                          uint16_t* k_out, uint16_t* v_out, hipStream_t stream);
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
+// Debug check of one run's device metadata against the plan's own copy of
+// the lengths (plan_lens: seq_lens [B] then query_start_loc [B+1], on the
+// device): every sequence's seq_lens and query_start_loc entry equal to the
+// plan's, and block-table entries 0 .. ceil(L_s / P) - 1 of every row in
+// [0, num_pages). Enqueues the check on stream, waits for it, and returns in
+// *kind 0 (all good) or the first violation found (1: seq_lens, 2:
+// query_start_loc, 3: block-table entry) and in *seq its sequence.
+hipError_t debug_check(const int32_t* seq_lens, const int32_t* qsl, const int32_t* bt, int32_t bt_stride,
+                       const int32_t* plan_lens, int32_t num_seqs, int32_t P, int32_t num_pages, int32_t* kind,
+                       int32_t* seq, hipStream_t stream);
+
 struct AppendParams {
   const uint16_t* k_new;
   const uint16_t* v_new;

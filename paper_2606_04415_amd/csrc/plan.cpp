@@ -10,6 +10,8 @@
 // phase's work so one kernel launch per phase covers the batch.
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -37,6 +39,39 @@ bool supported_dims(const flex_attn_shape& s) {
 }
 
 }  // namespace
+
+// FLEX_ATTN_LOG=1: one summary line per plan on stderr; 2: also every work
+// item.
+int log_level() {
+  static const int level = [] {
+    const char* v = std::getenv("FLEX_ATTN_LOG");
+    return v ? std::atoi(v) : 0;
+  }();
+  return level;
+}
+
+void log_plan(const ::flex_attn_plan_t& p) {
+  const flex_attn_plan_info& i = p.info;
+  std::fprintf(stderr,
+               "flexattn plan: %d seqs (%d decode, %d prefill); decode %d pieces in %d ranges x %d columns, "
+               "%d split seqs, %d pages/range; prefill %d tiles x %d (bm %d); CUs decode %d / prefill %d; "
+               "%d words, workspace %zu B, fused %d\n",
+               i.num_seqs, i.n_decode_seqs, i.n_prefill_seqs, i.n_decode_items, i.n_decode_ranges,
+               i.decode_wg_width, i.n_split_seqs, i.pages_per_split, i.n_prefill_items, i.prefill_grid_y, i.bm,
+               i.cus_decode, i.cus_prefill, i.plan_words, i.workspace_bytes, i.n_fused_wgs);
+  if (log_level() < 2) return;
+  const int32_t* w = p.words.data();
+  for (int32_t k = 0; k < i.n_decode_items; ++k) {
+    const int32_t* it = w + w[H_OFF_DEC] + kItemWords * k;
+    std::fprintf(stderr, "  decode %d: seq %d piece %d/%d keys [%d, %d) slot %d\n", k, it[0], it[1], it[2], it[3],
+                 it[4], it[7]);
+  }
+  for (int32_t k = 0; k < i.n_prefill_items; ++k) {
+    const int32_t* it = w + w[H_OFF_PRE] + kItemWords * k;
+    std::fprintf(stderr, "  prefill %d: seq %d tile %d rows [%d, %d) key_end %d\n", k, it[0], it[1], it[2], it[3],
+                 it[4]);
+  }
+}
 
 int check_shape(const flex_attn_shape& sh) {
   if (sh.num_q_heads <= 0 || sh.num_kv_heads <= 0 || sh.num_q_heads % sh.num_kv_heads)
@@ -105,11 +140,10 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   // Grouped-query decode: one work-group per CU walking a long range measured
   // fastest; latent decode launches one work-group per piece, so more pieces.
   const int64_t wg_per_cu = o.wg_per_cu ? o.wg_per_cu : (sh.head_dim_qk == 576 ? 2 : 1);
-  const int64_t max_splits = o.max_splits ? o.max_splits : 32;
   const int64_t min_tokens = o.min_split_tokens ? o.min_split_tokens : 256;
   const int64_t granule = o.split_granule ? o.split_granule : 32;
   int32_t bm = o.bm ? o.bm : (latent || split ? 128 : 0);   // grouped-query default: chosen below
-  if (cus_total < 1 || wg_per_cu < 1 || max_splits < 1 || min_tokens < 1 || granule < 1)
+  if (cus_total < 1 || wg_per_cu < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
   if (o.cus_decode < -1 || o.cus_decode > cus_total)
     return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
@@ -347,6 +381,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   plan->shape = sh;
   plan->rows_per_wg = rows_per_wg;
   plan->cus_total = int32_t(cus_total);
+  plan->max_pages_per_seq = max_pages_per_seq;
   const int32_t n_pre_items = int32_t(tiles.size());
   // Launch order for one work-group per piece: longest key range first.
   std::vector<int32_t> order(n_dec_items);
@@ -362,7 +397,8 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int32_t off_merge = off_order + n_dec_items;
   const int32_t off_pre = off_merge + int32_t(merge_list.size());
   const int32_t off_fused = off_pre + kItemWords * n_pre_items;
-  const int32_t total = off_fused + int32_t(fused.size());
+  const int32_t off_lens = off_fused + int32_t(fused.size());
+  const int32_t total = off_lens + 2 * num_seqs + 1;
   auto& w = plan->words;
   w.assign(kHeaderWords, 0);
   w[H_MAGIC] = kPlanMagic;
@@ -387,6 +423,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   w[H_OFF_MERGE] = off_merge;
   w[H_OFF_FUSED] = off_fused;
   w[H_N_FUSED] = int32_t(fused.size());
+  w[H_OFF_LENS] = off_lens;
   w.insert(w.end(), dec_words.begin(), dec_words.end());
   w.insert(w.end(), ranges.begin(), ranges.end());
   w.insert(w.end(), order.begin(), order.end());
@@ -396,6 +433,8 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     w.insert(w.end(), item, item + kItemWords);
   }
   w.insert(w.end(), fused.begin(), fused.end());
+  w.insert(w.end(), seq_lens, seq_lens + num_seqs);
+  w.insert(w.end(), qsl, qsl + num_seqs + 1);
 
   // Workspace: per (decode item, column) the rows' (max, sum) pairs, then the
   // unnormalised partial outputs; needed only when some sequence is split.
@@ -425,7 +464,38 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   info.decode_bytes = double(dec_bytes);
   info.prefill_flops = double(pre_flops);
   info.n_fused_wgs = int32_t(fused.size());
+  if (log_level() > 0) log_plan(*plan);
   *out_plan = plan;
+  return FLEX_OK;
+}
+
+extern "C" int flex_attn_validate_host(const flex_attn_plan_t* plan, const int32_t* bt, int32_t bt_stride,
+                                       int32_t num_pages, const int32_t* h_seq_lens, const int32_t* h_qsl) {
+  clear_error();
+  if (!plan || !bt || !h_seq_lens || !h_qsl) return set_error(FLEX_ERR_INVALID_ARG, "NULL argument");
+  const int32_t B = plan->info.num_seqs;
+  const int32_t* lens = plan->words.data() + plan->words[H_OFF_LENS];
+  const int32_t* pqsl = lens + B;
+  if (bt_stride < plan->max_pages_per_seq)
+    return set_error(FLEX_ERR_INVALID_ARG, "block_table_stride " + std::to_string(bt_stride) +
+                                               " is below the plan's max_pages_per_seq " +
+                                               std::to_string(plan->max_pages_per_seq));
+  if (num_pages <= 0) return set_error(FLEX_ERR_INVALID_ARG, "num_pages must be positive");
+  const int64_t P = plan->shape.page_size;
+  for (int32_t s = 0; s < B; ++s) {
+    if (h_seq_lens[s] != lens[s])
+      return set_error(FLEX_ERR_INVALID_ARG, "sequence " + std::to_string(s) + ": seq_lens differs from the plan's");
+    if (h_qsl[s] != pqsl[s] || (s == B - 1 && h_qsl[B] != pqsl[B]))
+      return set_error(FLEX_ERR_INVALID_ARG,
+                       "sequence " + std::to_string(s) + ": query_start_loc differs from the plan's");
+    for (int64_t t = 0; t < cdiv(lens[s], P); ++t) {
+      const int32_t pg = bt[int64_t(s) * bt_stride + t];
+      if (pg < 0 || pg >= num_pages)
+        return set_error(FLEX_ERR_INVALID_ARG, "sequence " + std::to_string(s) + ", page " + std::to_string(t) +
+                                                   ": block-table entry " + std::to_string(pg) +
+                                                   " outside [0, num_pages)");
+    }
+  }
   return FLEX_OK;
 }
 

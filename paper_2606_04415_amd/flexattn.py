@@ -32,7 +32,7 @@ EXPORTED = [
     "flex_attn_prefill", "flex_attn_mixed", "flex_attn_corun_create", "flex_attn_corun_destroy",
     "flex_attn_corun_streams", "flex_attn_corun_set_timing", "flex_attn_corun_timing_read",
     "flex_attn_debug_gather", "flex_attn_workspace_init", "flex_attn_kv_append",
-    "flex_attn_mixed_static", "flex_attn_static_scratch_bytes",
+    "flex_attn_mixed_static", "flex_attn_static_scratch_bytes", "flex_attn_validate_host", "flex_attn_set_debug",
     "flex_ctl_create", "flex_ctl_destroy", "flex_ctl_set_profile", "flex_ctl_observe", "flex_ctl_decide",
     "flex_ctl_estimates", "flex_ts_create", "flex_ts_destroy", "flex_ts_next", "flex_ts_observe", "flex_ts_totals",
 ]
@@ -58,7 +58,7 @@ class Shape(ctypes.Structure):
 
 class PlanOpts(ctypes.Structure):
     _fields_ = [("cus_total", ctypes.c_int32), ("cus_decode", ctypes.c_int32), ("bm", ctypes.c_int32),
-                ("min_split_tokens", ctypes.c_int32), ("max_splits", ctypes.c_int32),
+                ("min_split_tokens", ctypes.c_int32),
                 ("wg_per_cu", ctypes.c_int32), ("split_granule", ctypes.c_int32),
                 ("hbm_gbps", ctypes.c_double), ("decode_gbps_per_cu", ctypes.c_double),
                 ("prefill_tflops_per_cu", ctypes.c_double)]
@@ -162,6 +162,8 @@ def lib():
     L.flex_attn_mixed_static.argtypes = [vp, ctypes.POINTER(Args), ctypes.c_int, vp, vp]
     L.flex_attn_static_scratch_bytes.argtypes = []
     L.flex_attn_static_scratch_bytes.restype = ctypes.c_size_t
+    L.flex_attn_validate_host.argtypes = [vp, ctypes.POINTER(i32), i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    L.flex_attn_set_debug.argtypes = [ctypes.c_int]
     L.flex_attn_corun_create.argtypes = [i32, i32, ctypes.POINTER(vp)]
     L.flex_attn_corun_destroy.argtypes = [vp]
     L.flex_attn_corun_destroy.restype = None
@@ -289,9 +291,33 @@ def current_stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
+def _require(cond, what):
+    if not cond:
+        raise ValueError(what)
+
+
 def make_args(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, lse=None,
               d_plan=None, workspace=None) -> Args:
-    """Args from device tensors (bf16 caches [pages, P, Hkv, d] with unit inner stride)."""
+    """Args from device tensors (bf16 caches [pages, P, Hkv, d] with unit inner stride).
+
+    Checks what the C side cannot see: dtypes (bf16 q/caches/out, fp32 lse,
+    int32 metadata), contiguity of q, out, lse and the metadata rows, a unit
+    innermost cache stride, and that every tensor is on one device."""
+    import torch
+    for name, t in (("q", q), ("k_cache", k_cache), ("out", out)) + ((("v_cache", v_cache),) if v_cache is not None else ()):
+        _require(t.dtype == torch.bfloat16, f"{name} must be bfloat16, not {t.dtype}")
+    for name, t in (("block_table", block_table), ("seq_lens", seq_lens), ("query_start_loc", query_start_loc)):
+        _require(t.dtype == torch.int32, f"{name} must be int32, not {t.dtype}")
+    _require(lse is None or lse.dtype == torch.float32, "lse must be float32")
+    for name, t in (("q", q), ("out", out), ("seq_lens", seq_lens), ("query_start_loc", query_start_loc)) + \
+            ((("lse", lse),) if lse is not None else ()):
+        _require(t.is_contiguous(), f"{name} must be contiguous")
+    _require(block_table.dim() == 2 and block_table.stride(1) == 1, "block_table must be 2-D with unit column stride")
+    for name, t in (("k_cache", k_cache),) + ((("v_cache", v_cache),) if v_cache is not None else ()):
+        _require(t.dim() == 4 and t.stride(3) == 1, f"{name} must be [pages, P, Hkv, d] with a unit innermost stride")
+    devs = {t.device for t in (q, k_cache, block_table, seq_lens, query_start_loc, out)
+            if t is not None}
+    _require(len(devs) == 1, f"tensors on several devices: {devs}")
     a = Args()
     a.q = q.data_ptr()
     a.k_cache = k_cache.data_ptr()
@@ -337,6 +363,26 @@ def flex_attn_mixed(plan: Plan, args: Args, mode: int, stream=None, corun: "Coru
     s = stream if stream is not None else current_stream()
     check(lib().flex_attn_mixed(plan.handle, ctypes.byref(args), mode, s,
                                 corun.handle if corun is not None else None), "flex_attn_mixed")
+
+
+def flex_attn_validate_host(plan: Plan, block_table, num_pages: int, seq_lens, query_start_loc):
+    """Host-side check of a run's metadata against the plan (torch CPU int32 tensors or int lists).
+    Raises FlexAttnError (FLEX_ERR_INVALID_ARG) naming the first violation."""
+    import torch
+    bt = torch.as_tensor(block_table, dtype=torch.int32).contiguous()
+    if bt.dim() != 2:
+        raise ValueError("block_table must be 2-D")
+    ptr = ctypes.cast(bt.data_ptr(), ctypes.POINTER(ctypes.c_int32))
+    check(lib().flex_attn_validate_host(plan.handle, ptr, bt.stride(0), int(num_pages), _i32_array(list(seq_lens)),
+                                        _i32_array(list(query_start_loc))), "flex_attn_validate_host")
+
+
+def set_debug(level: int) -> int:
+    """Debug mode of the run calls (device check before launch); returns the previous level."""
+    r = lib().flex_attn_set_debug(int(level))
+    if r < 0:
+        check(r, "flex_attn_set_debug")
+    return r
 
 
 def flex_attn_mixed_static(plan: Plan, args: Args, mode: int, stream=None, corun: "Corun" = None):

@@ -98,7 +98,7 @@ def test_plan_matches_rederivation_fuzz():
         for n in ns:
             qsl.append(qsl[-1] + n)
         maxp = max([1] + [-(-L // P) for L in ls]) + rng.randint(0, 3)
-        opts = OP.Opts(cus_decode=rng.choice([0, 64, 192, -1]), max_splits=rng.choice([0, 1, 3]),
+        opts = OP.Opts(cus_decode=rng.choice([0, 64, 192, -1]),
                        wg_per_cu=rng.choice([0, 2]), min_split_tokens=rng.choice([0, 16, 1000]),
                        bm=(rng.choice([0, 0, 16, 32, 128]) if sh.head_dim_qk in (64, 128)
                            else rng.choice([0, 64]) if sh.head_dim_qk == 576 else rng.choice([0, 128])),
@@ -133,7 +133,7 @@ def test_shape_status_matches(sh):
 
 
 @pytest.mark.parametrize("opts", [OP.Opts(cus_decode=-2), OP.Opts(cus_decode=300), OP.Opts(bm=96),
-                                  OP.Opts(wg_per_cu=-1), OP.Opts(max_splits=-4)])
+                                  OP.Opts(wg_per_cu=-1), OP.Opts(min_split_tokens=-4)])
 def test_opts_status_matches(opts):
     compare(OP.Shape(28, 4, 128, 128, 16, 0.1, 0), opts, [0, 1, 3], [5, 9], 4)
 
@@ -197,3 +197,81 @@ def test_export_too_small():
     plan = F.flex_attn_plan(sh, None, [0, 1], [40], 4)
     buf = (ctypes.c_int32 * 4)()
     assert F.lib().flex_attn_plan_export(plan.handle, buf, 4) == F.FLEX_ERR_WORKSPACE
+
+
+def test_block_table_stride_below_the_plans_rows_is_refused():
+    sh = F.make_shape(28, 4, 128, 128, 16, 0.088)
+    plan = F.flex_attn_plan(sh, None, [0, 1, 3], [40, 50], 8)     # rows must hold 8 entries
+    a = F.Args()
+    a.q = a.k_cache = a.v_cache = a.block_table = a.seq_lens = a.query_start_loc = a.out = a.d_plan = 0x1000
+    a.k_stride = (ctypes.c_int64 * 3)(16 * 4 * 128, 4 * 128, 128)
+    a.v_stride = (ctypes.c_int64 * 3)(16 * 4 * 128, 4 * 128, 128)
+    a.num_pages, a.block_table_stride = 10, 4
+    a.d_plan_bytes = plan.info["device_plan_bytes"]
+    assert F.lib().flex_attn_prefill(plan.handle, ctypes.byref(a), None) == F.FLEX_ERR_INVALID_ARG
+    assert "max_pages_per_seq" in F.last_error()
+
+
+def test_validate_host_catches_bad_metadata():
+    """The host-side form of the debug check: a block-table entry outside the
+    pool, a negative one, seq_lens or query_start_loc that differ from the
+    plan's, and a row stride below the plan's row length are each refused."""
+    sh = F.make_shape(28, 4, 128, 128, 16, 0.088)
+    qsl, ls = [0, 1, 41, 42], [40, 40, 17]
+    plan = F.flex_attn_plan(sh, None, qsl, ls, 4)
+    bt = torch.tensor([[0, 1, 2, 99], [3, 4, 5, 99], [6, 7, 99, 99]], dtype=torch.int32)   # 99: unused entries
+    F.flex_attn_validate_host(plan, bt, 8, ls, qsl)
+    bad = bt.clone()
+    bad[1, 2] = 8          # outside [0, 8)
+    with pytest.raises(F.FlexAttnError) as e:
+        F.flex_attn_validate_host(plan, bad, 8, ls, qsl)
+    assert e.value.status == F.FLEX_ERR_INVALID_ARG and "sequence 1, page 2" in str(e.value)
+    bad = bt.clone()
+    bad[2, 0] = -1
+    with pytest.raises(F.FlexAttnError):
+        F.flex_attn_validate_host(plan, bad, 8, ls, qsl)
+    with pytest.raises(F.FlexAttnError) as e:
+        F.flex_attn_validate_host(plan, bt, 8, [40, 41, 17], qsl)
+    assert "seq_lens" in str(e.value)
+    with pytest.raises(F.FlexAttnError) as e:
+        F.flex_attn_validate_host(plan, bt, 8, ls, [0, 1, 40, 42])
+    assert "query_start_loc" in str(e.value)
+    with pytest.raises(F.FlexAttnError) as e:
+        F.flex_attn_validate_host(plan, bt[:, :3], 8, ls, qsl)
+    assert "max_pages_per_seq" in str(e.value)
+
+
+def test_debug_level_switch():
+    prev = F.set_debug(1)
+    assert F.set_debug(0) == 1
+    F.set_debug(prev)
+    assert F.lib().flex_attn_set_debug(-1) == F.FLEX_ERR_INVALID_ARG
+
+
+def test_plan_log_line():
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r); from paper_2606_04415_amd import flexattn as F; "
+            "F.flex_attn_plan(F.make_shape(28, 4, 128, 128, 16, 0.088), None, [0, 1, 3], [40, 50], 4)" % ROOT)
+    r = subprocess.run([sys.executable, "-c", code], env=dict(os.environ, FLEX_ATTN_LOG="2"),
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert "flexattn plan: 2 seqs (1 decode, 1 prefill)" in r.stderr and "prefill 0: seq 1" in r.stderr
+
+
+def test_binding_refuses_wrong_dtypes_and_layouts():
+    q = torch.zeros(3, 28, 128, dtype=torch.bfloat16)
+    k = torch.zeros(4, 16, 4, 128, dtype=torch.bfloat16)
+    bt = torch.zeros(2, 4, dtype=torch.int32)
+    sl = torch.tensor([40, 50], dtype=torch.int32)
+    qsl = torch.tensor([0, 1, 3], dtype=torch.int32)
+    out = torch.zeros(3, 28, 128, dtype=torch.bfloat16)
+    F.make_args(q, k, k, bt, sl, qsl, out)
+    with pytest.raises(ValueError, match="int32"):
+        F.make_args(q, k, k, bt.long(), sl, qsl, out)
+    with pytest.raises(ValueError, match="bfloat16"):
+        F.make_args(q.float(), k, k, bt, sl, qsl, out)
+    with pytest.raises(ValueError, match="contiguous"):
+        F.make_args(q.transpose(0, 1), k, k, bt, sl, qsl, out)
+    with pytest.raises(ValueError, match="innermost"):
+        F.make_args(q, k.transpose(2, 3), k, bt, sl, qsl, out)

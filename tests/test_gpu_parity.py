@@ -60,7 +60,7 @@ RAGGED_GQA = [
 def test_ragged_gqa_d128_page16(min_split):
     ns, ls = RAGGED_GQA[0]
     b = custom_batch(QW, ns, ls, seed=3)
-    opts = F.make_opts(min_split_tokens=min_split, max_splits=4 if min_split else 0)
+    opts = F.make_opts(min_split_tokens=min_split)
     log(f"ragged GQA 28/4 d128 page16, min_split_tokens={min_split}")
     full_check(b, opts, "ragged-d128")
 
@@ -87,7 +87,7 @@ def test_ragged_latent(hq):
     ls = [1, 63, 65, 3000, 130, 200, 700]
     b = custom_batch(MLA, ns, ls, seed=6, num_q_heads=hq)
     log(f"ragged latent 576/512 page64, {hq} heads, forced splits")
-    full_check(b, F.make_opts(min_split_tokens=128, max_splits=8), f"latent-h{hq}")
+    full_check(b, F.make_opts(min_split_tokens=128), f"latent-h{hq}")
 
 
 def test_single_key_is_exact():
@@ -157,7 +157,7 @@ def test_page_permutation_bitwise():
 def test_run_to_run_bitwise():
     ns, ls = RAGGED_GQA[0]
     b = custom_batch(QW, ns, ls, seed=9)
-    opts = F.make_opts(min_split_tokens=16, max_splits=8)
+    opts = F.make_opts(min_split_tokens=16)
     o1, l1, pa = run(b, opts=opts)
     d = device_inputs(b)
     o2, l2, _ = run(b, d=d, pa=pa)

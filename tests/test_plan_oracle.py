@@ -127,8 +127,10 @@ def check_fused(sh, r, b):
     """The one-launch order: every work-group once, on its XCD, each phase in order."""
     nd, npf, R, bm, gy = b[3], b[4], b[16], b[14], b[8]
     off_f, nf = b[20], b[21]
-    assert off_f == b[10] + 8 * npf and off_f + nf == len(b) and r.info["n_fused_wgs"] == nf
-    fused = b[off_f:]
+    assert off_f == b[10] + 8 * npf and off_f + nf == b[22] and r.info["n_fused_wgs"] == nf
+    B = b[2]
+    assert len(b) == b[22] + 2 * B + 1                      # then seq_lens and query_start_loc as given
+    fused = b[off_f:off_f + nf]
     G = sh.num_q_heads // sh.num_kv_heads
     fusable = sh.head_dim_qk != 576 and G > 4 and 3 <= sh.num_kv_heads <= 8 and bm == 32 and nd + npf > 0
     assert (nf > 0) == fusable and nf % 8 == 0
@@ -166,7 +168,7 @@ def test_fuzz_invariants():
         qsl, ls, maxp = random_batch(rng, sh.page_size, rng.randint(0, 40), rng.randint(0, 4))
         cus_total = rng.choice([0, 0, 16])
         opts = OP.Opts(cus_decode=rng.choice([0, 8, -1] if cus_total else [0, 64, 128, -1]),
-                       max_splits=rng.choice([0, 2, 8]), wg_per_cu=rng.choice([0, 1, 8]),
+                       wg_per_cu=rng.choice([0, 1, 8]),
                        bm=0 if mla else rng.choice([0, 0, 16, 32, 128]), cus_total=cus_total,
                        split_granule=8 if cus_total else 0)
         check_invariants(sh, opts, qsl, ls, maxp)
