@@ -18,15 +18,25 @@ from __future__ import annotations
 
 import argparse
 import json
+import os
 import sys
 
 
-def _time_on(stream_handle, fn, reps, warmup=30):
+def _time_on(stream_handle, fn, reps, warmup=30, settle_ms=100.0):
+    """Mean us per call of fn over reps calls on the stream, after warmup calls
+    and settle_ms of further untimed calls (the device raises its clock over
+    the first MFMA-heavy launches after idle)."""
+    import time
     import torch
     s = torch.cuda.ExternalStream(stream_handle) if stream_handle else torch.cuda.current_stream()
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < settle_ms * 1e-3:
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(s)
     for i in range(reps):
@@ -36,7 +46,12 @@ def _time_on(stream_handle, fn, reps, warmup=30):
     return e0.elapsed_time(e1) / reps * 1e3   # us
 
 
-def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0, counts=None, corun: bool = True):
+def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0, counts=None, corun: bool = True,
+          check_outputs: bool = False):
+    """Phase curves and co-run step times (see the module text). With
+    check_outputs, each split's plan also runs once serially and once
+    co-run into separate outputs, and `corun_bitwise_equals_serial` records
+    whether the two are bit-identical."""
     import torch
     from . import flexattn as F
     from .workloads import WORKLOADS, algorithmic_work, make_batch
@@ -84,9 +99,21 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
         # would synchronize with the co-run streams at every step)
         caller = torch.cuda.Stream()
         cs = caller.cuda_stream
+        if check_outputs:
+            res["corun_bitwise_equals_serial"] = {}
         for cd in [c for c in counts if c < total]:
             pa, args = plan_for(cd)
             cr = F.Corun(total - cd, cd)
+            if check_outputs:
+                outs = []
+                for mode in (F.FLEX_MODE_SERIAL, F.FLEX_MODE_CORUN):
+                    o, _ = pa.alloc_out(q)
+                    a = pa.args(q, kv[0][0], kv[0][1], bt, sl, qsl, o)
+                    F.flex_attn_mixed(pa.plan, a, mode, stream=cs, corun=cr)
+                    torch.cuda.synchronize()
+                    outs.append(o)
+                res["corun_bitwise_equals_serial"][cd] = bool(torch.equal(outs[0].view(torch.int16),
+                                                                          outs[1].view(torch.int16)))
             us = _time_on(cs, lambda i=0: F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_CORUN,
                                                              stream=cs, corun=cr), reps)
             cr.close()
@@ -107,6 +134,21 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
     return res
 
 
+PROFILE_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "profiles")
+
+
+def profile_from(result):
+    """(cus, decode GB/s, prefill TFLOP/s) of a sweep result (dict or JSON file
+    path), the alone-phase profile flex_ctl_set_profile takes (Sec. 3.3: the
+    scheduler's per-phase profile)."""
+    if isinstance(result, str):
+        with open(result) as f:
+            result = json.load(f)
+    cus = sorted(int(c) for c in result["decode"] if str(c) in result["prefill"] or int(c) in result["prefill"])
+    get = lambda d, c: d[str(c)] if str(c) in d else d[c]
+    return cus, [get(result["decode"], c)["GBps"] for c in cus], [get(result["prefill"], c)["TFLOPs"] for c in cus]
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--workload", default="mixed")
@@ -114,9 +156,17 @@ def main():
     ap.add_argument("--pools", type=int, default=4, help="KV cache copies rotated over repetitions")
     ap.add_argument("--cus", default="", help="comma-separated CU counts (default: every eighth of the device)")
     ap.add_argument("--no-corun", action="store_true", help="phase curves only")
+    ap.add_argument("--check-outputs", action="store_true", help="co-run vs serial bit-identity at every split")
+    ap.add_argument("--save", default="", help="also write the result to this JSON file")
     args = ap.parse_args()
     counts = [int(c) for c in args.cus.split(",") if c] or None
-    print(json.dumps(sweep(args.workload, args.reps, args.pools, counts=counts, corun=not args.no_corun)), flush=True)
+    r = sweep(args.workload, args.reps, args.pools, counts=counts, corun=not args.no_corun,
+              check_outputs=args.check_outputs)
+    r["command"] = "python -m paper_2606_04415_amd.cusweep " + " ".join(sys.argv[1:])
+    if args.save:
+        with open(args.save, "w") as f:
+            json.dump(r, f, indent=1)
+    print(json.dumps(r), flush=True)
 
 
 if __name__ == "__main__":

@@ -32,7 +32,9 @@ over separate steps). A step is the KV append of its new tokens plus the
 attention of the mixed batch (GPU time, HIP events on the issuing stream,
 with no per-phase events inside: the controller's phase times come from an
 untimed repeat of the step's attention); plan building and upload are host
-work outside it. Request time stamps use
+work outside it, timed per step (plan_host_ms) and added in series to the
+device time in total_with_plan_ms (the run if planning did not overlap the
+previous step's GPU work, which a serving engine would do). Request time stamps use
 the running sum of step times: TTFT = end of the step that finishes a
 request's prompt minus the time it arrived; TPOT = the time from a request's
 previous token (or the end of its prompt) to each of its decode tokens, over
@@ -47,6 +49,7 @@ from __future__ import annotations
 import argparse
 import json
 import math
+import os
 import random
 import sys
 import time
@@ -153,6 +156,7 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
     nxt = 0
     clock = 0.0
     step_ms: List[float] = []
+    plan_ms: List[float] = []
     tok_ms: List[float] = []   # time since the previous token, for every decode token
     splits: Dict[str, int] = {}
     reasons: Dict[int, int] = {}
@@ -214,7 +218,8 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
                 slots.append(r.pages[pos // P] * P + pos % P)
         n_dec = sum(1 for n in ns if n == 1)
         pend_prefill = sum(r.prompt - r.prefilled for r in waiting + active) - (args.chunk - budget)
-        # the policy's choice
+        # the policy's choice (host planning and upload are timed: plan_host_ms)
+        t_plan = time.perf_counter()
         probe = F.PagedAttention(shape, F.make_opts(), qsl, ls, max_pages)
         info = probe.plan.info
         mode, cd = F.FLEX_MODE_SERIAL, 0
@@ -238,6 +243,7 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
             pa = F.PagedAttention(shape, F.make_opts(wg_per_cu=2), qsl, ls, max_pages)
         else:
             pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd), qsl, ls, max_pages)
+        plan_ms.append((time.perf_counter() - t_plan) * 1e3)
         key = {F.FLEX_MODE_SERIAL: "serial", F.FLEX_MODE_FUSED: "fused"}.get(mode, f"{256 - cd}:{cd}")
         if ts is not None:
             key = "decode" if phase == F.FLEX_TS_DECODE else "prefill"
@@ -308,6 +314,7 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         return xs[min(len(xs) - 1, int(p * len(xs)))] if xs else None
 
     busy = [x for x in step_ms if x > 0]
+    plan_total = sum(plan_ms)
     ttft = [r.first_ms - r.arrival_ms for r in reqs[:nxt] if r.first_ms is not None and r.arrival_step >= 0]
     res = {"mix": mix, "policy": policy, "steps": args.steps, "total_ms": round(clock, 3),
            "step_ms": {"mean": round(sum(busy) / max(1, len(busy)), 4), "p50": pct(busy, 0.5), "p90": pct(busy, 0.9),
@@ -319,18 +326,29 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
            "throughput": {"decode_tok_per_s": round(len(tok_ms) / clock * 1e3, 1) if clock else None,
                           "prefill_tok_per_s": round(prefill_tokens / clock * 1e3, 1) if clock else None},
            "device_ms": {k: round(v, 3) for k, v in phase_ms.items()},
+           # host planning (plan build + upload, incl. the policy's probe plan) per step: a serving
+           # engine overlaps it with the previous step's GPU work; total_with_plan_ms is the run if it
+           # did not (host and device time in series)
+           "plan_host_ms": {"mean": round(plan_total / max(1, len(plan_ms)), 4), "p90": pct(plan_ms, 0.9)},
+           "total_with_plan_ms": round(clock + plan_total, 3),
            "splits": splits}
     if ctl is not None:
         res["reasons"] = {str(k): v for k, v in sorted(reasons.items())}
     return res
 
 
-def measure_profile(reps: int = 10):
-    """Alone phase rates on 64..256 CUs (quarters) for the mixed step, to seed the controller."""
-    from .cusweep import sweep
+def measure_profile(reps: int = 10, remeasure: bool = False):
+    """Alone phase rates on 64..256 CUs (quarters) for the mixed step, to seed
+    the controller: the committed CU sweep (profiles/cusweep_mixed.json) when
+    present, else measured now."""
+    from .cusweep import PROFILE_DIR, profile_from, sweep
+    path = os.path.join(PROFILE_DIR, "cusweep_mixed.json")
+    if os.path.exists(path) and not remeasure:
+        cus, dec, pre = profile_from(path)
+        keep = [i for i, c in enumerate(cus) if c % 64 == 0]
+        return [cus[i] for i in keep], [dec[i] for i in keep], [pre[i] for i in keep]
     r = sweep("mixed", reps=reps, pools=2, counts=[64, 128, 192, 256], corun=False)
-    cus = sorted(int(c) for c in r["decode"])
-    return (cus, [r["decode"][c]["GBps"] for c in cus], [r["prefill"][c]["TFLOPs"] for c in cus])
+    return profile_from(r)
 
 
 def main():
@@ -349,6 +367,8 @@ def main():
     ap.add_argument("--rate", type=float, default=0.2, help="Poisson arrivals per step")
     ap.add_argument("--fixed-decode-cus", type=int, default=128)
     ap.add_argument("--no-profile", action="store_true", help="controller starts from its prior only")
+    ap.add_argument("--remeasure-profile", action="store_true",
+                    help="measure the phase profile now instead of reading profiles/cusweep_mixed.json")
     ap.add_argument("--decode-share", type=float, default=0.5,
                     help="timeslice policy: target decode share of device time (or name it: timeslice:0.3)")
     ap.add_argument("--ts-decay", type=float, default=0.9,
@@ -356,7 +376,7 @@ def main():
     ap.add_argument("--no-controller-fused", dest="controller_fused", action="store_false",
                     help="the controller chooses between serial and co-run only")
     args = ap.parse_args()
-    profile = None if args.no_profile else measure_profile()
+    profile = None if args.no_profile else measure_profile(remeasure=args.remeasure_profile)
     if profile:
         print(json.dumps({"profile": {"cus": profile[0], "decode_GBps": profile[1], "prefill_TFLOPs": profile[2]}}),
               flush=True)

@@ -339,3 +339,17 @@ def test_timeslice_decay_forgets():
     assert d < 1e-15 and p > 0
     assert ts.next(True, True) == F.FLEX_TS_DECODE
     ts.close()
+
+
+def test_controller_seeds_from_the_committed_cu_sweep():
+    """The measured CU sweep of the mixed step (profiles/cusweep_mixed.json)
+    is the controller's alone-phase profile (flex_ctl_set_profile)."""
+    from paper_2606_04415_amd.serve_sim import measure_profile
+    cus, dec, pre = measure_profile()
+    assert cus == [64, 128, 192, 256] and all(x > 0 for x in dec + pre)
+    ctl = F.Controller()
+    ctl.set_profile(cus, dec, pre)
+    d_est, p_est = ctl.estimates()
+    assert all(x > 0 for x in d_est + p_est)
+    d = ctl.decide(1.2e9, 1.5e11, active_decode_seqs=128)
+    assert d["mode"] in (F.FLEX_MODE_SERIAL, F.FLEX_MODE_CORUN) and d["predicted_us"] > 0
