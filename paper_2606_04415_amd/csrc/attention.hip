@@ -14,6 +14,7 @@
 //                     workspace; a second launch combines them in split order,
 //                     so results are bit-identical run to run (no float
 //                     atomics).
+#include <float.h>
 #include <math.h>
 
 #include <mutex>
@@ -696,9 +697,13 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
   constexpr bool kValuSum = VALIAS;
   f32x4 o[RB][C::NACC], lsum[RB];
   float lpart[RB];
+  // Row maxima start at the lowest finite float rather than -inf: -m then
+  // enters the exponent with no guard. Scores of masked keys are -inf, so a
+  // row whose keys are all masked in a tile keeps this floor and adds zeros;
+  // its first visible score lifts m past the rescale threshold.
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    m[rb] = -INFINITY;
+    m[rb] = -FLT_MAX;
     lsum[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
     lpart[rb] = 0.f;
 #pragma unroll
@@ -911,12 +916,22 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
           for (int r = 0; r < 4; ++r)
             s[rb][i][r] = kc0 + 16 * i + 4 * gq + r < row_limit[rb] ? s[rb][i][r] : -INFINITY;
       }
-      float mx = fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3]));
+      // One chain, so that the compiler pairs it into three-input maxima.
+      float mx = s[rb][0][0];
 #pragma unroll
-      for (int i = 1; i < 2 * CH; ++i)
-        mx = fmaxf(mx, fmaxf(fmaxf(s[rb][i][0], s[rb][i][1]), fmaxf(s[rb][i][2], s[rb][i][3])));
-      cmax[rb] = group_max(mx) * p.scale_log2;
+      for (int i = 0; i < 2 * CH; ++i)
+#pragma unroll
+        for (int r = (i == 0 ? 1 : 0); r < 4; ++r) mx = fmaxf(mx, s[rb][i][r]);
+      cmax[rb] = mx;
     }
+    if constexpr (RB == 2) {
+      group_max2(cmax[0], cmax[1]);
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) cmax[rb] = group_max(cmax[rb]);
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) cmax[rb] *= p.scale_log2;
 
     // Lazy rescale: a row's max moves only when the tile max exceeds it by
     // more than the threshold; then its accumulators and sum scale by 2^(m-m').
@@ -944,7 +959,7 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
       u32x4 pop[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const float neg_m = m[rb] == -INFINITY ? 0.f : -m[rb];
+        const float neg_m = -m[rb];
 #pragma unroll
         for (int e2 = 0; e2 < 4; ++e2) {
           const f32x4& sb = s[rb][2 * ch + (e2 >> 1)];

@@ -146,6 +146,21 @@ __device__ __forceinline__ float swap32_combine_max(float v) {
   return fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
 }
 __device__ __forceinline__ float group_max(float v) { return swap32_combine_max(swap16_combine_max(v)); }
+// group_max of two values at once, in three swaps instead of four. With
+// lane-group rows a = (a0..a3), b = (b0..b3): swap16(a, b) pairs a0|a1 and
+// a2|a3 in rows 0 and 2 and b's in rows 1 and 3; after one max, swap32 of the
+// result with itself pairs rows 0|2 and 1|3, and a last swap16 of the second
+// max with itself spreads a's total to every row of one output and b's to
+// every row of the other.
+__device__ __forceinline__ void group_max2(float& a, float& b) {
+  auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  const float c = fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+  t = __builtin_amdgcn_permlane32_swap(__float_as_uint(c), __float_as_uint(c), false, false);
+  const float d = fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+  t = __builtin_amdgcn_permlane16_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+  a = __uint_as_float(t[0]);
+  b = __uint_as_float(t[1]);
+}
 __device__ __forceinline__ float group_sum(float v) {
   uint32_t u = __float_as_uint(v);
   auto t = __builtin_amdgcn_permlane16_swap(u, u, false, false);
