@@ -573,6 +573,145 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   wait_vmem<0>();
 }
 
+// Tile loads of one work-group: BN keys of K rows (and of V rows unless V
+// aliases K) from the paged cache into one LDS stage, through 16-byte DMA
+// loads. Load instruction j of wave w fills 1 KB of a stage: lane slot
+// s = 64 * (w * NI + j) + lane is one 16-byte chunk of a K row
+// (s < K_SLOTS) or of a V row. Byte offsets split into a per-lane part fixed
+// for the whole launch and a per-tile part: a tile starts on a multiple of
+// BN keys, so in a tile that lies below key_end the slot of row r within its
+// page is r % P (pages of at most BN keys) or kb % P + r (larger pages).
+// s_pt holds the block-table entries of the current page window.
+template <int DQK, int DV, int NW, int BN, bool VALIAS, int NS, int P>
+struct TileLoader {
+  using C = RowParCfg<DQK, DV, NW, 1, BN, VALIAS, NS>;
+  static_assert(VALIAS || P >= BN || (64 % C::CPR == 0 && P % (64 / C::CPR) == 0),
+                "a load instruction stays in one page");
+  // A whole tile whose load instructions each stay in one page (every row
+  // layout but the padded latent rows with pages of at most BN keys): the
+  // tile's pages are read once into scalar registers and every load goes
+  // through a buffer resource on its page, with the launch-fixed per-lane
+  // offsets; no per-tile vector address arithmetic.
+  static constexpr bool kUniformPage = !(VALIAS && P <= BN);
+  static constexpr int PPT = P <= BN ? BN / P : 1;   // pages per tile
+
+  uint8_t* lds;
+  const int* s_pt;
+  int w, lane, key_end;
+  const uint8_t* kbase;
+  const uint8_t* vbase;
+  uint32_t ksp, kss, vsp, vss;
+  uint32_t ld_lane_off[C::NI];
+
+  __device__ __forceinline__ TileLoader(const AttnParams& p, int head_kv, uint8_t* lds_, const int* s_pt_, int w_,
+                                        int lane_, int key_end_)
+      : lds(lds_), s_pt(s_pt_), w(w_), lane(lane_), key_end(key_end_) {
+    kbase = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(head_kv) * p.kc.sh);
+    vbase = reinterpret_cast<const uint8_t*>((VALIAS ? p.kc.base : p.vc.base) +
+                                             int64_t(head_kv) * (VALIAS ? p.kc.sh : p.vc.sh));
+    ksp = uint32_t(p.kc.sp) * 2u;
+    kss = uint32_t(p.kc.ss) * 2u;
+    vsp = uint32_t(VALIAS ? p.kc.sp : p.vc.sp) * 2u;
+    vss = uint32_t(VALIAS ? p.kc.ss : p.vc.ss) * 2u;
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      int row;
+      uint32_t xoff;
+      slot_of(j, row, xoff);
+      ld_lane_off[j] = (P <= BN ? uint32_t(row % P) : uint32_t(row)) * (is_v(j) ? vss : kss) + xoff;
+    }
+  }
+  // Whether load j of this wave fills V rows (wave-uniform).
+  __device__ __forceinline__ bool is_v(int j) const { return !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS; }
+  // Row and byte offset within the row of the chunk lane slot s loads.
+  __device__ __forceinline__ void slot_of(int j, int& row, uint32_t& xoff) const {
+    const int blk = w * C::NI + j;
+    const int s = blk * 64 + lane;
+    int x = 0;
+    row = 0;
+    if (VALIAS || blk * 64 < C::K_SLOTS) {   // wave-uniform
+      if (s < C::K_SLOTS) {
+        row = s / C::ROWB;
+        const int pc = s % C::ROWB;
+        x = pc < C::CPR ? swz_k<DQK, VALIAS>(pc, row) : 0;
+      }
+    } else if (s < C::SLOTS) {
+      const int s2 = s - C::K_SLOTS;
+      row = s2 / (C::CPRV > 0 ? C::CPRV : 1);
+      x = swz_v<DV>(s2 % (C::CPRV > 0 ? C::CPRV : 1), row);
+    }
+    xoff = 16u * uint32_t(x);
+  }
+  // Page of a slot within its tile (pages of at most BN keys): per lane for
+  // the padded latent rows; for unpadded rows one load instruction covers
+  // 64 / CPR whole rows of one page, so it is wave-uniform.
+  __device__ __forceinline__ int tile_page(int j, int row) const {
+    if constexpr (P > BN) return 0;
+    if constexpr (VALIAS) return row / P;
+    const int blk = w * C::NI + j;
+    const int row0 = blk * 64 < C::K_SLOTS ? blk * 64 / C::CPR : (blk * 64 - C::K_SLOTS) / (C::CPRV > 0 ? C::CPRV : 1);
+    return __builtin_amdgcn_readfirstlane(row0 / P);
+  }
+  __device__ __forceinline__ void issue_whole(int kb, int st, int pt_base) const {
+    uint8_t* sbase = lds + st * C::STAGE;
+    int pg[PPT];
+#pragma unroll
+    for (int t = 0; t < PPT; ++t) pg[t] = __builtin_amdgcn_readfirstlane(s_pt[kb / P - pt_base + t]);
+    const uint32_t in_page = P > BN ? uint32_t(kb % P) : 0u;   // first slot of the tile in its page
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      const bool isv = is_v(j);
+      const uint8_t* base = isv ? vbase : kbase;
+      const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
+      const int tp = tile_page(j, 0);
+      int page = pg[0];
+#pragma unroll
+      for (int t = 1; t < PPT; ++t) page = tp == t ? pg[t] : page;
+      const i32x4 r = uniform_rsrc(base + (uint64_t(uint32_t(page)) * sp + in_page * ss), uint32_t(min(P, BN)) * ss);
+      dma16_buf(r, ld_lane_off[j], sbase + (w * C::NI + j) * 1024);
+    }
+  }
+  // Issue this wave's loads of the key tile starting at kb into stage st.
+  // Keys past key_end read the last key's row (masked later); padding slots
+  // read a dummy row.
+  __device__ __forceinline__ void issue(int kb, int st, int pt_base) const {
+    uint8_t* sbase = lds + st * C::STAGE;
+    const bool whole = kb + BN <= key_end;
+    if constexpr (kUniformPage) {
+      if (whole) {
+        issue_whole(kb, st, pt_base);
+        return;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < C::NI; ++j) {
+      const bool isv = is_v(j);
+      const uint8_t* base = isv ? vbase : kbase;
+      const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
+      int pidx;
+      uint32_t off;
+      if (whole) {
+        int row = 0;
+        if constexpr (VALIAS && P <= BN) {
+          uint32_t xoff;
+          slot_of(j, row, xoff);
+        }
+        pidx = kb / P - pt_base + tile_page(j, row);
+        off = P <= BN ? ld_lane_off[j] : ld_lane_off[j] + uint32_t(kb % P) * ss;
+      } else {
+        int row;
+        uint32_t xoff;
+        slot_of(j, row, xoff);
+        const uint32_t key = uint32_t(min(kb + row, key_end - 1));
+        pidx = int(key / P) - pt_base;
+        off = (key % P) * ss + xoff;
+      }
+      const uint32_t page = uint32_t(s_pt[pidx]);
+      dma16(base + (uint64_t(page) * sp + off), sbase + (w * C::NI + j) * 1024);
+    }
+  }
+};
+
 // One work-group's work: item `item` of the phase, column `col`, threads
 // 0 .. NW*64-1 of the work-group, the work-group's dynamic LDS.
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB>
@@ -711,123 +850,8 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
   }
   const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 x 8
 
-  // Gather addressing. Load instruction j of this wave fills 1 KB of a stage:
-  // lane slot s = 64 * (w * NI + j) + lane is one 16-byte chunk of a K row
-  // (s < K_SLOTS) or of a V row. Byte offsets split into a per-lane part fixed
-  // for the whole launch and a per-tile part: a tile starts on a multiple of
-  // BN keys, so in a tile that lies below key_end the slot of row r within its
-  // page is r % P (pages of at most BN keys) or kb % P + r (larger pages).
-  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(p.kc.base + int64_t(head_kv) * p.kc.sh);
-  const uint8_t* vbase =
-      reinterpret_cast<const uint8_t*>((VALIAS ? p.kc.base : p.vc.base) + int64_t(head_kv) * (VALIAS ? p.kc.sh : p.vc.sh));
-  const uint32_t ksp = uint32_t(p.kc.sp) * 2u, kss = uint32_t(p.kc.ss) * 2u;
-  const uint32_t vsp = uint32_t(VALIAS ? p.kc.sp : p.vc.sp) * 2u, vss = uint32_t(VALIAS ? p.kc.ss : p.vc.ss) * 2u;
-  // Row and byte offset within the row of the chunk lane slot s loads.
-  auto slot_of = [&](int j, int& row, uint32_t& xoff) {
-    const int blk = w * C::NI + j;
-    const int s = blk * 64 + lane;
-    int x = 0;
-    row = 0;
-    if (VALIAS || blk * 64 < C::K_SLOTS) {   // wave-uniform
-      if (s < C::K_SLOTS) {
-        row = s / C::ROWB;
-        const int pc = s % C::ROWB;
-        x = pc < C::CPR ? swz_k<DQK, VALIAS>(pc, row) : 0;
-      }
-    } else if (s < C::SLOTS) {
-      const int s2 = s - C::K_SLOTS;
-      row = s2 / (C::CPRV > 0 ? C::CPRV : 1);
-      x = swz_v<DV>(s2 % (C::CPRV > 0 ? C::CPRV : 1), row);
-    }
-    xoff = 16u * uint32_t(x);
-  };
-  // Page of a slot within its tile (pages of at most BN keys): per lane for
-  // the padded latent rows; for unpadded rows one load instruction covers
-  // 64 / CPR whole rows of one page, so it is wave-uniform.
-  auto tile_page = [&](int j, int row) {
-    if constexpr (P > BN) return 0;
-    if constexpr (VALIAS) return row / P;
-    const int blk = w * C::NI + j;
-    const int row0 = blk * 64 < C::K_SLOTS ? blk * 64 / C::CPR : (blk * 64 - C::K_SLOTS) / (C::CPRV > 0 ? C::CPRV : 1);
-    return __builtin_amdgcn_readfirstlane(row0 / P);
-  };
-  static_assert(VALIAS || P >= BN || (64 % C::CPR == 0 && P % (64 / C::CPR) == 0),
-                "a load instruction stays in one page");
-  uint32_t ld_lane_off[C::NI];
-#pragma unroll
-  for (int j = 0; j < C::NI; ++j) {
-    const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
-    int row;
-    uint32_t xoff;
-    slot_of(j, row, xoff);
-    ld_lane_off[j] = (P <= BN ? uint32_t(row % P) : uint32_t(row)) * (isv ? vss : kss) + xoff;
-  }
-
-  // Issue this wave's loads of the key tile starting at kb into stage st.
-  // Keys past key_end read the last key's row (masked later); padding slots
-  // read a dummy row.
-  // A whole tile whose load instructions each stay in one page (every row
-  // layout but the padded latent rows with pages of at most BN keys): the
-  // tile's pages are read once into scalar registers and every load goes
-  // through a buffer resource on its page, with the launch-fixed per-lane
-  // offsets; no per-tile vector address arithmetic.
-  constexpr bool kUniformPage = !(VALIAS && P <= BN);
-  constexpr int PPT = P <= BN ? BN / P : 1;   // pages per tile
-  auto issue_whole = [&](int kb, int st, int pt_base) {
-    uint8_t* sbase = lds + st * C::STAGE;
-    int pg[PPT];
-#pragma unroll
-    for (int t = 0; t < PPT; ++t) pg[t] = __builtin_amdgcn_readfirstlane(s_pt[kb / P - pt_base + t]);
-    const uint32_t in_page = P > BN ? uint32_t(kb % P) : 0u;   // first slot of the tile in its page
-#pragma unroll
-    for (int j = 0; j < C::NI; ++j) {
-      const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
-      const uint8_t* base = isv ? vbase : kbase;
-      const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
-      const int tp = tile_page(j, 0);
-      int page = pg[0];
-#pragma unroll
-      for (int t = 1; t < PPT; ++t) page = tp == t ? pg[t] : page;
-      const i32x4 r = uniform_rsrc(base + (uint64_t(uint32_t(page)) * sp + in_page * ss), uint32_t(min(P, BN)) * ss);
-      dma16_buf(r, ld_lane_off[j], sbase + (w * C::NI + j) * 1024);
-    }
-  };
-  auto issue = [&](int kb, int st, int pt_base) {
-    uint8_t* sbase = lds + st * C::STAGE;
-    const bool whole = kb + BN <= key_end;
-    if constexpr (kUniformPage) {
-      if (whole) {
-        issue_whole(kb, st, pt_base);
-        return;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < C::NI; ++j) {
-      const bool isv = !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS;
-      const uint8_t* base = isv ? vbase : kbase;
-      const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
-      int pidx;
-      uint32_t off;
-      if (whole) {
-        int row = 0;
-        if constexpr (VALIAS && P <= BN) {
-          uint32_t xoff;
-          slot_of(j, row, xoff);
-        }
-        pidx = kb / P - pt_base + tile_page(j, row);
-        off = P <= BN ? ld_lane_off[j] : ld_lane_off[j] + uint32_t(kb % P) * ss;
-      } else {
-        int row;
-        uint32_t xoff;
-        slot_of(j, row, xoff);
-        const uint32_t key = uint32_t(min(kb + row, key_end - 1));
-        pidx = int(key / P) - pt_base;
-        off = (key % P) * ss + xoff;
-      }
-      const uint32_t page = uint32_t(s_pt[pidx]);
-      dma16(base + (uint64_t(page) * sp + off), sbase + (w * C::NI + j) * 1024);
-    }
-  };
+  const TileLoader<DQK, DV, NW, BN, VALIAS, NS, P> loader(p, head_kv, lds, s_pt, w, lane, key_end);
+  auto issue = [&](int kb, int st, int pt_base) { loader.issue(kb, st, pt_base); };
 
   // Per-lane LDS byte offsets of the MFMA operand reads within a stage. The
   // row swizzles depend only on the row modulo 16 (K) or 8 (V), so they are
