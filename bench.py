@@ -225,6 +225,13 @@ def launch_timer(stream, fn, n, settle_ms, warmup):
     return [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)], i
 
 
+def prefill_kernel_name(bm, head_dim_qk):
+    """The kernel a plan's prefill tiles run on."""
+    if head_dim_qk in (64, 128) and bm == 128:
+        return "flat_prefill_kernel"
+    return "rowpar_kernel (prefill)"
+
+
 def roof(bound, achieved, unit):
     peak = HBM_PEAK_GBPS if bound == "hbm" else BF16_PEAK_TFLOPS
     return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit, "frac": round(achieved / peak, 4)}
@@ -268,6 +275,9 @@ def bench_config(name, steps, warmup, settle_ms, pools):
         if leg == "decode":
             r["GBps"] = round(dec_b / (d["mean"] * 1e-6) / 1e9, 1)
             r["roofline"] = roof("hbm", r["GBps"], "GB/s")
+            r["roofline"]["traffic"] = measured_traffic(name, "decode")
+            r["kernel"] = "decode_gqa_kernel + merge_kernel" if w.head_dim_qk != 576 else \
+                "rowpar_kernel (latent decode) + merge_kernel"
             r["algorithmic_bytes"] = dec_b
             if w.head_dim_qk == 576:   # latent decode sits near the ridge: its MFMA side too
                 fl = work["decode"]["flops"]
@@ -276,6 +286,8 @@ def bench_config(name, steps, warmup, settle_ms, pools):
         elif leg == "prefill":
             r["TFLOPs"] = round(pre_f / (d["mean"] * 1e-6) / 1e12, 1)
             r["roofline"] = roof("mfma", r["TFLOPs"], "TFLOP/s")
+            r["roofline"]["traffic"] = measured_traffic(name, "prefill")
+            r["kernel"] = prefill_kernel_name(pa.plan.info["bm"], w.head_dim_qk)
             r["algorithmic_flops"] = pre_f
         else:
             r["bound_us"] = round(max((dec_b + work["prefill"]["bytes"]) / (HBM_PEAK_GBPS * 1e3),
@@ -488,7 +500,7 @@ def main():
         achieved = pre_flops / (c_pre * 1e-3) / 1e12
         roof_ = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                  "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(w.name, "prefill"),
-                 "kernel": "rowpar_kernel (prefill)", "algorithmic_flops_per_launch": pre_flops,
+                 "kernel": prefill_kernel_name(info["bm"], w.head_dim_qk), "algorithmic_flops_per_launch": pre_flops,
                  "avg_launch_us": round(c_pre * 1e3, 2), "cus": cp,
                  "frac_of_cu_share": round(achieved / (BF16_PEAK_TFLOPS * cp / n_cus), 4)}
 
@@ -516,7 +528,7 @@ def main():
                                         "avg_phase_us": round(c_dec * 1e3, 2)}
         else:
             a = pre_flops / (c_pre * 1e-3) / 1e12
-            result["roofline_other"] = {"bound": "mfma", "kernel": "rowpar_kernel (prefill)",
+            result["roofline_other"] = {"bound": "mfma", "kernel": prefill_kernel_name(info["bm"], w.head_dim_qk),
                                         "achieved": round(a, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                         "frac": round(a / BF16_PEAK_TFLOPS, 4), "cus": cp,
                                         "frac_of_cu_share": round(a / (BF16_PEAK_TFLOPS * cp / n_cus), 4),

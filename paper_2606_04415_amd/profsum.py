@@ -9,7 +9,7 @@ kernels change).
 
     python -m paper_2606_04415_amd.profsum stats <kernel_stats.csv> <title> <command> > profiles/x.md
     python -m paper_2606_04415_amd.profsum traffic --workload mixed --fetch <csv> --write <csv> \\
-        --copy-fetch <csv> --copy-write <csv> --command "..." [--command "..."] > profiles/traffic.json
+        --copy-fetch <csv> --copy-write <csv> --command "..." [--command "..."] [--into traffic.json] > new.json
 """
 from __future__ import annotations
 
@@ -42,6 +42,22 @@ def stats_table(path, title, command):
     return "\n".join(out) + "\n"
 
 
+def kernel_role(name):
+    """decode / prefill / merge for the library's kernels, None for others.
+    rowpar_kernel's seventh template argument is its row layout (2: latent
+    decode rows, else prefill tiles)."""
+    if "merge_kernel" in name:
+        return "merge"
+    if "decode_gqa_kernel" in name:
+        return "decode"
+    if "flat_prefill_kernel" in name:
+        return "prefill"
+    if "rowpar_kernel<" in name:
+        targs = name.split("rowpar_kernel<", 1)[1].split(">", 1)[0].split(",")
+        return "decode" if len(targs) > 6 and targs[6].strip() == "2" else "prefill"
+    return None
+
+
 def counter_means(path, counter):
     """Mean per-dispatch value of `counter` for each kernel name (KiB for the size counters)."""
     acc, n = defaultdict(float), defaultdict(set)
@@ -62,9 +78,14 @@ def traffic(args):
     f = counter_means(args.fetch, "FETCH_SIZE")
     w = counter_means(args.write, "WRITE_SIZE")
     entries = {}
+    if args.into and os.path.exists(args.into):
+        with open(args.into) as fh:
+            prev = json.load(fh)
+        if prev.get("kernel_source_sha256_16") == source_hash():
+            entries.update(prev.get("entries", {}))
+            args.command = prev.get("commands", []) + [c for c in args.command if c not in prev.get("commands", [])]
     for name in f:
-        role = "decode" if ("decode" in name or "DecodeLatent" in name) else \
-               "merge" if "merge" in name else "prefill" if "rowpar" in name else None
+        role = kernel_role(name)
         if role is None:
             continue
         fb = f[name] * 1024 * fetch_scale
@@ -90,6 +111,8 @@ def main():
     for k in ("fetch", "write", "copy_fetch", "copy_write"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     t.add_argument("--command", action="append", default=[])
+    t.add_argument("--into", default="",
+                   help="an existing traffic.json whose entries (same kernel source) are kept")
     a = ap.parse_args()
     if a.cmd == "stats":
         sys.stdout.write(stats_table(a.csv, a.title, a.command))
