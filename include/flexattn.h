@@ -256,7 +256,11 @@ int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, 
  * decode on stream; FLEX_MODE_CORUN forks stream into the two CU-masked
  * streams of corun (prefill on its prefill stream, decode on its decode
  * stream) and joins them back into stream, the one-device analog of the
- * paper's dynamic co-location (Sec. 3.4). FLEX_MODE_FUSED runs both phases
+ * paper's dynamic co-location (Sec. 3.4). The fork and, for steps expected
+ * to run under a millisecond (plan info work on the pair's CU shares), the
+ * join are stream memory operations on the pair's step counters; longer
+ * steps join through events, which hold no CU while they wait (a memory-value
+ * wait on stream polls from a kernel). FLEX_MODE_FUSED runs both phases
  * in one launch on stream (then the split-K merge): each work-group of the
  * launch serves one prefill work-group's tile and column or one or two
  * decode ranges, in the plan's fused order (the phases interleaved by a

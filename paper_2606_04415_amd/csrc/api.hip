@@ -28,7 +28,9 @@ struct flex_attn_corun {
   hipStream_t decode = nullptr;
   // Fork/join through stream memory operations on three 64-bit step counters
   // (caller, prefill, decode): far cheaper, on the host and on the device,
-  // than event records and event waits across queues.
+  // than event records and event waits across queues, for sub-millisecond
+  // steps; longer steps join through events (see run_mixed). The counters
+  // only ever compare greater-or-equal, so steps of either kind mix.
   uint64_t* flags = nullptr;   // a slot of the device's counter pool, zeroed at creation
   int slot = -1;
   uint64_t step = 0;           // last step number issued
@@ -40,6 +42,7 @@ struct flex_attn_corun {
   int64_t t_count = 0;
   std::vector<hipEvent_t> ev;        // 4 per slot: prefill start/end, decode start/end
   std::vector<unsigned char> has;    // 2 per slot: prefill ran, decode ran
+  hipEvent_t join_ev[2] = {nullptr, nullptr};   // prefill done, decode done (long steps)
 };
 
 namespace {
@@ -309,6 +312,16 @@ extern "C" int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_a
 
 namespace {
 
+// Whether a co-run step of this plan is expected to run for a millisecond or
+// more (longer phase on its CU share, at about 1 PFLOP/s of prefill and
+// 6 TB/s of decode per 256 CUs). Such steps join through events.
+constexpr double kEventJoinUs = 1000.0;
+bool long_step(const flex_attn_plan_t* plan, const flex_attn_corun* c) {
+  const double pre_us = plan->info.prefill_flops / (1.0e15 / 256.0 * c->cus_prefill) * 1e6;
+  const double dec_us = plan->info.decode_bytes / (6.0e12 / 256.0 * c->cus_decode) * 1e6;
+  return std::max(pre_us, dec_us) >= kEventJoinUs;
+}
+
 int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode, void* stream,
               flex_attn_corun_t* corun, void* ws_override) {
   if (mode != FLEX_MODE_SERIAL && mode != FLEX_MODE_CORUN && mode != FLEX_MODE_FUSED)
@@ -357,6 +370,18 @@ int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode
   st = timed_phase(corun, 1, has_dec, corun->decode, dec);
   if (st != FLEX_OK) return st;
   timing_end_step(corun);
+  if (long_step(plan, corun)) {
+    // The runtime serves a memory-value wait on the caller stream with a
+    // polling kernel that may run on any CU for the whole step: over
+    // millisecond phases it measured to slow a latent prefill phase by 7%
+    // (128 of 256 CUs) to 40% (64 CUs) and to end up to 6 ms after it.
+    // Event waits hold no CU; they cost about 12 us more per step.
+    if ((e = hipEventRecord(corun->join_ev[0], corun->prefill)) != hipSuccess) return hip_fail(e, "join record");
+    if ((e = hipEventRecord(corun->join_ev[1], corun->decode)) != hipSuccess) return hip_fail(e, "join record");
+    if ((e = hipStreamWaitEvent(s, corun->join_ev[0], 0)) != hipSuccess) return hip_fail(e, "join wait");
+    if ((e = hipStreamWaitEvent(s, corun->join_ev[1], 0)) != hipSuccess) return hip_fail(e, "join wait");
+    return FLEX_OK;
+  }
   if ((e = hipStreamWriteValue64(corun->prefill, f + 1, step, 0)) != hipSuccess) return hip_fail(e, "join write");
   if ((e = hipStreamWriteValue64(corun->decode, f + 2, step, 0)) != hipSuccess) return hip_fail(e, "join write");
   if ((e = hipStreamWaitValue64(s, f + 1, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
@@ -461,7 +486,9 @@ extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, f
   }
   if ((e = hipExtStreamCreateWithCUMask(&c->prefill, words, mask_p)) != hipSuccess ||
       (e = hipExtStreamCreateWithCUMask(&c->decode, words, mask_d)) != hipSuccess ||
-      (e = hipMemset(c->flags, 0, 3 * sizeof(uint64_t))) != hipSuccess) {
+      (e = hipMemset(c->flags, 0, 3 * sizeof(uint64_t))) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&c->join_ev[0], hipEventDisableTiming)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&c->join_ev[1], hipEventDisableTiming)) != hipSuccess) {
     const int st = hip_fail(e, "co-run stream creation");
     flex_attn_corun_destroy(c);
     return st;
@@ -473,6 +500,8 @@ extern "C" int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, f
 extern "C" void flex_attn_corun_destroy(flex_attn_corun_t* c) {
   if (!c) return;
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
+  for (hipEvent_t e : c->join_ev)
+    if (e) (void)hipEventDestroy(e);
   if (c->prefill) (void)hipStreamDestroy(c->prefill);
   if (c->decode) (void)hipStreamDestroy(c->decode);
   if (c->slot >= 0) {

@@ -22,13 +22,20 @@ import os
 import sys
 
 
-def _time_on(stream_handle, fn, reps, warmup=30, settle_ms=100.0):
+def _time_on(stream_handle, fn, reps, warmup=30, settle_ms=100.0, budget_ms=1500.0):
     """Mean us per call of fn over reps calls on the stream, after warmup calls
     and settle_ms of further untimed calls (the device raises its clock over
-    the first MFMA-heavy launches after idle)."""
+    the first MFMA-heavy launches after idle). Slow calls get fewer warmup
+    calls and repetitions, so that one measurement stays near budget_ms."""
     import time
     import torch
     s = torch.cuda.ExternalStream(stream_handle) if stream_handle else torch.cuda.current_stream()
+    t0 = time.perf_counter()
+    fn()
+    torch.cuda.synchronize()
+    once_ms = (time.perf_counter() - t0) * 1e3
+    fit = max(3, int(budget_ms / max(once_ms, 1e-3) / 2))
+    warmup, reps = min(warmup, fit), min(reps, fit)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -101,7 +108,9 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
         cs = caller.cuda_stream
         if check_outputs:
             res["corun_bitwise_equals_serial"] = {}
+        res["corun_phases_us"] = {}
         for cd in [c for c in counts if c < total]:
+            print(f"co-run prefill {total - cd} / decode {cd}: measuring", file=sys.stderr, flush=True)
             pa, args = plan_for(cd)
             cr = F.Corun(total - cd, cd)
             if check_outputs:
@@ -116,9 +125,19 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
                                                                           outs[1].view(torch.int16)))
             us = _time_on(cs, lambda i=0: F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_CORUN,
                                                              stream=cs, corun=cr), reps)
+            # each phase's own duration in the co-run step (events on its stream)
+            cr.set_timing(True)
+            for i in range(min(reps, 5)):
+                F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_CORUN, stream=cs, corun=cr)
+            torch.cuda.synchronize()
+            pre, dec = cr.timing_read()
+            cr.set_timing(False)
             cr.close()
             res["corun_step_us"][cd] = round(us, 2)
-            print(f"co-run prefill {total - cd} / decode {cd}: {us:.1f} us", file=sys.stderr, flush=True)
+            res["corun_phases_us"][cd] = {"prefill": round(sum(pre) / len(pre) * 1e3, 2),
+                                          "decode": round(sum(dec) / len(dec) * 1e3, 2)}
+            print(f"co-run prefill {total - cd} / decode {cd}: {us:.1f} us (phases {res['corun_phases_us'][cd]})",
+                  file=sys.stderr, flush=True)
         pa, args = plan_for(0)
         res["serial_us"] = round(_time_on(cs, lambda i=0: F.flex_attn_mixed(pa.plan, args[i % len(args)],
                                                                             F.FLEX_MODE_SERIAL, stream=cs), reps), 2)
