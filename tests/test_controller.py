@@ -353,3 +353,32 @@ def test_controller_seeds_from_the_committed_cu_sweep():
     assert all(x > 0 for x in d_est + p_est)
     d = ctl.decide(1.2e9, 1.5e11, active_decode_seqs=128)
     assert d["mode"] in (F.FLEX_MODE_SERIAL, F.FLEX_MODE_CORUN) and d["predicted_us"] > 0
+
+
+def test_latent_sweep_seeds_a_serial_decision():
+    """Seeded with the measured CU sweep of the latent step
+    (profiles/cusweep_mla.json), the controller runs that step's work
+    serially: its decode loses most of its speed on a small CU share, so no
+    split beats prefill then decode on the whole device (the sweep's own
+    co-run steps agree)."""
+    import json
+    import os
+    from paper_2606_04415_amd.cusweep import PROFILE_DIR, profile_from
+    path = os.path.join(PROFILE_DIR, "cusweep_mla.json")
+    with open(path) as f:
+        sweep = json.load(f)
+    assert sweep["serial_us"] < sweep["best_split"]["us"]
+    cus, dec, pre = profile_from(path)
+    assert cus == [32, 64, 96, 128, 160, 192, 224, 256]
+    ctl = F.Controller()
+    ctl.set_profile(cus, dec, pre)
+    d = ctl.decide(sweep["decode_bytes"], sweep["prefill_flops"], active_decode_seqs=256)
+    assert d["mode"] == F.FLEX_MODE_SERIAL
+    # the mixed step's sweep, same rule: a co-run split
+    cus_m, dec_m, pre_m = profile_from(os.path.join(PROFILE_DIR, "cusweep_mixed.json"))
+    ctl_m = F.Controller()
+    ctl_m.set_profile(cus_m, dec_m, pre_m)
+    with open(os.path.join(PROFILE_DIR, "cusweep_mixed.json")) as f:
+        mixed = json.load(f)
+    dm = ctl_m.decide(mixed["decode_bytes"], mixed["prefill_flops"], active_decode_seqs=128)
+    assert dm["mode"] == F.FLEX_MODE_CORUN
