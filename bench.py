@@ -22,11 +22,15 @@ second idle); decode is flat. So the setup runs untimed steps of every leg
 until about `--settle-ms` of work has passed ("settle" in the line), after
 the W warm-up steps; the K co-run steps right after the warm-up, before the
 settle, are reported as `cold_corun_us`. The legs are then timed
-interleaved: blocks of steps of each mode in rotating order, an event after
-every step (p10/p50/p90 from those), each block bracketed by
-synchronisations; `value` is the co-run blocks' time over K. A second pass
-with HIP events around each phase's kernel (on the stream it runs on) gives
-the phase durations for the roofline.
+interleaved: blocks of steps of each mode in rotating order, each block
+bracketed by synchronisations and one pair of HIP events; `value` is the
+co-run blocks' time over K and every leg's `mean` comes from its blocks.
+Recording an event between steps adds work to the stream (about 3 us per
+decode step, 5 us per co-run step), so the p10/p50/p90 of each leg come from
+a separate pass with an event after every step, whose mean is reported as
+`per_step_events_mean`. A further pass with HIP events around each phase's
+kernels (on the stream they run on) gives the phase durations for the
+roofline.
 """
 from __future__ import annotations
 
@@ -203,8 +207,10 @@ def time_kv_append(b, kv, shape, steps, stream):
 
 
 def launch_timer(stream, fn, n, settle_ms, warmup):
-    """Settle, then time n launches back to back with an event after each
-    (per-launch microseconds)."""
+    """Settle, then time n launches back to back between one pair of events
+    (their mean, us), and n more with an event after each (per-launch us,
+    for the distribution; the events add work to the stream). Returns
+    (mean, per-launch list, settle launches)."""
     import torch
     for i in range(warmup):
         fn(i)
@@ -216,13 +222,28 @@ def launch_timer(stream, fn, n, settle_ms, warmup):
             fn(i)
             i += 1
         torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for j in range(n):
+        fn(j)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mean = e0.elapsed_time(e1) * 1e3 / n
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
     ev[0].record(stream)
     for j in range(n):
         fn(j)
         ev[j + 1].record(stream)
     torch.cuda.synchronize()
-    return [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)], i
+    return mean, [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)], i
+
+
+def timed_dist(mean, per):
+    """mean from an unbroken block; p10/p50/p90 from the per-step pass."""
+    d = dist(per)
+    d["per_step_events_mean"] = d["mean"]
+    d["mean"] = round(mean, 2)
+    return d
 
 
 def prefill_kernel_name(bm, head_dim_qk):
@@ -269,8 +290,8 @@ def bench_config(name, steps, warmup, settle_ms, pools):
         legs.append(("serial_step", lambda i: F.flex_attn_mixed(pa.plan, args[i % len(args)], F.FLEX_MODE_SERIAL,
                                                                 stream=cs)))
     for leg, fn in legs:
-        us, settled = launch_timer(st, fn, steps, settle_ms, warmup)
-        d = dist(us)
+        mean, us, settled = launch_timer(st, fn, steps, settle_ms, warmup)
+        d = timed_dist(mean, us)
         r = {"us": d, "settle_launches": settled}
         if leg == "decode":
             r["GBps"] = round(dec_b / (d["mean"] * 1e-6) / 1e9, 1)
@@ -431,16 +452,20 @@ def main():
                           "fused_wgs": pa_f.plan.info["n_fused_wgs"]}), flush=True)
         return
 
-    def block(mode, n, start):
-        """n steps of one mode back to back; per-step times and the block's time (us)."""
+    def block(mode, n, start, per_step=False):
+        """n steps of one mode back to back between one pair of events; with
+        per_step, an event after every step too. Returns (per-step times or
+        [], the block's time), us."""
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
         torch.cuda.synchronize()
         ev[0].record(caller)
         for j in range(n):
             step[mode](start + j)
-            ev[j + 1].record(caller)
+            if per_step or j == n - 1:
+                ev[j + 1].record(caller)
         torch.cuda.synchronize()
-        return [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)], ev[0].elapsed_time(ev[n]) * 1e3
+        per = [ev[j].elapsed_time(ev[j + 1]) * 1e3 for j in range(n)] if per_step else []
+        return per, ev[0].elapsed_time(ev[n]) * 1e3
 
     # W warm-up steps, then K co-run steps before settling (the cold figure)
     log(f"warm-up: {args.warmup} steps; cold co-run: {args.steps} steps")
@@ -466,9 +491,11 @@ def main():
     for r in range(nb):
         order = legs[r % len(legs):] + legs[:r % len(legs)]
         for mode in order:
-            us, t = block(mode, sizes[r], r * 1000)
-            per[mode] += us
+            _, t = block(mode, sizes[r], r * 1000)
             total[mode] += t
+    # the distribution: one more pass per leg with an event after every step
+    for mode in legs:
+        per[mode], _ = block(mode, args.steps, 9000, per_step=True)
     c_ms = total["corun"] / args.steps / 1e3
 
     # phase durations (events on each kernel's own stream), a separate pass
@@ -515,7 +542,7 @@ def main():
                    "why": "untimed steps of every leg after the warm-up: the device raises its clock over the first "
                           "~100-200 MFMA-heavy launches after idle"},
         "cold_corun_us": round(cold_total / args.steps, 2),
-        "step_us": {m: dist(per[m]) for m in legs},
+        "step_us": {m: timed_dist(total[m] / args.steps, per[m]) for m in legs},
         "phases_us": {"corun_prefill": round(c_pre * 1e3, 2), "corun_decode": round(c_dec * 1e3, 2)},
         "roofline": roof_,
     }
