@@ -210,9 +210,21 @@ def check(status: int, what: str):
         raise FlexAttnError(status, what, f"{status_string(status)}: {last_error()}")
 
 
-def _i32_array(values: Sequence[int]):
-    vals = [int(v) for v in values]
-    return (ctypes.c_int32 * max(1, len(vals)))(*vals)
+def _i32_array(values):
+    """An int32* argument over values (an int sequence, a numpy array or a CPU
+    tensor): a view when they already are contiguous int32, else one
+    vectorised conversion (no per-element Python loop). Values outside int32
+    raise ValueError. The returned pointer keeps its array alive."""
+    import numpy as np
+    if hasattr(values, "detach"):   # torch tensor
+        values = values.detach().cpu().numpy()
+    a = np.asarray(values).reshape(-1)
+    if a.dtype != np.int32:
+        if a.size and (a.dtype.kind not in "iu" or int(a.min()) < -2 ** 31 or int(a.max()) > 2 ** 31 - 1):
+            raise ValueError("expected integers that fit int32")
+        a = a.astype(np.int32)
+    a = np.ascontiguousarray(a) if a.size else np.zeros(1, dtype=np.int32)
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
 
 
 class Plan:
@@ -256,13 +268,13 @@ def make_opts(**kw) -> PlanOpts:
 
 def flex_attn_plan(shape: Shape, opts: Optional[PlanOpts], query_start_loc: Sequence[int],
                    seq_lens: Sequence[int], max_pages_per_seq: int) -> Plan:
-    """Host plan (no HIP call). Raises FlexAttnError with the library's status on failure."""
-    qsl = [int(x) for x in query_start_loc]
-    sl = [int(x) for x in seq_lens]
+    """Host plan (no HIP call). query_start_loc and seq_lens: int sequences,
+    numpy arrays or CPU tensors. Raises FlexAttnError with the library's
+    status on failure."""
     out = ctypes.c_void_p()
     st = lib().flex_attn_plan(ctypes.byref(shape), ctypes.byref(opts) if opts is not None else None,
-                              len(sl), _i32_array(qsl), _i32_array(sl), int(max_pages_per_seq),
-                              ctypes.byref(out))
+                              len(seq_lens), _i32_array(query_start_loc), _i32_array(seq_lens),
+                              int(max_pages_per_seq), ctypes.byref(out))
     check(st, "flex_attn_plan")
     return Plan(out.value)
 
@@ -270,11 +282,9 @@ def flex_attn_plan(shape: Shape, opts: Optional[PlanOpts], query_start_loc: Sequ
 def plan_status(shape: Shape, opts: Optional[PlanOpts], query_start_loc, seq_lens, max_pages_per_seq) -> int:
     """Status code of flex_attn_plan for these inputs (the plan, if any, is freed)."""
     out = ctypes.c_void_p()
-    qsl = list(query_start_loc)
-    sl = list(seq_lens)
     st = lib().flex_attn_plan(ctypes.byref(shape), ctypes.byref(opts) if opts is not None else None,
-                              len(sl), _i32_array(qsl), _i32_array(sl), int(max_pages_per_seq),
-                              ctypes.byref(out))
+                              len(seq_lens), _i32_array(query_start_loc), _i32_array(seq_lens),
+                              int(max_pages_per_seq), ctypes.byref(out))
     if st == FLEX_OK:
         lib().flex_attn_plan_destroy(out)
     return st
@@ -373,8 +383,8 @@ def flex_attn_validate_host(plan: Plan, block_table, num_pages: int, seq_lens, q
     if bt.dim() != 2:
         raise ValueError("block_table must be 2-D")
     ptr = ctypes.cast(bt.data_ptr(), ctypes.POINTER(ctypes.c_int32))
-    check(lib().flex_attn_validate_host(plan.handle, ptr, bt.stride(0), int(num_pages), _i32_array(list(seq_lens)),
-                                        _i32_array(list(query_start_loc))), "flex_attn_validate_host")
+    check(lib().flex_attn_validate_host(plan.handle, ptr, bt.stride(0), int(num_pages), _i32_array(seq_lens),
+                                        _i32_array(query_start_loc)), "flex_attn_validate_host")
 
 
 def set_debug(level: int) -> int:

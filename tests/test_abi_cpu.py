@@ -275,3 +275,21 @@ def test_binding_refuses_wrong_dtypes_and_layouts():
         F.make_args(q.transpose(0, 1), k, k, bt, sl, qsl, out)
     with pytest.raises(ValueError, match="innermost"):
         F.make_args(q, k.transpose(2, 3), k, bt, sl, qsl, out)
+
+
+def test_plan_takes_lists_arrays_and_tensors_alike():
+    """The binding passes int32 metadata without a per-element copy; lists,
+    numpy arrays and CPU tensors give the same plan words, and values that do
+    not fit int32 are refused before the library sees them."""
+    import numpy as np
+    import torch
+    shape = F.make_shape(8, 2, 64, 64, 16, 0.125, False)
+    qsl, sl = [0, 1, 40, 41], [300, 40, 900]
+    words = F.flex_attn_plan(shape, None, qsl, sl, 64).export()
+    assert F.flex_attn_plan(shape, None, np.array(qsl, dtype=np.int64), np.array(sl), 64).export() == words
+    assert F.flex_attn_plan(shape, None, torch.tensor(qsl, dtype=torch.int32),
+                            torch.tensor(sl, dtype=torch.int32), 64).export() == words
+    with pytest.raises(ValueError):
+        F.flex_attn_plan(shape, None, qsl, [300, 40, 2 ** 31], 64)
+    with pytest.raises(ValueError):
+        F.flex_attn_plan(shape, None, [0.0, 1.0, 40.0, 41.0], sl, 64)
