@@ -4,7 +4,8 @@
 // decode_gqa_kernel   decode phase, grouped-query heads (head dim 64 / 128):
 //                     one work-group per (decode item, KV head); its waves take
 //                     32-key chunks of the item's key range in turn, streaming
-//                     K and V straight from HBM into registers.
+//                     K and V from HBM into registers (K through a wave-private
+//                     LDS buffer that turns whole-line loads into MFMA rows).
 // rowpar_kernel       prefill phase (all layouts) and decode of the 576/512
 //                     latent layout: each wave owns 16 or 32 query rows; the
 //                     work-group streams key tiles, gathered through the block
@@ -157,14 +158,38 @@ __device__ __forceinline__ u32x4 softmax_chunk(const f32x4 (&s)[2], bool masked,
 // boundaries. When a wave leaves a piece it writes that piece's output (whole
 // sequence) or partial (split sequence), combining through LDS first when a
 // head has several waves.
+//
+// K reads: the A operand of S^T = K Q^T puts key n of a 16-key block in lane
+// n of every lane group, so a load straight into operand layout spans 16
+// keys x 64 bytes per instruction: half of each 128-byte line, which on a CU
+// share streams at about 60% of the rate of whole-line reads. Each K load
+// instruction instead reads 8 keys x 128 contiguous bytes (lane 8q + x: key
+// q, 16-byte chunk x of one half row; at head dim 128 the two lane octets of
+// a key pair take opposite halves so the LDS writes below are conflict free),
+// and the chunk passes through the wave's own 32-key LDS buffer (rows
+// XOR-swizzled by 16-byte chunk) on its way to the MFMA. V loads already
+// cover whole rows (4 keys x 256 bytes per instruction at head dim 128).
 // ---------------------------------------------------------------------------
 template <int D>
 struct DecodeChunk {
   static constexpr int DC = D / 32;
   using VRow = typename std::conditional<D == 128, u32x4, u32x2>::type;
-  u32x4 k[2][DC];   // A operand rows: key 16b + n, dims 32c + 8gq .. +8
+  u32x4 k[2][DC];   // K of 16-key block b, load t: key 16b + kkey(t), chunk kchunk(t)
   VRow v[8];        // value dims DPL*n .. of the lane's 8 keys
 };
+
+// Bytes of one wave's K staging buffer (32 keys).
+template <int D>
+constexpr int decode_kstage_bytes() { return 32 * D * 2; }
+
+// Physical 16-byte chunk of logical chunk x in key row r of a K staging
+// buffer: reads of one chunk by the 16 lanes of a lane group, and the
+// whole-line writes, hit 16 distinct 16-byte bank groups.
+template <int D>
+__device__ __forceinline__ int decode_kswz(int x, int r) {
+  if constexpr (D == 128) return x ^ (r & 15);
+  else return x ^ ((r >> 1) & 7);
+}
 
 // Position in a wave's chunk stream: piece i (plan item), chunk ci of it, and
 // the piece's first entry in the LDS page window. Wave-uniform.
@@ -175,12 +200,13 @@ struct DecodeCursor {
 __device__ __forceinline__ int pages_in(int k0, int k1, int P) { return (k1 - 1) / P - k0 / P + 1; }
 
 // One decode work-group's work: balanced range `range` (-1: none) of the
-// plan, column `col` of W, with threads tid = 0 .. NW*64-1 and the range's
-// block-table window at s_pt. Every call passes exactly one work-group
-// barrier (two or more per piece with COMBINE).
+// plan, column `col` of W, with threads tid = 0 .. NW*64-1, the range's
+// block-table window at s_pt and NW K staging buffers at s_kst (16-byte
+// aligned). Every call passes exactly one work-group barrier (two or more
+// per piece with COMBINE).
 template <int D, int NW, int P, bool COMBINE, bool NT>
 __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, int col, int W, int tid,
-                                                int* s_pt) {
+                                                int* s_pt, uint8_t* s_kst) {
   // K/V loads marked non-temporal when the launch has the whole device: with
   // every CU streaming the cache this measured 12% faster (6.2 vs 5.6 TB/s),
   // on a half-device co-run share it measured slower.
@@ -205,8 +231,22 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
   const uint8_t* vbase_b = reinterpret_cast<const uint8_t*>(p.vc.base + int64_t(active ? g : 0) * p.vc.sh);
   const uint32_t ksp_b = uint32_t(p.kc.sp) * 2u, kss_b = uint32_t(p.kc.ss) * 2u;
   const uint32_t vsp_b = uint32_t(p.vc.sp) * 2u, vss_b = uint32_t(p.vc.ss) * 2u;
-  const uint32_t k_lane = uint32_t(n) * kss_b + 16u * gq;
   const uint32_t v_lane = uint32_t(4 * gq) * vss_b + 2u * DPL * n;
+  // K load t of a 16-key block: key kkey, 16-byte chunk kchunk of that key's
+  // row (global byte offset k_lane[t], staging offset k_wr[t]); operand read
+  // cc: key n, chunk 4cc + gq (staging offset k_rd[cc]).
+  constexpr int KROW = 2 * D;
+  uint8_t* const kst = s_kst + w * decode_kstage_bytes<D>();
+  uint32_t k_lane[DC], k_wr[DC], k_rd[DC];
+#pragma unroll
+  for (int t = 0; t < DC; ++t) {
+    const int q8 = lane >> 3, x8 = lane & 7;
+    const int kkey = D == 128 ? 8 * (t & 1) + q8 : 8 * t + q8;
+    const int kchunk = D == 128 ? 8 * ((t >> 1) ^ (q8 & 1)) + x8 : x8;
+    k_lane[t] = uint32_t(kkey) * kss_b + 16u * uint32_t(kchunk);
+    k_wr[t] = uint32_t(kkey * KROW + 16 * decode_kswz<D>(kchunk, kkey));
+    k_rd[t] = uint32_t(n * KROW + 16 * decode_kswz<D>(4 * t + gq, n));
+  }
   __shared__ float s_m[NW][16];
   __shared__ float s_l[NW][16];
   __shared__ float s_o[COMBINE ? NW : 1][16][D];   // wave combine (several waves per head)
@@ -215,9 +255,8 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
   {
     int poff = 0;
     for (int i = i_begin; i < i_end; ++i) {
-      const int32_t* it = p.items + 8 * i;
-      const int k0 = it[3], k1 = it[4];
-      const int32_t* bt_row = p.bt + int64_t(it[0]) * p.bt_stride + k0 / P;
+      const int k0 = scalar_word(p.items, 8 * i + 3), k1 = scalar_word(p.items, 8 * i + 4);
+      const int32_t* bt_row = p.bt + int64_t(scalar_word(p.items, 8 * i)) * p.bt_stride + k0 / P;
       const int npg = pages_in(k0, k1, P);
       for (int t = tid; t < npg; t += NW * 64) s_pt[poff + t] = bt_row[t];
       poff += npg;
@@ -227,10 +266,9 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
   // First piece at or after i (window offset poff) in which this wave has a chunk.
   auto open = [&](DecodeCursor& c, int i, int poff) {
     for (; active && i < i_end; ++i) {
-      const int32_t* it = p.items + 8 * i;
-      const int k0 = it[3], k1 = it[4];
+      const int k0 = scalar_word(p.items, 8 * i + 3), k1 = scalar_word(p.items, 8 * i + 4);
       if (u * 32 < k1 - k0) {
-        c = DecodeCursor{i, u, it[0], k0, k1, poff};
+        c = DecodeCursor{i, u, scalar_word(p.items, 8 * i), k0, k1, poff};
         return;
       }
       poff += pages_in(k0, k1, P);
@@ -244,8 +282,13 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
 
   // K/V loads of one chunk through buffer resources built per 16-key half
   // from scalar page bases; the record count ends at the piece's last key,
-  // so loads past it read zeros and never touch memory.
+  // so loads past it read zeros and never touch memory. A cursor past the
+  // end of the range still issues every load, with empty resources: the
+  // same instruction stream on every path lets the compiler's wait counts
+  // leave the next chunk's loads in flight (a conditional prefetch makes it
+  // wait as if none had been issued).
   auto load = [&](Chunk& c, const DecodeCursor& cur) {
+    const bool live = cur.i < i_end;
     const int kc0 = cur.k0 + 32 * cur.ci;
     __amdgpu_buffer_rsrc_t kr[2], vr[2];
 #pragma unroll
@@ -253,8 +296,8 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
       const int key = kc0 + 16 * b;
       // (readfirstlane keeps resources in scalar registers: one the compiler
       // sees in vector registers becomes a loop.)
-      const uint32_t nvalid = uint32_t(__builtin_amdgcn_readfirstlane(min(max(cur.k1 - key, 0), 16)));
-      const int pidx = cur.poff + min(key, cur.k1 - 1) / P - cur.k0 / P;
+      const uint32_t nvalid = uint32_t(__builtin_amdgcn_readfirstlane(live ? min(max(cur.k1 - key, 0), 16) : 0));
+      const int pidx = live ? cur.poff + min(key, cur.k1 - 1) / P - cur.k0 / P : 0;
       const uint32_t pg = uint32_t(__builtin_amdgcn_readfirstlane(s_pt[pidx]));
       const uint32_t slot = uint32_t(key % P);
       kr[b] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(kbase_b + (uint64_t(pg) * ksp_b + slot * kss_b)),
@@ -266,7 +309,7 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int cc = 0; cc < DC; ++cc)
-        c.k[b][cc] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr[b], int(k_lane + 64u * cc), 0, kLoadAux));
+        c.k[b][cc] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr[b], int(k_lane[cc]), 0, kLoadAux));
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int off = int(v_lane + uint32_t(e & 3) * vss_b);
@@ -282,7 +325,7 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
   u32x4 qop[DC];
   int q_piece = -1;
   auto load_q = [&](int i) {
-    const int tok = p.items[8 * i + 6];
+    const int tok = scalar_word(p.items, 8 * i + 6);
     const bool ok = n < G;
     const uint16_t* qr = p.q + (int64_t(tok) * p.Hq + g * G + (ok ? n : 0)) * D + 8 * gq;
 #pragma unroll
@@ -297,13 +340,24 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
 
   auto compute = [&](const Chunk& c, const DecodeCursor& cur) {
     const int kc0 = cur.k0 + 32 * cur.ci;
+    // K rows into the staging buffer and back in operand layout. Only this
+    // wave touches its buffer and a wave's LDS accesses run in order; the
+    // wave barrier keeps the compiler from moving the reads above the writes
+    // (or the next chunk's writes above these reads).
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < DC; ++t) *reinterpret_cast<u32x4*>(kst + k_wr[t] + 16 * KROW * b) = c.k[b][t];
+    wave_lds_sync();
     f32x4 s[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int cc = 0; cc < DC; ++cc) s[b] = mfma_16x16x32(c.k[b][cc], qop[cc], s[b]);
+      for (int cc = 0; cc < DC; ++cc)
+        s[b] = mfma_16x16x32(*reinterpret_cast<const u32x4*>(kst + k_rd[cc] + 16 * KROW * b), qop[cc], s[b]);
     }
+    wave_lds_sync();
     const u32x4 pop = softmax_chunk<DPL>(s, kc0 + 32 > cur.k1, kc0, cur.k1, gq, p.scale_log2, m, l, o);
     u32x4 vop[DPL];
     if constexpr (D == 128) transpose8x8(c.v, vop);
@@ -318,10 +372,9 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
   // Lane (n, gq) holds rows 4gq + r of the accumulators at value dims
   // DPL*n .. DPL*n + DPL - 1.
   auto finish = [&](int i) {
-    const int32_t* it = p.items + 8 * i;
-    const int nspl = it[2];
-    const int tok = it[6];
-    const int64_t slot = int64_t(it[7]) * W + col;   // this piece's workspace slot
+    const int nspl = scalar_word(p.items, 8 * i + 2);
+    const int tok = scalar_word(p.items, 8 * i + 6);
+    const int64_t slot = int64_t(scalar_word(p.items, 8 * i + 7)) * W + col;   // this piece's workspace slot
     const float ltot = group_sum(l);
     if constexpr (!COMBINE) {   // one wave per head
       if (active) {
@@ -417,7 +470,7 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
     if (q_piece != i) load_q(i);
   };
 
-  DecodeCursor c;
+  DecodeCursor c{i_end, 0, 0, 0, 0, 0};
   open(c, i_begin, 0);
   if (c.i < i_end) load_q(c.i);
   wait_vmem_all();
@@ -425,20 +478,25 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
 
   // Two fixed chunk buffers, the loop unrolled by two: the next chunk's loads
   // stay in flight during this chunk's math (a register copy between
-  // iterations would force them to land first).
+  // iterations would force them to land first). Vector loads retire in
+  // order, so everything a chunk's math waits for is issued before the next
+  // chunk's loads: the piece change (outputs of finished pieces, Q of the
+  // new one) comes first. (With the Q reload issued after them, the wait for
+  // Q, merged over both paths of its branch, drained the prefetch at every
+  // chunk.)
   Chunk A, B;
-  if (c.i < i_end) load(A, c);
+  load(A, c);
   while (c.i < i_end) {
+    enter(c.i);
     DecodeCursor c2 = c;
     advance(c2);
-    if (c2.i < i_end) load(B, c2);
-    enter(c.i);
+    load(B, c2);
     compute(A, c);
     if (c2.i >= i_end) break;
+    enter(c2.i);
     DecodeCursor c3 = c2;
     advance(c3);
-    if (c3.i < i_end) load(A, c3);
-    enter(c2.i);
+    load(A, c3);
     compute(B, c2);
     c = c3;
   }
@@ -448,9 +506,10 @@ __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, 
 template <int D, int NW, int P, bool COMBINE, bool NT>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void decode_gqa_kernel(AttnParams p) {
-  extern __shared__ int s_pt[];   // block-table entries of the range
+  // The waves' K staging buffers, then the range's block-table entries.
+  extern __shared__ __attribute__((aligned(16))) uint8_t s_dyn[];
   decode_gqa_body<D, NW, P, COMBINE, NT>(p, int(blockIdx.x), int(blockIdx.y), int(gridDim.y), int(threadIdx.x),
-                                         s_pt);
+                                         reinterpret_cast<int*>(s_dyn + NW * decode_kstage_bytes<D>()), s_dyn);
 }
 
 // ---------------------------------------------------------------------------
@@ -1197,8 +1256,10 @@ void fused_kernel(AttnParams pp, AttnParams pd, const int32_t* order) {
   constexpr int DNW = 8 / RPW;
   const int sub = int(threadIdx.x) / (DNW * 64);
   const int r = RPW * j + sub;
-  decode_gqa_body<D, DNW, P, false, false>(pd, r < pd.n_ranges ? r : -1, 0, 1, int(threadIdx.x) % (DNW * 64),
-                                           reinterpret_cast<int*>(lds) + sub * pd.range_pages);
+  decode_gqa_body<D, DNW, P, false, false>(
+      pd, r < pd.n_ranges ? r : -1, 0, 1, int(threadIdx.x) % (DNW * 64),
+      reinterpret_cast<int*>(lds + 8 * decode_kstage_bytes<D>()) + sub * pd.range_pages,
+      lds + sub * DNW * decode_kstage_bytes<D>());
 }
 
 template <int D, int P, int RPW>
@@ -1206,7 +1267,7 @@ static hipError_t launch_fused_t(const AttnParams& pp, const AttnParams& pd, con
                                  hipStream_t stream) {
   constexpr int NS = D == 128 ? 3 : 4;
   using C = RowParCfg<D, D, 8, 2, 64, false, NS>;
-  const size_t dec_lds = size_t(RPW) * size_t(pd.range_pages) * 4;
+  const size_t dec_lds = 8 * size_t(decode_kstage_bytes<D>()) + size_t(RPW) * size_t(std::max(pd.range_pages, 1)) * 4;
   const size_t lds = C::LDS_BYTES > dec_lds ? C::LDS_BYTES : dec_lds;
   auto kern = fused_kernel<D, P, RPW>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -1346,25 +1407,26 @@ static hipError_t launch_rowpar(const AttnParams& p, dim3 grid, hipStream_t stre
 
 template <int D, int P>
 static hipError_t launch_decode_gqa(const AttnParams& p, hipStream_t stream) {
-  // One work-group per (balanced range, KV head); the range's block-table
-  // entries take dynamic LDS.
+  // One work-group per (balanced range, KV head); the waves' K staging
+  // buffers and the range's block-table entries take dynamic LDS.
   // Four waves when the work-group serves at most four KV heads, else eight
   // (one per head).
   const dim3 grid(p.n_ranges, p.grid_y);
-  const size_t window = size_t(p.range_pages) * 4;
+  const size_t window = size_t(std::max(p.range_pages, 1)) * 4;   // a dead cursor reads entry 0
   const int hw = p.rows_per_wg / p.G;
   const bool nt = p.whole_device != 0;
-  if (hw <= 2) {   // several waves per head, combined through LDS
-    if (nt) hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P, true, true>), grid, dim3(256), window, stream, p);
-    else hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P, true, false>), grid, dim3(256), window, stream, p);
-  } else if (hw <= 4) {
-    if (nt) hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P, false, true>), grid, dim3(256), window, stream, p);
-    else hipLaunchKernelGGL((decode_gqa_kernel<D, 4, P, false, false>), grid, dim3(256), window, stream, p);
-  } else {
-    if (nt) hipLaunchKernelGGL((decode_gqa_kernel<D, 8, P, false, true>), grid, dim3(512), window, stream, p);
-    else hipLaunchKernelGGL((decode_gqa_kernel<D, 8, P, false, false>), grid, dim3(512), window, stream, p);
-  }
-  return hipGetLastError();
+  auto go = [&](auto kern, int nw) {
+    const size_t lds = size_t(nw) * decode_kstage_bytes<D>() + window;
+    const hipError_t attr = set_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
+    if (attr != hipSuccess) return attr;
+    hipLaunchKernelGGL(kern, grid, dim3(nw * 64), lds, stream, p);
+    return hipGetLastError();
+  };
+  if (hw <= 2)   // several waves per head, combined through LDS
+    return nt ? go(decode_gqa_kernel<D, 4, P, true, true>, 4) : go(decode_gqa_kernel<D, 4, P, true, false>, 4);
+  if (hw <= 4)
+    return nt ? go(decode_gqa_kernel<D, 4, P, false, true>, 4) : go(decode_gqa_kernel<D, 4, P, false, false>, 4);
+  return nt ? go(decode_gqa_kernel<D, 8, P, false, true>, 8) : go(decode_gqa_kernel<D, 8, P, false, false>, 8);
 }
 
 static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t stream) {

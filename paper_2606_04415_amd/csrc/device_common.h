@@ -48,6 +48,25 @@ __device__ __forceinline__ void lds_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// Order one wave's LDS accesses around an exchange between its own lanes: a
+// wave's LDS instructions execute in issue order, so the barrier only has to
+// stop the compiler from moving accesses across it.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Word idx of an array the kernel only reads, through a scalar load (the
+// index is made wave-uniform): scalar loads are counted apart from vector
+// memory, so reading plan metadata does not wait for the K/V loads in
+// flight, which a vector load issued after them would (vector loads retire
+// in order).
+typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
+__device__ __forceinline__ int32_t scalar_word(const int32_t* base, int idx) {
+  return ((const_i32_ptr)(base))[__builtin_amdgcn_readfirstlane(idx)];
+}
+
 // Let every outstanding vector-memory access land (placed after loads issued
 // before a pipelined loop, so loop-carried wait tracking starts clean).
 __device__ __forceinline__ void wait_vmem_all() { wait_vmem<0>(); }

@@ -65,6 +65,17 @@ def test_ragged_gqa_d128_page16(min_split):
     full_check(b, opts, "ragged-d128")
 
 
+def test_decode_ranges_cross_many_pieces():
+    """48 decodes of 1 to ~300 keys planned for a 32-CU share: each balanced
+    range spans many pieces, so a wave changes piece (finishes one, loads the
+    next one's Q) between most chunks, and a wave's prefetch often runs past
+    the end of its range."""
+    ls = [1 + (37 * i) % 300 for i in range(48)]
+    b = custom_batch(QW, [1] * 48, ls, seed=8)
+    log("48 short decodes, ranges planned for 32 CUs")
+    full_check(b, F.make_opts(cus_decode=32, min_split_tokens=16), "many-pieces")
+
+
 def test_ragged_gqa_d64_page64_group16():
     ns = [1, 1, 1, 70, 1, 130, 3]
     ls = [1, 63, 65, 70, 2000, 400, 3]
