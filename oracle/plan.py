@@ -43,8 +43,9 @@ the contract is:
   sequence has n * G rows; tile rows [t*BM, min(n*G, (t+1)*BM)), key_end =
   L - n + (row_end - 1) // G + 1 (the causal limit of the last row's token);
   one work-group per (tile, KV head), Hkv of them. With BM unset the
-  grouped-query default is 128 when sum over prefill sequences of
-  ceil(n * G / 128) * Hkv >= 4 * cus_prefill, else 32.
+  grouped-query default is 128 when F = sum over prefill sequences of
+  ceil(n * G / 128) * Hkv satisfies F >= 4 * cus_prefill, or
+  F <= 3 * cus_prefill with cus_prefill < cus_total (a co-run share), else 32.
 * co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
   the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
   prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
@@ -222,11 +223,13 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     cus_prefill = cus_total - cus_decode if (dec and pre and cus_decode < cus_total) else cus_total
 
     # --- grouped-query tile height: 128 flat rows when every prefill CU gets at least
-    # four such work-groups, else 32 tokens
+    # four such work-groups or, on a co-run share, when all of them fit in one
+    # round (three per CU), else 32 tokens
     G = sh.num_q_heads // sh.num_kv_heads
     if bm == 0:
         flat_wgs = sum(cdiv((qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads for s in pre)
-        bm = 128 if flat_wgs >= 4 * cus_prefill else 32
+        share = cus_prefill < cus_total
+        bm = 128 if (flat_wgs >= 4 * cus_prefill or (share and flat_wgs <= 3 * cus_prefill)) else 32
     flat = not mla and not split and bm == 128   # rows are (token, query head) pairs of one KV head
 
     # --- decode partition: balanced page ranges over the concatenated decode sequences

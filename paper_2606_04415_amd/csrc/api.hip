@@ -158,7 +158,6 @@ int run_decode(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args*
   p.merge = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_MERGE];
   p.n_merge = info.n_split_seqs;
   p.range_pages = info.pages_per_split;
-  p.whole_device = info.cus_decode >= plan->cus_total ? 1 : 0;
   p.grid_y = info.decode_wg_width;
   const hipError_t e = launch_decode(p, plan->shape.head_dim_qk, info.n_split_seqs > 0, s);
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "decode launch");

@@ -207,9 +207,8 @@ __device__ __forceinline__ int pages_in(int k0, int k1, int P) { return (k1 - 1)
 template <int D, int NW, int P, bool COMBINE, bool NT>
 __device__ __forceinline__ void decode_gqa_body(const AttnParams& p, int range, int col, int W, int tid,
                                                 int* s_pt, uint8_t* s_kst) {
-  // K/V loads marked non-temporal when the launch has the whole device: with
-  // every CU streaming the cache this measured 12% faster (6.2 vs 5.6 TB/s),
-  // on a half-device co-run share it measured slower.
+  // K/V loads marked non-temporal (read once, never reused): 7% faster on a
+  // 96- or 128-CU share and 12% on the whole device than plain loads.
   constexpr int kLoadAux = NT ? 2 : 0;
   static_assert(D == 64 || D == 128, "head dim");
   constexpr int DC = D / 32;   // 32-dim chunks of the QK^T contraction
@@ -1237,8 +1236,8 @@ void flat_prefill_kernel(AttnParams p) {
 // (RPW = 2) or one 8-wave body (RPW = 1). Prefill and decode work-groups
 // share the device in the proportion the order interleaves them, instead
 // of two CU-masked streams; the dispatcher hands work-groups out in id
-// order as compute units free up. Decode K/V loads are plain (the phase
-// never has the whole device to itself). Entries < 0 are padding.
+// order as compute units free up. Decode K/V loads are non-temporal, as in
+// the decode kernel. Entries < 0 are padding.
 // ---------------------------------------------------------------------------
 template <int D, int P, int RPW>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
@@ -1256,7 +1255,7 @@ void fused_kernel(AttnParams pp, AttnParams pd, const int32_t* order) {
   constexpr int DNW = 8 / RPW;
   const int sub = int(threadIdx.x) / (DNW * 64);
   const int r = RPW * j + sub;
-  decode_gqa_body<D, DNW, P, false, false>(
+  decode_gqa_body<D, DNW, P, false, true>(
       pd, r < pd.n_ranges ? r : -1, 0, 1, int(threadIdx.x) % (DNW * 64),
       reinterpret_cast<int*>(lds + 8 * decode_kstage_bytes<D>()) + sub * pd.range_pages,
       lds + sub * DNW * decode_kstage_bytes<D>());
@@ -1414,7 +1413,6 @@ static hipError_t launch_decode_gqa(const AttnParams& p, hipStream_t stream) {
   const dim3 grid(p.n_ranges, p.grid_y);
   const size_t window = size_t(std::max(p.range_pages, 1)) * 4;   // a dead cursor reads entry 0
   const int hw = p.rows_per_wg / p.G;
-  const bool nt = p.whole_device != 0;
   auto go = [&](auto kern, int nw) {
     const size_t lds = size_t(nw) * decode_kstage_bytes<D>() + window;
     const hipError_t attr = set_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
@@ -1422,11 +1420,9 @@ static hipError_t launch_decode_gqa(const AttnParams& p, hipStream_t stream) {
     hipLaunchKernelGGL(kern, grid, dim3(nw * 64), lds, stream, p);
     return hipGetLastError();
   };
-  if (hw <= 2)   // several waves per head, combined through LDS
-    return nt ? go(decode_gqa_kernel<D, 4, P, true, true>, 4) : go(decode_gqa_kernel<D, 4, P, true, false>, 4);
-  if (hw <= 4)
-    return nt ? go(decode_gqa_kernel<D, 4, P, false, true>, 4) : go(decode_gqa_kernel<D, 4, P, false, false>, 4);
-  return nt ? go(decode_gqa_kernel<D, 8, P, false, true>, 8) : go(decode_gqa_kernel<D, 8, P, false, false>, 8);
+  if (hw <= 2) return go(decode_gqa_kernel<D, 4, P, true, true>, 4);   // several waves per head, combined through LDS
+  if (hw <= 4) return go(decode_gqa_kernel<D, 4, P, false, true>, 4);
+  return go(decode_gqa_kernel<D, 8, P, false, true>, 8);
 }
 
 static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t stream) {

@@ -63,6 +63,8 @@ constexpr int kFusedMinKvHeads = 3;
 // Most pages one balanced decode range may hold (its block-table entries are
 // staged in LDS by the decode kernel).
 constexpr int64_t kMaxRangePages = 8192;
+// Flat 128-row prefill work-groups resident on one CU (50 KB of LDS each).
+constexpr int64_t kFlatResidentPerCu = 3;
 
 // KV heads one grouped-query decode work-group covers (one wave each, or
 // several waves per head when fewer heads than 4).

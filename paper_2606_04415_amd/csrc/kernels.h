@@ -36,7 +36,6 @@ struct AttnParams {
   int32_t rows_per_wg;    // decode rows owned by one work-group
   int32_t grid_y;
   int32_t xcd_remap;      // prefill: 1-D grid mapped so each XCD serves one column
-  int32_t whole_device;   // decode: the plan partitions decode for every CU
   float scale_log2;       // sm_scale * log2(e)
 };
 

@@ -222,13 +222,16 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   // Grouped-query prefill tiles: 128 flattened rows (a row is a (token,
   // query head) pair of one KV head, token-major: every 16-row block of a
   // wave is full whatever the group size) when the batch gives every
-  // prefill CU at least four such work-groups; else 32 tokens, whose larger
-  // work-groups fill a CU one at a time and leave no ragged last round on
-  // small batches.
+  // prefill CU at least four such work-groups, or, on a co-run share, when
+  // they all fit in one round (three flat work-groups are resident per CU);
+  // else 32 tokens, whose larger work-groups fill a CU one at a time and
+  // leave no short last round. (On the whole device the one-round case runs
+  // alike either way, and 32-token tiles keep the one-launch order.)
   if (bm == 0) {
     int64_t flat_wgs = 0;
     for (int32_t s : pre) flat_wgs += cdiv(int64_t(qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads;
-    bm = flat_wgs >= 4 * cus_prefill ? 128 : 32;
+    const bool share = cus_prefill < cus_total;
+    bm = flat_wgs >= 4 * cus_prefill || (share && flat_wgs <= kFlatResidentPerCu * cus_prefill) ? 128 : 32;
   }
   const bool flat = !latent && !split && bm == 128;
   const int32_t pre_grid_y =

@@ -101,7 +101,8 @@ def check_invariants(sh, opts, qsl, ls, maxp):
     flat = sh.head_dim_qk in (64, 128) and bm == 128
     if sh.head_dim_qk in (64, 128) and not (o.bm or 0):   # default tile height
         flat_wgs = sum(-(-(qsl[s + 1] - qsl[s]) * G // 128) * sh.num_kv_heads for s in pre)
-        assert bm == (128 if flat_wgs >= 4 * b[13] else 32)
+        share = b[13] < (o.cus_total or 256)
+        assert bm == (128 if (flat_wgs >= 4 * b[13] or (share and flat_wgs <= 3 * b[13])) else 32)
     assert b[8] == (sh.num_kv_heads if flat else b[8])
     rows = {}
     for it in pre_items:
