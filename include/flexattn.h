@@ -89,20 +89,28 @@ typedef struct flex_attn_shape {
  * multiples of split_granule from the rates below. */
 typedef struct flex_attn_plan_opts {
   int32_t cus_total;          /* [256] */
-  int32_t cus_decode;         /* [0 = all CUs] */
+  int32_t cus_decode;         /* CUs of the co-run decode share [0 = all CUs: no share];
+                                 -1: the cost model's best multiple of split_granule */
   int32_t bm;                 /* prefill rows per tile. Grouped-query: 16 or 32 tokens, or 128
                                  flattened rows, each a (token, query head) pair of one KV head
                                  [128 when the batch gives every prefill CU at least four
-                                 such 128-row work-groups, else 32]; 576/512: 64 or 128 tokens
-                                 [128]; 192/128: 128 [128] */
+                                 such 128-row work-groups, or, on a co-run share, when all of
+                                 them fit in one round (three per CU); else 32]; 576/512: 64
+                                 or 128 tokens [128]; 192/128: 128 [128] */
   int32_t min_split_tokens;   /* shortest balanced decode range, in keys [256] */
   int32_t wg_per_cu;          /* decode work-groups aimed at per CU
                                  [1 grouped-query, 2 for 576/512] */
   int32_t split_granule;      /* co-run split granularity in CUs [32] */
-  double hbm_gbps;            /* cost model: device HBM bandwidth [8000] */
-  double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws [37] */
-  double prefill_tflops_per_cu; /* cost model: prefill rate of one CU [4] (both defaults
-                                   measured with half an MI355X running the phase) */
+  double hbm_gbps;            /* cost model: device streaming rate [6500, what decode
+                                 reaches on 160 to 256 CUs] */
+  double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws beside a running
+                                 prefill [43] */
+  double prefill_tflops_per_cu; /* cost model: prefill rate of one CU [4] (defaults measured
+                                   on MI355X, the Qwen2.5-7B-shaped mixed step) */
+  int32_t decode_tail;        /* 0: a grouped-query co-run plan splits its decode pages in
+                                 two groups of ranges, the second (the tail) run on the
+                                 prefill stream after the prefill (see flex_attn_mixed);
+                                 -1: no tail [0] */
 } flex_attn_plan_opts;
 
 /* Summary of a plan. */
@@ -127,6 +135,10 @@ typedef struct flex_attn_plan_info {
   double prefill_flops;      /* algorithmic flops of the prefill phase */
   int32_t n_fused_wgs;       /* work-groups of the one-launch (FUSED) form; 0 when the
                                 shape has none (see flex_attn_mixed) */
+  int32_t n_decode_tail_ranges; /* the last ranges of the n_decode_ranges, which CORUN runs
+                                   on the prefill stream after the prefill; 0: no tail */
+  double decode_tail_bytes;  /* algorithmic KV bytes of those ranges (the CORUN decode
+                                phase streams decode_bytes - decode_tail_bytes) */
 } flex_attn_plan_info;
 
 /* Device tensors of one run. Strides are in elements.
@@ -256,7 +268,11 @@ int flex_attn_prefill(const flex_attn_plan_t* plan, const flex_attn_args* args, 
  * decode on stream; FLEX_MODE_CORUN forks stream into the two CU-masked
  * streams of corun (prefill on its prefill stream, decode on its decode
  * stream) and joins them back into stream, the one-device analog of the
- * paper's dynamic co-location (Sec. 3.4). The fork and, for steps expected
+ * paper's dynamic co-location (Sec. 3.4). When the plan has a decode tail
+ * (info n_decode_tail_ranges > 0), the decode stream runs the other ranges
+ * and the prefill stream runs the tail's ranges right after the prefill, so
+ * the prefill share streams decode pages once its own phase is done; the
+ * split-K merge then runs on stream after the join. The fork and, for steps expected
  * to run under a millisecond (plan info work on the pair's CU shares), the
  * join are stream memory operations on the pair's step counters; longer
  * steps join through events, which hold no CU while they wait (a memory-value
@@ -448,6 +464,10 @@ typedef struct flex_ctl_signals {
   int32_t pending_decode_seqs;  /* (1)/(4) sequences waiting to decode beyond this step */
   int32_t active_decode_seqs;   /* (4) sequences decoding in this step */
   int32_t fused_available;      /* the step's plan has a one-launch form (n_fused_wgs > 0) */
+  int32_t decode_tail;          /* co-run plans of this step form a decode tail (grouped-query
+                                   heads, plan option decode_tail 0): a co-run step is then
+                                   predicted as the prefill plus decode's rest at the rate
+                                   decode reaches on all CUs, not as the slower phase */
 } flex_ctl_signals;
 
 /* What the last step measured (e.g. flex_attn_corun_timing_read). A

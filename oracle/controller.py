@@ -166,7 +166,8 @@ class Controller:
             self._blend(self.pre, self.n_pre, k, prefill_flops / (prefill_ms * 1e-3) / 1e12)
 
     def decide(self, decode_bytes: float, prefill_flops: float, pending_prefill_tokens: int = 0,
-               pending_decode_seqs: int = 0, active_decode_seqs: int = 1, fused_available: bool = False) -> dict:
+               pending_decode_seqs: int = 0, active_decode_seqs: int = 1, fused_available: bool = False,
+               decode_tail: bool = False) -> dict:
         o, K = self.o, self.K
         self.decisions += 1
         B, F = decode_bytes, prefill_flops
@@ -186,7 +187,15 @@ class Controller:
         pred = {}
         for k in range(1, K + 1):
             td, tp = phase_times(k)
-            pred[k] = max(td, tp) + o.corun_overhead_us if k < K else td + tp
+            if k == K:
+                pred[k] = td + tp
+            elif decode_tail and td > tp:
+                # the co-run decode share streams until the prefill ends; the
+                # rest runs on every CU at the rate decode reaches there
+                bytes_left = B - self.dec[k] * 1e3 * tp
+                pred[k] = tp + bytes_left / (self.dec[K] * 1e3) + o.corun_overhead_us
+            else:
+                pred[k] = max(td, tp) + o.corun_overhead_us
         best = 1
         for k in range(2, K + 1):
             if pred[k] < pred[best]:

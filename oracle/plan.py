@@ -47,8 +47,11 @@ the contract is:
   ceil(n * G / 128) * Hkv satisfies F >= 4 * cus_prefill, or
   F <= 3 * cus_prefill with cus_prefill < cus_total (a co-run share), else 32.
 * co-run CU split: explicit, or (cus_decode = -1) the argmin over multiples of
-  the granule of max(decode_bytes / min(hbm, n_d * bw_cu),
-  prefill_flops / ((cus_total - n_d) * flops_cu)), smallest n_d on ties.
+  the granule of the step time, smallest n_d on ties: with t_p =
+  prefill_flops / ((cus_total - n_d) * flops_cu) and r_s = min(hbm, n_d *
+  bw_cu), max(decode_bytes / r_s, t_p), or, where a decode tail can form
+  (grouped-query heads, decode_tail 0), t_p + max(0, decode_bytes - r_s t_p)
+  / min(hbm, cus_total * bw_cu).
 
 * fused order (one launch for both phases), only for grouped-query heads
   with G > 4, W = 1, 3 <= Hkv <= 8 and BM = 32 (else empty): prefill
@@ -68,9 +71,10 @@ the contract is:
   (decode_gbps_per_cu 1e9). Ties in start time: prefill first, then phase
   order. Entry 8 k + x is the k-th of XCD x's list, -1 past its end.
 
-Blob layout (int32, version 6): 23-word header (word 19: offset of the
+Blob layout (int32, version 7): 24-word header (word 19: offset of the
 merge list, 20: offset of the fused order, 21: its length, 22: offset of the
-lengths), 8 words per decode item, the range table, the piece launch order,
+lengths, 23: ranges of the decode tail, the last ones of the range table),
+8 words per decode item, the range table, the piece launch order,
 the merge list, 8 words per prefill item, the fused order, then seq_lens [B]
 and query_start_loc [B+1] as given; see ``build_plan``.
 """
@@ -82,13 +86,14 @@ from typing import List, Optional, Sequence
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED = 0, -1, -2
 MAGIC = 0x46504C58
-VERSION = 6
-HEADER = 23
+VERSION = 7
+HEADER = 24
 ITEM = 8
 # cost-model rates of one CU when the options leave them 0 (the library's
 # defaults: measured with half of an MI355X running one phase alone)
-DEFAULT_DECODE_GBPS_PER_CU = 37.0
+DEFAULT_DECODE_GBPS_PER_CU = 43.0
 DEFAULT_PREFILL_TFLOPS_PER_CU = 4.0
+DEFAULT_HBM_GBPS = 6500.0
 
 
 def cdiv(a: int, b: int) -> int:
@@ -114,9 +119,10 @@ class Opts:
     min_split_tokens: int = 0    # 0 -> 256
     wg_per_cu: int = 0           # 0 -> 1 (grouped-query), 2 (576/512 latent layout)
     split_granule: int = 0       # 0 -> 32
-    hbm_gbps: float = 0.0        # 0 -> 8000
-    decode_gbps_per_cu: float = 0.0   # 0 -> 37
+    hbm_gbps: float = 0.0        # 0 -> 6500
+    decode_gbps_per_cu: float = 0.0   # 0 -> 43
     prefill_tflops_per_cu: float = 0.0  # 0 -> 4
+    decode_tail: int = 0         # 0 -> a tail group of ranges on grouped-query co-run plans; -1 -> none
 
 
 @dataclass
@@ -169,6 +175,8 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     bm = o.bm or (128 if mla or split else 0)      # grouped-query default chosen after the CU split
     if cus_total < 1 or wg_per_cu < 1 or min_tokens < 1 or granule < 1:
         return PlanResult(ERR_INVALID_ARG)
+    if o.decode_tail not in (0, -1):
+        return PlanResult(ERR_INVALID_ARG)
     if o.cus_decode < -1 or o.cus_decode > cus_total:
         return PlanResult(ERR_INVALID_ARG)
     if (mla and bm not in (64, 128)) or (split and bm != 128) or (
@@ -209,13 +217,20 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     elif o.cus_decode > 0:
         cus_decode = o.cus_decode
     else:
-        hbm = (o.hbm_gbps or 8000.0) * 1e9
+        hbm = (o.hbm_gbps or DEFAULT_HBM_GBPS) * 1e9
         bw_cu = (o.decode_gbps_per_cu or DEFAULT_DECODE_GBPS_PER_CU) * 1e9
         fl_cu = (o.prefill_tflops_per_cu or DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
+        tail_model = not mla and not split and o.decode_tail == 0
+        r_all = min(hbm, float(cus_total) * bw_cu)
         best, best_t = None, None
         nd = granule
         while nd < cus_total:
-            t = max(dec_bytes / min(hbm, nd * bw_cu), pre_flops / ((cus_total - nd) * fl_cu))
+            r_share = min(hbm, float(nd) * bw_cu)
+            t_pre = float(pre_flops) / (float(cus_total - nd) * fl_cu)
+            t = max(float(dec_bytes) / r_share, t_pre)
+            if tail_model:   # the prefill, then decode's rest on the whole device
+                rest = float(dec_bytes) - r_share * t_pre
+                t = t_pre + rest / r_all if rest > 0.0 else t_pre
             if best_t is None or t < best_t:
                 best, best_t = nd, t
             nd += granule
@@ -232,12 +247,39 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         bm = 128 if (flat_wgs >= 4 * cus_prefill or (share and flat_wgs <= 3 * cus_prefill)) else 32
     flat = not mla and not split and bm == 128   # rows are (token, query head) pairs of one KV head
 
-    # --- decode partition: balanced page ranges over the concatenated decode sequences
+    # --- decode partition: balanced page ranges over the concatenated decode sequences;
+    # on a grouped-query co-run share, pages [0, TA) for the decode share and a tail
+    # group [TA, T) sized for the prefill share (run after the prefill), TA from the
+    # cost model: what the decode share covers during the prefill plus its share
+    # of the rest at the device's streaming rate
     min_pps = cdiv(min_tokens, P)
     pages = [cdiv(seq_lens[s], P) for s in dec]
     T = sum(pages)
-    R = max(1, min((cus_decode * wg_per_cu) // W, T // min_pps), cdiv(T, MAX_RANGE_PAGES)) if dec else 0
-    bounds = [(r * T) // R for r in range(R + 1)] if dec else [0]
+    TA = T
+    if not mla and not split and o.decode_tail == 0 and cus_prefill < cus_total and T > 1:
+        hbm = (o.hbm_gbps or DEFAULT_HBM_GBPS) * 1e9
+        bw_cu = (o.decode_gbps_per_cu or DEFAULT_DECODE_GBPS_PER_CU) * 1e9
+        fl_cu = (o.prefill_tflops_per_cu or DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
+        r_share = min(hbm, float(cus_decode) * bw_cu)
+        r_all = min(hbm, float(cus_total) * bw_cu)
+        t_pre = float(pre_flops) / (float(cus_prefill) * fl_cu)
+        during = r_share * t_pre
+        if during < float(dec_bytes):
+            t_rest = (float(dec_bytes) - during) / r_all
+            share_rest = r_all * (float(cus_decode) / float(cus_total)) * t_rest
+            frac = (during + share_rest) / float(dec_bytes)
+            TA = min(T - 1, max(1, math.floor(frac * float(T))))
+    TB = T - TA
+
+    def n_ranges(npages, cus):
+        if npages == 0:
+            return 0
+        return max(1, min((cus * wg_per_cu) // W, npages // min_pps), cdiv(npages, MAX_RANGE_PAGES))
+    RA = n_ranges(TA, cus_decode) if dec else 0
+    RB = n_ranges(TB, cus_prefill) if dec else 0
+    R = RA + RB
+    bounds = ([(r * TA) // RA for r in range(RA + 1)] + [TA + (r * TB) // RB for r in range(1, RB + 1)]
+              if dec else [0])
     start = [0]
     for n_p in pages:
         start.append(start[-1] + n_p)       # first global page of each decode sequence
@@ -259,7 +301,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         for j, i in enumerate(mine):
             dec_items.append((i, [s, j, len(mine), pieces[i][2], pieces[i][3], mine[0], qsl[s], i]))
     dec_items = [it for _, it in sorted(dec_items, key=lambda x: x[0])]
-    ppr = cdiv(T, R) if R else 0
+    ppr = max(cdiv(TA, RA) if RA else 0, cdiv(TB, RB) if RB else 0)
 
     # --- prefill tiles, longest key range first
     tiles = []
@@ -293,7 +335,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     total += 2 * B + 1
     hdr = [MAGIC, VERSION, B, nd_, np_, len(dec), len(pre), W, pre_height,
            HEADER, off_pre, ppr, cus_decode, cus_prefill, bm, total, R, off_ranges, off_order, off_merge,
-           off_fused, len(fused), off_lens]
+           off_fused, len(fused), off_lens, RB]
     blob = (hdr + [x for it in dec_items for x in it] + ranges + order + merge + [x for it in tiles for x in it]
             + fused + list(seq_lens) + list(qsl))
     # workspace: (max, sum) per decode item, column and row, then the partial outputs;

@@ -147,20 +147,41 @@ int debug_validate(const flex_attn_plan_t* plan, const flex_attn_args* a, hipStr
   return FLEX_OK;
 }
 
-int run_decode(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args* a, hipStream_t s) {
+// Which decode ranges a launch covers: all of them (then the merge), or the
+// co-run decode share's part / the tail (no merge; it follows the join).
+enum class DecodePart { all, head, tail };
+
+int run_decode(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args* a, hipStream_t s,
+               DecodePart part = DecodePart::all) {
   const flex_attn_plan_info& info = plan->info;
   if (info.n_decode_items == 0) return FLEX_OK;
+  const int32_t R = plan->words[H_N_RANGES], RB = plan->words[H_N_TAIL_RANGES];
   p.items = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_DEC];
   p.n_items = info.n_decode_items;
   p.ranges = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_RANGES];
-  p.n_ranges = plan->words[H_N_RANGES];
+  p.n_ranges = part == DecodePart::all ? R : part == DecodePart::head ? R - RB : RB;
+  if (part == DecodePart::tail) p.ranges += R - RB;   // (a range reads entries r and r + 1)
   p.order = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_ORDER];
   p.merge = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_MERGE];
   p.n_merge = info.n_split_seqs;
   p.range_pages = info.pages_per_split;
   p.grid_y = info.decode_wg_width;
-  const hipError_t e = launch_decode(p, plan->shape.head_dim_qk, info.n_split_seqs > 0, s);
+  if (p.n_ranges == 0) return FLEX_OK;
+  const hipError_t e =
+      launch_decode(p, plan->shape.head_dim_qk, part == DecodePart::all && info.n_split_seqs > 0, s);
   return e == hipSuccess ? FLEX_OK : hip_fail(e, "decode launch");
+}
+
+int run_decode_merge(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args* a, hipStream_t s) {
+  const flex_attn_plan_info& info = plan->info;
+  if (info.n_decode_items == 0 || info.n_split_seqs == 0) return FLEX_OK;
+  p.items = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_DEC];
+  p.n_items = info.n_decode_items;
+  p.merge = static_cast<const int32_t*>(a->d_plan) + plan->words[H_OFF_MERGE];
+  p.n_merge = info.n_split_seqs;
+  p.grid_y = info.decode_wg_width;
+  const hipError_t e = launch_decode_merge(p, plan->shape.head_dim_qk, s);
+  return e == hipSuccess ? FLEX_OK : hip_fail(e, "merge launch");
 }
 
 int run_prefill(const flex_attn_plan_t* plan, AttnParams p, const flex_attn_args* a, hipStream_t s) {
@@ -363,12 +384,19 @@ int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode
     return hip_fail(e, "fork wait");
   if ((e = hipStreamWaitValue64(corun->decode, f, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
     return hip_fail(e, "fork wait");
+  // With a decode tail, the decode stream takes the other ranges and the
+  // prefill stream the tail's, behind the prefill (outside its timed phase);
+  // the merge follows the join.
+  const bool tail = has_dec && plan->words[H_N_TAIL_RANGES] > 0;
+  auto dec_head = [&](hipStream_t ds) { return run_decode(plan, p, args, ds, DecodePart::head); };
   timing_begin_step(corun);
   st = timed_phase(corun, 0, has_pre, corun->prefill, pre);
   if (st != FLEX_OK) return st;
-  st = timed_phase(corun, 1, has_dec, corun->decode, dec);
+  if (tail && (st = run_decode(plan, p, args, corun->prefill, DecodePart::tail)) != FLEX_OK) return st;
+  st = tail ? timed_phase(corun, 1, has_dec, corun->decode, dec_head) : timed_phase(corun, 1, has_dec, corun->decode, dec);
   if (st != FLEX_OK) return st;
   timing_end_step(corun);
+  auto merge_after_join = [&]() { return tail ? run_decode_merge(plan, p, args, s) : FLEX_OK; };
   if (long_step(plan, corun)) {
     // The runtime serves a memory-value wait on the caller stream with a
     // polling kernel that may run on any CU for the whole step: over
@@ -379,7 +407,7 @@ int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode
     if ((e = hipEventRecord(corun->join_ev[1], corun->decode)) != hipSuccess) return hip_fail(e, "join record");
     if ((e = hipStreamWaitEvent(s, corun->join_ev[0], 0)) != hipSuccess) return hip_fail(e, "join wait");
     if ((e = hipStreamWaitEvent(s, corun->join_ev[1], 0)) != hipSuccess) return hip_fail(e, "join wait");
-    return FLEX_OK;
+    return merge_after_join();
   }
   if ((e = hipStreamWriteValue64(corun->prefill, f + 1, step, 0)) != hipSuccess) return hip_fail(e, "join write");
   if ((e = hipStreamWriteValue64(corun->decode, f + 2, step, 0)) != hipSuccess) return hip_fail(e, "join write");
@@ -387,7 +415,7 @@ int run_mixed(const flex_attn_plan_t* plan, const flex_attn_args* args, int mode
     return hip_fail(e, "join wait");
   if ((e = hipStreamWaitValue64(s, f + 2, step, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
     return hip_fail(e, "join wait");
-  return FLEX_OK;
+  return merge_after_join();
 }
 
 // Scratch of the allocation-free entry point: split-K partials of the

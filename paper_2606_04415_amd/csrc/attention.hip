@@ -1459,6 +1459,8 @@ static hipError_t launch_merge(const AttnParams& p, int dqk, hipStream_t stream)
   return hipGetLastError();
 }
 
+hipError_t launch_decode_merge(const AttnParams& p, int dqk, hipStream_t stream) { return launch_merge(p, dqk, stream); }
+
 hipError_t launch_decode(const AttnParams& p, int dqk, bool has_splits, hipStream_t stream) {
   if (p.n_items == 0) return hipSuccess;
   hipError_t e = launch_decode_kernel(p, dqk, stream);

@@ -9,21 +9,21 @@
 
 namespace flexattn {
 
-// Plan word layout: a 23-word header, 8 words per decode item, the range
-// table, the piece launch order, the merge list, 8 words per prefill item,
+// Plan word layout: a 24-word header, 8 words per decode item, the range
+// table (the decode tail's ranges last; H_N_TAIL_RANGES of them), the piece launch order, the merge list, 8 words per prefill item,
 // the fused order, then the batch's seq_lens [B] and query_start_loc [B+1]
 // as the plan saw them (the debug check compares the device copies with
 // them).
 constexpr int32_t kPlanMagic = 0x46504C58;
-constexpr int32_t kPlanVersion = 6;
-constexpr int kHeaderWords = 23;
+constexpr int32_t kPlanVersion = 7;
+constexpr int kHeaderWords = 24;
 constexpr int kItemWords = 8;
 
 enum HeaderField {
   H_MAGIC = 0, H_VERSION, H_NUM_SEQS, H_N_DEC_ITEMS, H_N_PRE_ITEMS, H_N_DEC_SEQS,
   H_N_PRE_SEQS, H_DEC_WIDTH, H_PRE_GRID_Y, H_OFF_DEC, H_OFF_PRE, H_PPS, H_CUS_DEC,
   H_CUS_PRE, H_BM, H_TOTAL_WORDS, H_N_RANGES, H_OFF_RANGES, H_OFF_ORDER, H_OFF_MERGE,
-  H_OFF_FUSED, H_N_FUSED, H_OFF_LENS
+  H_OFF_FUSED, H_N_FUSED, H_OFF_LENS, H_N_TAIL_RANGES
 };
 
 // Decode item (one piece: the overlap of a balanced page range with one
@@ -70,11 +70,14 @@ constexpr int64_t kFlatResidentPerCu = 3;
 // several waves per head when fewer heads than 4).
 constexpr int32_t kDecodeHeadsPerWG = 8;
 
-// Cost-model rates of one CU when the options leave them 0: measured on
-// MI355X with half the device (128 CUs) running one phase of the
-// Qwen2.5-7B-shaped mixed step alone (decode 4.79 TB/s, prefill 511 TFLOP/s).
-constexpr double kDefaultDecodeGBpsPerCU = 37.0;
+// Cost-model rates when the options leave them 0, measured on MI355X with
+// the Qwen2.5-7B-shaped mixed step: one CU's decode rate beside a running
+// prefill (4.29 TB/s on 96 CUs, 5.21 TB/s on 128), one CU's prefill rate
+// (511 TFLOP/s on 128 CUs), and the device's streaming rate (decode alone on
+// 160 to 256 CUs: 6.3 to 6.55 TB/s).
+constexpr double kDefaultDecodeGBpsPerCU = 43.0;
 constexpr double kDefaultPrefillTFlopsPerCU = 4.0;
+constexpr double kDefaultHbmGBps = 6500.0;
 
 // Rows (query heads) one decode work-group owns in the 576/512 layout.
 constexpr int kLatentRowsPerWG = 64;       // latent heads must be a multiple of this

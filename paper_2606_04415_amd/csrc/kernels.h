@@ -40,6 +40,8 @@ struct AttnParams {
 };
 
 hipError_t launch_decode(const AttnParams& p, int head_dim_qk, bool has_splits, hipStream_t stream);
+// The split-K merge alone (after decode launches that skipped it).
+hipError_t launch_decode_merge(const AttnParams& p, int head_dim_qk, hipStream_t stream);
 hipError_t launch_prefill(const AttnParams& p, int head_dim_qk, int bm, hipStream_t stream);
 // One launch for both phases (grouped-query heads, 32-row prefill tiles):
 // pp / pd are the prefill and decode parameter blocks, order the plan's fused

@@ -145,6 +145,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   int32_t bm = o.bm ? o.bm : (latent || split ? 128 : 0);   // grouped-query default: chosen below
   if (cus_total < 1 || wg_per_cu < 1 || min_tokens < 1 || granule < 1)
     return set_error(FLEX_ERR_INVALID_ARG, "plan options must be positive");
+  if (o.decode_tail < -1 || o.decode_tail > 0) return set_error(FLEX_ERR_INVALID_ARG, "decode_tail must be 0 or -1");
   if (o.cus_decode < -1 || o.cus_decode > cus_total)
     return set_error(FLEX_ERR_INVALID_ARG, "cus_decode must be -1, 0 or in [1, cus_total]");
   if (latent ? (bm != 64 && bm != 128) : split ? bm != 128 : (bm != 0 && bm != 16 && bm != 32 && bm != 128))
@@ -196,22 +197,31 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
                  (n * (L - n) + n * (n + 1) / 2);
   }
 
-  // Co-run CU split: explicit, or the cost model's argmin of the slower phase.
+  // Co-run CU split: explicit, or the cost model's argmin of the step time:
+  // the slower phase, or with a decode tail (grouped-query plans) the
+  // prefill plus what decode has left by then at the device's streaming rate.
   int64_t cus_decode;
   if (o.cus_decode == 0 || dec.empty() || pre.empty()) {
     cus_decode = cus_total;
   } else if (o.cus_decode > 0) {
     cus_decode = o.cus_decode;
   } else {
-    const double hbm = (o.hbm_gbps != 0.0 ? o.hbm_gbps : 8000.0) * 1e9;
+    const double hbm = (o.hbm_gbps != 0.0 ? o.hbm_gbps : kDefaultHbmGBps) * 1e9;
     const double bw_cu = (o.decode_gbps_per_cu != 0.0 ? o.decode_gbps_per_cu : kDefaultDecodeGBpsPerCU) * 1e9;
     const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : kDefaultPrefillTFlopsPerCU) * 1e12;
+    const bool tail_model = !latent && !split && o.decode_tail == 0;
+    const double r_all = std::min(hbm, double(cus_total) * bw_cu);
     int64_t best = -1;
     double best_t = 0.0;
     for (int64_t nd = granule; nd < cus_total; nd += granule) {
-      const double t_dec = double(dec_bytes) / std::min(hbm, double(nd) * bw_cu);
+      const double r_share = std::min(hbm, double(nd) * bw_cu);
+      const double t_dec = double(dec_bytes) / r_share;
       const double t_pre = double(pre_flops) / (double(cus_total - nd) * fl_cu);
-      const double t = std::max(t_dec, t_pre);
+      double t = std::max(t_dec, t_pre);
+      if (tail_model) {
+        const double rest = double(dec_bytes) - r_share * t_pre;
+        t = rest > 0.0 ? t_pre + rest / r_all : t_pre;
+      }
       if (best < 0 || t < best_t) { best = nd; best_t = t; }
     }
     cus_decode = best > 0 ? best : cus_total;
@@ -238,27 +248,59 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
       latent || split ? sh.num_q_heads : flat ? sh.num_kv_heads : sh.num_kv_heads * ((G + 7) / 8);
 
   // Decode partition (balanced split-K): the pages of all decode sequences,
-  // concatenated in batch order, are cut into R near-equal ranges, one
+  // concatenated in batch order, are cut into near-equal ranges, one
   // work-group column each, aiming at wg_per_cu resident work-groups per
   // decode CU. A piece is the overlap of a range with one sequence; pieces
   // are listed by range (batch order, keys ascending) and the list index is
   // the piece's workspace slot, so a sequence's pieces are consecutive.
+  //
+  // Decode tail (grouped-query co-run plans): the decode share streams pages
+  // [0, TA) while the prefill runs; pages [TA, T) form a second group of
+  // ranges, sized for the prefill share, that runs on the prefill stream
+  // once the prefill is done (both groups then stream together until both
+  // end). TA follows the cost model: what the decode share covers during the
+  // prefill, plus its share of the rest at the device's streaming rate.
   const int64_t min_pps = cdiv(min_tokens, P);
   std::vector<int64_t> start(dec.size() + 1, 0);   // first global page of each decode sequence
   for (size_t d = 0; d < dec.size(); ++d) start[d + 1] = start[d] + cdiv(seq_lens[dec[d]], P);
   const int64_t T = start[dec.size()];
-  // (At least ceil(T / kMaxRangePages) ranges: a range's block-table entries
-  // are staged in LDS.)
-  const int64_t R = dec.empty() ? 0
-                                : std::max<int64_t>({int64_t(1), std::min<int64_t>(cus_decode * wg_per_cu / W, T / min_pps),
-                                                     cdiv(T, kMaxRangePages)});
+  int64_t TA = T;
+  if (!latent && !split && o.decode_tail == 0 && cus_prefill < cus_total && T > 1) {
+    const double hbm = (o.hbm_gbps != 0.0 ? o.hbm_gbps : kDefaultHbmGBps) * 1e9;
+    const double bw_cu = (o.decode_gbps_per_cu != 0.0 ? o.decode_gbps_per_cu : kDefaultDecodeGBpsPerCU) * 1e9;
+    const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : kDefaultPrefillTFlopsPerCU) * 1e12;
+    const double r_share = std::min(hbm, double(cus_decode) * bw_cu);   // decode beside the prefill
+    const double r_all = std::min(hbm, double(cus_total) * bw_cu);      // after it
+    const double t_pre = double(pre_flops) / (double(cus_prefill) * fl_cu);
+    const double during = r_share * t_pre;
+    if (during < double(dec_bytes)) {
+      const double t_rest = (double(dec_bytes) - during) / r_all;
+      const double share_rest = r_all * (double(cus_decode) / double(cus_total)) * t_rest;
+      const double frac = (during + share_rest) / double(dec_bytes);
+      TA = std::min(T - 1, std::max(int64_t(1), int64_t(std::floor(frac * double(T)))));
+    }
+  }
+  const int64_t TB = T - TA;
+  // Ranges per group (at least ceil(pages / kMaxRangePages): a range's
+  // block-table entries are staged in LDS).
+  auto n_ranges = [&](int64_t pages, int64_t cus) -> int64_t {
+    if (pages == 0) return 0;
+    return std::max<int64_t>({int64_t(1), std::min<int64_t>(cus * wg_per_cu / W, pages / min_pps),
+                              cdiv(pages, kMaxRangePages)});
+  };
+  const int64_t RA = dec.empty() ? 0 : n_ranges(TA, cus_decode);
+  const int64_t RB = dec.empty() ? 0 : n_ranges(TB, cus_prefill);
+  const int64_t R = RA + RB;
+  auto bound = [&](int64_t r) -> int64_t {   // first page of range r
+    return r <= RA ? r * TA / std::max<int64_t>(RA, 1) : TA + (r - RA) * TB / RB;
+  };
   struct Piece { int32_t s, d, k0, k1; };
   std::vector<Piece> pieces;
   std::vector<int32_t> ranges;
   size_t d0 = 0;   // first sequence that can overlap the current range
   for (int64_t r = 0; r < R; ++r) {
     ranges.push_back(int32_t(pieces.size()));
-    const int64_t lo_r = r * T / R, hi_r = (r + 1) * T / R;
+    const int64_t lo_r = bound(r), hi_r = bound(r + 1);
     while (d0 < dec.size() && start[d0 + 1] <= lo_r) ++d0;
     for (size_t d = d0; d < dec.size() && start[d] < hi_r; ++d) {
       const int64_t lo = std::max(lo_r, start[d]), hi = std::min(hi_r, start[d + 1]);
@@ -269,7 +311,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     }
   }
   ranges.push_back(int32_t(pieces.size()));
-  const int64_t ppr = R ? cdiv(T, R) : 0;
+  const int64_t ppr = std::max(RA ? cdiv(TA, RA) : 0, RB ? cdiv(TB, RB) : 0);   // most pages of a range
   std::vector<int32_t> first_piece(dec.size(), -1), n_pieces(dec.size(), 0);
   for (size_t i = 0; i < pieces.size(); ++i) {
     const int32_t d = pieces[i].d;
@@ -427,6 +469,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   w[H_OFF_FUSED] = off_fused;
   w[H_N_FUSED] = int32_t(fused.size());
   w[H_OFF_LENS] = off_lens;
+  w[H_N_TAIL_RANGES] = int32_t(RB);
   w.insert(w.end(), dec_words.begin(), dec_words.end());
   w.insert(w.end(), ranges.begin(), ranges.end());
   w.insert(w.end(), order.begin(), order.end());
@@ -467,6 +510,9 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   info.decode_bytes = double(dec_bytes);
   info.prefill_flops = double(pre_flops);
   info.n_fused_wgs = int32_t(fused.size());
+  info.n_decode_tail_ranges = int32_t(RB);
+  for (size_t i = size_t(ranges[RA]); i < pieces.size(); ++i)
+    info.decode_tail_bytes += double(pieces[i].k1 - pieces[i].k0) * double(kv_row);
   if (log_level() > 0) log_plan(*plan);
   *out_plan = plan;
   return FLEX_OK;

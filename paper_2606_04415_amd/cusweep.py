@@ -10,7 +10,9 @@ and reports the best split next to serial execution:
     python -m paper_2606_04415_amd.cusweep --workload mixed
 
 Decode is timed alone on a stream masked to c CUs with a plan partitioned for
-c CUs; prefill alone on c CUs; a co-run step on (256 - c_d, c_d). Counts step
+c CUs (all its ranges, a decode tail included); prefill alone on c CUs with
+the plan for a c-CU prefill share; a co-run step on (256 - c_d, c_d), with
+the plan's decode tail where it forms one. Counts step
 in eighths of the device (the co-run mask granularity). Prints one JSON
 object on stdout.
 """
@@ -86,7 +88,8 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
     res = {"workload": workload, "cus_total": total, "decode_bytes": dec_bytes, "prefill_flops": pre_flops,
            "decode": {}, "prefill": {}, "corun_step_us": {}}
     for c in counts:
-        pa, args = plan_for(c if c < total else 0)
+        pa, args = plan_for(c if c < total else 0)                 # decode share of c CUs
+        pa_p, args_p = plan_for(total - c if c < total else 0)     # prefill share of c CUs
         corun_d = F.Corun(total - c, c) if c < total else None
         corun_p = F.Corun(c, total - c) if c < total else None
         sd = corun_d.streams()[1] if corun_d else None
@@ -95,7 +98,7 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
             us = _time_on(sd, lambda i=0: F.flex_attn_decode(pa.plan, args[i % len(args)], stream=sd), reps)
             res["decode"][c] = {"us": round(us, 2), "GBps": round(dec_bytes / (us * 1e-6) / 1e9, 1)}
         if pre_flops:
-            us = _time_on(sp, lambda i=0: F.flex_attn_prefill(pa.plan, args[i % len(args)], stream=sp), reps)
+            us = _time_on(sp, lambda i=0: F.flex_attn_prefill(pa_p.plan, args_p[i % len(args_p)], stream=sp), reps)
             res["prefill"][c] = {"us": round(us, 2), "TFLOPs": round(pre_flops / (us * 1e-6) / 1e12, 1)}
         for cr in (corun_d, corun_p):
             if cr:
@@ -109,9 +112,12 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
         if check_outputs:
             res["corun_bitwise_equals_serial"] = {}
         res["corun_phases_us"] = {}
+        res["decode_tail_frac"] = {}
         for cd in [c for c in counts if c < total]:
             print(f"co-run prefill {total - cd} / decode {cd}: measuring", file=sys.stderr, flush=True)
             pa, args = plan_for(cd)
+            inf = pa.plan.info
+            res["decode_tail_frac"][cd] = round(inf["decode_tail_bytes"] / inf["decode_bytes"], 4) if inf["decode_bytes"] else 0.0
             cr = F.Corun(total - cd, cd)
             if check_outputs:
                 outs = []
@@ -144,9 +150,18 @@ def sweep(workload: str = "mixed", reps: int = 20, pools: int = 4, seed: int = 0
         best = min(res["corun_step_us"], key=res["corun_step_us"].get)
         res["best_split"] = {"cus_prefill": total - best, "cus_decode": best, "us": res["corun_step_us"][best],
                              "speedup_vs_serial": round(res["serial_us"] / res["corun_step_us"][best], 4)}
-        # what the phase curves alone predict: max of the two phase times per split
-        pred = {cd: max(res["decode"][cd]["us"], res["prefill"][total - cd]["us"]) for cd in res["corun_step_us"]
-                if total - cd in res["prefill"]}
+        # what the phase curves alone predict per split: the slower phase, or, when
+        # the split's plan has a decode tail, the prefill plus decode's rest at the
+        # rate decode reaches on all CUs
+        pred = {}
+        for cd in res["corun_step_us"]:
+            if total - cd not in res["prefill"]:
+                continue
+            t_dec, t_pre = res["decode"][cd]["us"], res["prefill"][total - cd]["us"]
+            if res["decode_tail_frac"].get(cd) and t_dec > t_pre and total in res["decode"]:
+                pred[cd] = t_pre + (t_dec - t_pre) * res["decode"][total]["us"] / t_dec
+            else:
+                pred[cd] = max(t_dec, t_pre)
         res["predicted_step_us"] = {cd: round(v, 2) for cd, v in pred.items()}
         if pred:
             res["predicted_best_cus_decode"] = min(pred, key=pred.get)

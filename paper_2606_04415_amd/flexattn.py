@@ -61,7 +61,7 @@ class PlanOpts(ctypes.Structure):
                 ("min_split_tokens", ctypes.c_int32),
                 ("wg_per_cu", ctypes.c_int32), ("split_granule", ctypes.c_int32),
                 ("hbm_gbps", ctypes.c_double), ("decode_gbps_per_cu", ctypes.c_double),
-                ("prefill_tflops_per_cu", ctypes.c_double)]
+                ("prefill_tflops_per_cu", ctypes.c_double), ("decode_tail", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -73,7 +73,8 @@ class PlanInfo(ctypes.Structure):
                 ("cus_decode", ctypes.c_int32), ("cus_prefill", ctypes.c_int32), ("bm", ctypes.c_int32),
                 ("plan_words", ctypes.c_int32), ("device_plan_bytes", ctypes.c_size_t),
                 ("workspace_bytes", ctypes.c_size_t), ("decode_bytes", ctypes.c_double),
-                ("prefill_flops", ctypes.c_double), ("n_fused_wgs", ctypes.c_int32)]
+                ("prefill_flops", ctypes.c_double), ("n_fused_wgs", ctypes.c_int32),
+                ("n_decode_tail_ranges", ctypes.c_int32), ("decode_tail_bytes", ctypes.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -108,7 +109,8 @@ class CtlOpts(ctypes.Structure):
 class CtlSignals(ctypes.Structure):
     _fields_ = [("decode_bytes", ctypes.c_double), ("prefill_flops", ctypes.c_double),
                 ("pending_prefill_tokens", ctypes.c_int32), ("pending_decode_seqs", ctypes.c_int32),
-                ("active_decode_seqs", ctypes.c_int32), ("fused_available", ctypes.c_int32)]
+                ("active_decode_seqs", ctypes.c_int32), ("fused_available", ctypes.c_int32),
+                ("decode_tail", ctypes.c_int32)]
 
 
 class CtlObservation(ctypes.Structure):
@@ -481,9 +483,9 @@ class Controller:
         check(lib().flex_ctl_observe(self.handle, ctypes.byref(ob)), "flex_ctl_observe")
 
     def decide(self, decode_bytes, prefill_flops, pending_prefill_tokens=0, pending_decode_seqs=0,
-               active_decode_seqs=1, fused_available=False) -> dict:
+               active_decode_seqs=1, fused_available=False, decode_tail=False) -> dict:
         sg = CtlSignals(decode_bytes, prefill_flops, pending_prefill_tokens, pending_decode_seqs, active_decode_seqs,
-                        1 if fused_available else 0)
+                        1 if fused_available else 0, 1 if decode_tail else 0)
         d = CtlDecision()
         check(lib().flex_ctl_decide(self.handle, ctypes.byref(sg), ctypes.byref(d)), "flex_ctl_decide")
         return {"mode": d.mode, "cus_decode": d.cus_decode, "cus_prefill": d.cus_prefill, "reason": d.reason,

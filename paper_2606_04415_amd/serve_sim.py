@@ -231,7 +231,8 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         elif policy == "controller":
             d = ctl.decide(info["decode_bytes"], info["prefill_flops"], pending_prefill_tokens=max(0, pend_prefill),
                            pending_decode_seqs=len(waiting), active_decode_seqs=n_dec,
-                           fused_available=getattr(args, "controller_fused", True) and info["n_fused_wgs"] > 0)
+                           fused_available=getattr(args, "controller_fused", True) and info["n_fused_wgs"] > 0,
+                           decode_tail=True)   # grouped-query co-run plans form a decode tail
             reasons[d["reason"]] = reasons.get(d["reason"], 0) + 1
             if d["mode"] == F.FLEX_MODE_CORUN:
                 mode, cd = F.FLEX_MODE_CORUN, d["cus_decode"]
@@ -275,7 +276,10 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
             F.flex_attn_mixed(pa.plan, args_, mode, stream=caller.cuda_stream, corun=corun)
             pre_ms, dec_ms = corun.timing_read()
             corun.set_timing(False)
-            ctl.observe(cd if mode == F.FLEX_MODE_CORUN else 0, info["decode_bytes"], info["prefill_flops"],
+            # (a co-run step's timed decode phase leaves out the plan's decode tail)
+            pinfo = pa.plan.info
+            timed_bytes = pinfo["decode_bytes"] - (pinfo["decode_tail_bytes"] if mode == F.FLEX_MODE_CORUN else 0.0)
+            ctl.observe(cd if mode == F.FLEX_MODE_CORUN else 0, timed_bytes, info["prefill_flops"],
                         dec_ms[-1] if dec_ms else 0.0, pre_ms[-1] if pre_ms else 0.0,
                         step_ms=attn_ms if mode == F.FLEX_MODE_SERIAL else 0.0)
         if ts is not None:

@@ -43,7 +43,8 @@ def test_decisions_match_the_re_derivation(seed):
         B = rng.choice([0.0, rng.uniform(1e8, 3e9)])
         Fl = rng.choice([0.0, rng.uniform(1e10, 3e12)])
         sig = dict(pending_prefill_tokens=rng.randrange(0, 20000), pending_decode_seqs=rng.randrange(0, 400),
-                   active_decode_seqs=rng.randrange(0, 300), fused_available=rng.random() < 0.7)
+                   active_decode_seqs=rng.randrange(0, 300), fused_available=rng.random() < 0.7,
+                   decode_tail=rng.random() < 0.5)
         a = lib.decide(B, Fl, **sig)
         b = ref.decide(B, Fl, **sig)
         same(a, b)
@@ -79,6 +80,23 @@ def test_argmin_matches_closed_form_optimum():
     assert d["mode"] == F.FLEX_MODE_CORUN and d["cus_decode"] == 96 and d["reason"] == F.FLEX_CTL_BEST
     # at the balance point both phases take B / (40 GB/s * 96) = 260.4 us
     assert abs(d["predicted_us"] - B / (40e9 * 96) * 1e6) < 1e-6
+
+
+def test_decode_tail_moves_the_best_split():
+    # Same linear profile; B = 1.2 GB, F such that the prefill takes 240 us on 160
+    # CUs. Slower phase: 96 decode CUs give max(312.5, 240), 128 give max(234.4,
+    # 300) = 300 us, the best. With a decode tail, 96 decode CUs stream 0.9216 GB
+    # during the prefill's 240 us and the rest 0.2784 GB at 5120 GB/s (54.375 us):
+    # 294.375 us, better than 128 (300, decode done first) and 64 (200 + 0.688 GB
+    # at 5120 GB/s = 334.4 us).
+    ctl = F.Controller(granule=32, explore_every=-1, tolerance=1e-12, corun_overhead_us=1e-9)
+    profile_linear(ctl, 40.0, 5120.0, 4.0)
+    B, Fl = 1.2e9, 240e-6 * 4e12 * 160
+    d = ctl.decide(B, Fl, active_decode_seqs=64)
+    assert d["cus_decode"] == 128 and abs(d["predicted_us"] - 300.0) < 1e-6
+    d = ctl.decide(B, Fl, active_decode_seqs=64, decode_tail=True)
+    assert d["mode"] == F.FLEX_MODE_CORUN and d["cus_decode"] == 96
+    assert abs(d["predicted_us"] - 294.375) < 1e-6
 
 
 def test_monotone_in_the_steps_work():

@@ -72,12 +72,47 @@ def check_invariants(sh, opts, qsl, ls, maxp):
     if dec:
         min_pps = -(-(o.min_split_tokens or 256) // P)
         wgpc = o.wg_per_cu or (2 if sh.head_dim_qk == 576 else 1)
-        assert R == max(1, min(b[12] * wgpc // W, T // min_pps), -(-T // 8192))
+        # two groups of balanced ranges: [0, TA) for the decode share, the tail [TA, T)
+        RB = b[23]
+        RA = R - RB
+        start = {}
+        acc = 0
+        for s in dec:
+            start[s] = acc
+            acc += -(-ls[s] // P)
+        TA = start[dec_items[ranges[RA]][0]] + dec_items[ranges[RA]][3] // P if RB else T
+        TB = T - TA
+
+        def n_ranges(npages, cus):
+            return max(1, min(cus * wgpc // W, npages // min_pps), -(-npages // 8192)) if npages else 0
+        assert RA == n_ranges(TA, b[12]) and RB == n_ranges(TB, b[13])
         assert ranges[0] == 0 and ranges[-1] == nd
         assert all(x < y for x, y in zip(ranges, ranges[1:]))          # no empty range
         for rr in range(R):
             pages = sum(-(-(it[4] - it[3]) // P) for it in dec_items[ranges[rr]:ranges[rr + 1]])
-            assert pages in (T // R, -(-T // R))
+            n_g, t_g = (RA, TA) if rr < RA else (RB, TB)
+            assert pages in (t_g // n_g, -(-t_g // n_g))
+        # a tail only on grouped-query co-run shares; its first page balances the two
+        # groups' end times under the cost model (the decode share streams during the
+        # prefill, then shares the device with the tail in proportion to CUs)
+        N = o.cus_total or 256
+        tail_ok = bool(pre) and b[13] < N and sh.head_dim_qk in (64, 128) and o.decode_tail == 0
+        if RB:
+            assert tail_ok and 1 <= TA < T
+        if tail_ok and T > 1:
+            n_d, n_p = b[12], b[13]
+            hbm = (o.hbm_gbps or OP.DEFAULT_HBM_GBPS) * 1e9
+            bw = (o.decode_gbps_per_cu or OP.DEFAULT_DECODE_GBPS_PER_CU) * 1e9
+            fl = (o.prefill_tflops_per_cu or OP.DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
+            D = r.info["decode_bytes"]
+            t_p = r.info["prefill_flops"] / (n_p * fl)
+            r_s = min(hbm, n_d * bw)
+            if r_s * t_p >= D:
+                assert RB == 0
+            else:
+                # t_p + (x - r_s t_p) / (r_a n_d / N) == t_p + (D - x) / (r_a n_p / N)
+                x = (n_d * D + n_p * r_s * t_p) / (n_d + n_p)
+                assert abs(TA - min(T - 1, max(1, int(x / D * T)))) <= 1
     else:
         assert R == 0 and ranges == [0] and nd == 0
     # pieces are listed in slot order; a sequence's pieces are consecutive and tile [0, L)
@@ -237,3 +272,54 @@ def test_fused_order_worked_example():
     assert fused[0::8][:5] == [0, 16, 24, 32, 8]
     # XCD 4 serves tile 1 and 3 column 0 (entries 4, 12) and decode 4, 12, 20 (entries 20, 28, 36)
     assert fused[4::8][:5] == [4, 20, 28, 36, 12]
+
+
+def test_decode_tail_on_corun_shares():
+    """A mixed-step-shaped batch (128 decodes over 1k-8k keys, one 2048-token
+    chunk on 4096 cached keys) planned for each co-run split: a decode tail
+    whose first page balances the two groups where the cost model has the
+    prefill end first (64 and 96 decode CUs), none where the decode share
+    finishes first (check_invariants pins both), with decode_tail = -1, on the
+    whole device, or for the latent layout."""
+    rng = random.Random(5)
+    ls = [rng.randint(1024, 8192) for _ in range(128)] + [6144]
+    qsl = list(range(129)) + [128 + 2048]
+    sh = shape(P=16, d=128, Hq=28, Hkv=4)
+    maxp = max(-(-L // 16) for L in ls)
+    for cd in (64, 96, 128, 160, 192):
+        o = OP.Opts(cus_decode=cd)
+        check_invariants(sh, o, qsl, ls, maxp)
+        b = OP.build_plan(sh, o, qsl, ls, maxp).blob
+        assert b[12] == cd and (b[23] > 0) == (cd <= 96)
+    for o in (OP.Opts(cus_decode=128, decode_tail=-1), OP.Opts(cus_decode=0)):
+        check_invariants(sh, o, qsl, ls, maxp)
+        assert OP.build_plan(sh, o, qsl, ls, maxp).blob[23] == 0
+    lat = shape(mla=True)
+    assert OP.build_plan(lat, OP.Opts(cus_decode=128), qsl, ls, max(-(-L // lat.page_size) for L in ls)).blob[23] == 0
+    assert OP.build_plan(sh, OP.Opts(decode_tail=1), qsl, ls, maxp).status == OP.ERR_INVALID_ARG
+
+
+def test_auto_split_with_decode_tail():
+    """cus_decode = -1 on the mixed-step-shaped batch: the plan's split is the
+    one a time-stepped simulation of the step finds fastest (the decode share
+    streams at its rate until the prefill ends, then the whole device at the
+    streaming rate), and with the default rates it is 96 decode CUs, the
+    split measured fastest for this step (co-run 289 us against 300 us at
+    128/128)."""
+    rng = random.Random(5)
+    ls = [rng.randint(1024, 8192) for _ in range(128)] + [6144]
+    qsl = list(range(129)) + [128 + 2048]
+    sh = shape(P=16, d=128, Hq=28, Hkv=4)
+    maxp = max(-(-L // 16) for L in ls)
+    r = OP.build_plan(sh, OP.Opts(cus_decode=-1), qsl, ls, maxp)
+    D, Fl = r.info["decode_bytes"], r.info["prefill_flops"]
+    bw, fl, hbm = 43e9, 4e12, 6500e9
+
+    def simulate(nd, dt=1e-7):
+        t, left, t_pre = 0.0, D, Fl / ((256 - nd) * fl)
+        while left > 0:
+            left -= (min(hbm, nd * bw) if t < t_pre else hbm) * dt
+            t += dt
+        return max(t, t_pre)
+    times = {nd: simulate(nd) for nd in range(32, 256, 32)}
+    assert r.blob[12] == min(times, key=times.get) == 96
