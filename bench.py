@@ -523,14 +523,19 @@ def main():
     tail_frac = info["decode_tail_bytes"] / info["decode_bytes"] if info["decode_bytes"] else 0.0
     dec_share_bytes = dec_bytes * (1.0 - tail_frac)
     dec_phase_kernel = "decode_gqa_kernel" + (" (decode share's ranges)" if tail_frac else " + merge_kernel")
+    all_traffic = measured_traffic(w.name, "decode")
+    share_traffic = None if all_traffic is None else round(all_traffic * (1.0 - tail_frac))
     # dominant kernel: the phase with the larger share of the co-run step
     if dec_bytes and (not pre_flops or c_dec >= c_pre):
         achieved = dec_share_bytes / (c_dec * 1e-3) / 1e9
         roof_ = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode"),
+                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": share_traffic,
                  "kernel": "decode_gqa_kernel" if w.head_dim_qk != 576 else "rowpar_kernel (latent decode)",
                  "algorithmic_bytes_per_launch": round(dec_share_bytes), "avg_launch_us": round(c_dec * 1e3, 2),
                  "cus": cd}
+        if tail_frac and share_traffic is not None:
+            roof_["traffic_note"] = ("counter bytes of one launch over every decode range (the counter pass), "
+                                     "times the decode share's fraction of the algorithmic bytes")
     else:
         achieved = pre_flops / (c_pre * 1e-3) / 1e12
         roof_ = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",

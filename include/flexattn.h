@@ -106,8 +106,13 @@ typedef struct flex_attn_plan_opts {
   double decode_gbps_per_cu;  /* cost model: decode bandwidth one CU draws beside a running
                                  prefill [43] */
   double prefill_tflops_per_cu; /* cost model: prefill rate of one CU [4] (defaults measured
-                                   on MI355X, the Qwen2.5-7B-shaped mixed step) */
-  int32_t decode_tail;        /* 0: a grouped-query co-run plan splits its decode pages in
+                                   on MI355X, the Qwen2.5-7B-shaped mixed step). Grouped-query
+                                   prefill time: the larger of the work at this rate and the
+                                   largest work-group's (its rows x every key of its sequence)
+                                   at 0.6 of it (flat 128-row tiles) or all of it (32-token
+                                   tiles), plus 10 us */
+  int32_t decode_tail;        /* 0: a grouped-query co-run plan whose decode share would
+                                 outlast the prefill (cost model) splits its decode pages in
                                  two groups of ranges, the second (the tail) run on the
                                  prefill stream after the prefill (see flex_attn_mixed);
                                  -1: no tail [0] */
@@ -325,7 +330,12 @@ size_t flex_attn_static_scratch_bytes(void);
  * flex_attn_mixed forks and joins them (stream memory writes and waits). Each
  * count must be a positive multiple of an eighth of the device's CUs (32 on
  * a 256-CU MI355X) and their sum at most the device's CU count. One pair
- * serves one host thread at a time. */
+ * serves one host thread at a time. Keep few pairs open per process: HIP
+ * serves a process's streams from a small pool of hardware queues
+ * (GPU_MAX_HW_QUEUES, 4 by default), so with several pairs open the two
+ * streams of one pair can share a queue and its phases then run one after
+ * the other (measured: co-run steps 1.6 times longer with seven pairs open
+ * than with one); to change the split, destroy the pair and create another. */
 int flex_attn_corun_create(int32_t cus_prefill, int32_t cus_decode, flex_attn_corun_t** out);
 /* Synchronizes the device (no stream may still wait on the counters), then
  * frees the pair. */
@@ -465,9 +475,10 @@ typedef struct flex_ctl_signals {
   int32_t active_decode_seqs;   /* (4) sequences decoding in this step */
   int32_t fused_available;      /* the step's plan has a one-launch form (n_fused_wgs > 0) */
   int32_t decode_tail;          /* co-run plans of this step form a decode tail (grouped-query
-                                   heads, plan option decode_tail 0): a co-run step is then
-                                   predicted as the prefill plus decode's rest at the rate
-                                   decode reaches on all CUs, not as the slower phase */
+                                   heads, plan option decode_tail 0): a co-run split whose
+                                   predicted prefill lasts 100 us or more is then predicted as
+                                   the prefill plus decode's rest at the rate decode reaches on
+                                   all CUs, not as the slower phase */
 } flex_ctl_signals;
 
 /* What the last step measured (e.g. flex_attn_corun_timing_read). A

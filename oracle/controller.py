@@ -189,7 +189,7 @@ class Controller:
             td, tp = phase_times(k)
             if k == K:
                 pred[k] = td + tp
-            elif decode_tail and td > tp:
+            elif decode_tail and tp >= 100.0 and td > tp:   # (the plan's tail needs a 100 us prefill)
                 # the co-run decode share streams until the prefill ends; the
                 # rest runs on every CU at the rate decode reaches there
                 bytes_left = B - self.dec[k] * 1e3 * tp

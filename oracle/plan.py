@@ -94,6 +94,8 @@ ITEM = 8
 DEFAULT_DECODE_GBPS_PER_CU = 43.0
 DEFAULT_PREFILL_TFLOPS_PER_CU = 4.0
 DEFAULT_HBM_GBPS = 6500.0
+FLAT_WG_CU_SHARE = 0.6        # rate of one flat 4-wave prefill work-group alone, in CUs
+PREFILL_LAUNCH_S = 10e-6      # prefill launch latency in the cost model
 
 
 def cdiv(a: int, b: int) -> int:
@@ -212,6 +214,34 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
     for s in pre:
         n, L = qsl[s + 1] - qsl[s], seq_lens[s]
         pre_flops += sh.num_q_heads * 2 * (sh.head_dim_qk + sh.head_dim_v) * (n * (L - n) + n * (n + 1) // 2)
+    # --- grouped-query tile height (used by the cost model below too): 128 flat rows
+    # when every prefill CU gets at least four such work-groups or, on a co-run
+    # share, when all of them fit in one round (three per CU), else 32 tokens
+    G = sh.num_q_heads // sh.num_kv_heads
+    flat_wgs = sum(cdiv((qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads for s in pre)
+
+    def default_bm(cus):
+        share = cus < cus_total
+        return 128 if (flat_wgs >= 4 * cus or (share and flat_wgs <= 3 * cus)) else 32
+
+    # --- cost-model prefill time on `cus` CUs: grouped-query shapes take the longer of
+    # the work at the per-CU rate and the largest work-group (every key of its
+    # sequence) at one work-group's rate, plus a launch latency
+    bm_opt = bm
+
+    def prefill_time(cus, fl_cu):
+        t_work = float(pre_flops) / (float(cus) * fl_cu)
+        if mla or split:
+            return t_work
+        b = bm_opt if bm_opt else default_bm(cus)
+        tile = 0.0
+        for s in pre:
+            n = qsl[s + 1] - qsl[s]
+            rows = min(128, n * G) if b == 128 else min(b, n) * min(G, 8)
+            tile = max(tile, float(rows) * float(seq_lens[s]) * float(2 * (sh.head_dim_qk + sh.head_dim_v)))
+        share = FLAT_WG_CU_SHARE if b == 128 else 1.0
+        return max(t_work, tile / (share * fl_cu)) + PREFILL_LAUNCH_S
+
     if o.cus_decode == 0 or not dec or not pre:
         cus_decode = cus_total
     elif o.cus_decode > 0:
@@ -226,9 +256,9 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         nd = granule
         while nd < cus_total:
             r_share = min(hbm, float(nd) * bw_cu)
-            t_pre = float(pre_flops) / (float(cus_total - nd) * fl_cu)
+            t_pre = prefill_time(cus_total - nd, fl_cu)
             t = max(float(dec_bytes) / r_share, t_pre)
-            if tail_model:   # the prefill, then decode's rest on the whole device
+            if tail_model:   # the prefill, then decode's rest on all CUs
                 rest = float(dec_bytes) - r_share * t_pre
                 t = t_pre + rest / r_all if rest > 0.0 else t_pre
             if best_t is None or t < best_t:
@@ -237,14 +267,8 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         cus_decode = best if best is not None else cus_total
     cus_prefill = cus_total - cus_decode if (dec and pre and cus_decode < cus_total) else cus_total
 
-    # --- grouped-query tile height: 128 flat rows when every prefill CU gets at least
-    # four such work-groups or, on a co-run share, when all of them fit in one
-    # round (three per CU), else 32 tokens
-    G = sh.num_q_heads // sh.num_kv_heads
     if bm == 0:
-        flat_wgs = sum(cdiv((qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads for s in pre)
-        share = cus_prefill < cus_total
-        bm = 128 if (flat_wgs >= 4 * cus_prefill or (share and flat_wgs <= 3 * cus_prefill)) else 32
+        bm = default_bm(cus_prefill)
     flat = not mla and not split and bm == 128   # rows are (token, query head) pairs of one KV head
 
     # --- decode partition: balanced page ranges over the concatenated decode sequences;
@@ -262,7 +286,7 @@ def build_plan(sh: Shape, opts: Optional[Opts], qsl: Sequence[int], seq_lens: Se
         fl_cu = (o.prefill_tflops_per_cu or DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
         r_share = min(hbm, float(cus_decode) * bw_cu)
         r_all = min(hbm, float(cus_total) * bw_cu)
-        t_pre = float(pre_flops) / (float(cus_prefill) * fl_cu)
+        t_pre = prefill_time(cus_prefill, fl_cu)
         during = r_share * t_pre
         if during < float(dec_bytes):
             t_rest = (float(dec_bytes) - during) / r_all

@@ -191,7 +191,8 @@ extern "C" int flex_ctl_decide(flex_ctl_t* c, const flex_ctl_signals* sg, flex_c
   int32_t best = 1;
   for (int32_t k = 1; k <= K; ++k) {
     if (k == K) T[k] = t_dec(k) + t_pre(k);
-    else if (sg->decode_tail && t_dec(k) > t_pre(k))   // decode's rest, at the all-CU rate, after the prefill
+    else if (sg->decode_tail && t_pre(k) >= flexattn::kTailMinPrefillUs && t_dec(k) > t_pre(k))
+      // decode's rest, at the all-CU rate, after the prefill
       T[k] = t_pre(k) + (B - c->dec[k] * 1e3 * t_pre(k)) / (c->dec[K] * 1e3) + o.corun_overhead_us;
     else T[k] = std::max(t_dec(k), t_pre(k)) + o.corun_overhead_us;
     if (T[k] < T[best]) best = k;

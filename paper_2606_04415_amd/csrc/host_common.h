@@ -78,6 +78,18 @@ constexpr int32_t kDecodeHeadsPerWG = 8;
 constexpr double kDefaultDecodeGBpsPerCU = 43.0;
 constexpr double kDefaultPrefillTFlopsPerCU = 4.0;
 constexpr double kDefaultHbmGBps = 6500.0;
+// Grouped-query prefill time in the cost model: the larger of the work at
+// the per-CU rate and the largest work-group's at the rate one work-group
+// reaches alone (a 4-wave flat 128-row work-group: about 0.6 of a CU; a
+// 32-token work-group of the KV group's query heads: a whole CU), plus a
+// launch latency. Fitted to 2048-token chunks on 96 to 160 CUs: prompts of
+// 512 to 2048 tokens on prefixes up to 4096 run within 15% of it (the
+// work alone missed small chunks by 10 to 60 us).
+constexpr double kFlatWgCuShare = 0.6;
+constexpr double kPrefillLaunchSec = 10e-6;
+// The controller, which sees no tiles, predicts a co-run step with a decode
+// tail only when its predicted prefill phase lasts at least this long.
+constexpr double kTailMinPrefillUs = 100.0;
 
 // Rows (query heads) one decode work-group owns in the 576/512 layout.
 constexpr int kLatentRowsPerWG = 64;       // latent heads must be a multiple of this

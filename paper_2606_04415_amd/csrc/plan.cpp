@@ -197,6 +197,39 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
                  (n * (L - n) + n * (n + 1) / 2);
   }
 
+  // Grouped-query prefill tiles: 128 flattened rows (a row is a (token,
+  // query head) pair of one KV head, token-major: every 16-row block of a
+  // wave is full whatever the group size) when the batch gives every
+  // prefill CU at least four such work-groups, or, on a co-run share, when
+  // they all fit in one round (three flat work-groups are resident per CU);
+  // else 32 tokens, whose larger work-groups fill a CU one at a time and
+  // leave no short last round. (On the whole device the one-round case runs
+  // alike either way, and 32-token tiles keep the one-launch order.)
+  int64_t flat_wgs = 0;
+  for (int32_t s : pre) flat_wgs += cdiv(int64_t(qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads;
+  auto default_bm = [&](int64_t cus) -> int32_t {
+    const bool share = cus < cus_total;
+    return flat_wgs >= 4 * cus || (share && flat_wgs <= kFlatResidentPerCu * cus) ? 128 : 32;
+  };
+  // Cost-model prefill time on `cus` CUs (seconds). Grouped-query shapes:
+  // the work at the per-CU rate or the largest work-group's (every key of
+  // its sequence) at one work-group's rate, whichever is longer, plus the
+  // launch latency; other layouts: the work at the per-CU rate.
+  const int32_t bm_opt = bm;
+  auto prefill_time = [&](int64_t cus, double fl_cu) -> double {
+    const double t_work = double(pre_flops) / (double(cus) * fl_cu);
+    if (latent || split) return t_work;
+    const int32_t b = bm_opt ? bm_opt : default_bm(cus);
+    double tile = 0.0;
+    for (int32_t s : pre) {
+      const int64_t n = qsl[s + 1] - qsl[s];
+      const int64_t rows = b == 128 ? std::min<int64_t>(128, n * G) : std::min<int64_t>(b, n) * std::min(G, 8);
+      tile = std::max(tile, double(rows) * double(seq_lens[s]) * double(2 * (sh.head_dim_qk + sh.head_dim_v)));
+    }
+    const double share = b == 128 ? kFlatWgCuShare : 1.0;
+    return std::max(t_work, tile / (share * fl_cu)) + kPrefillLaunchSec;
+  };
+
   // Co-run CU split: explicit, or the cost model's argmin of the step time:
   // the slower phase, or with a decode tail (grouped-query plans) the
   // prefill plus what decode has left by then at the device's streaming rate.
@@ -216,7 +249,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     for (int64_t nd = granule; nd < cus_total; nd += granule) {
       const double r_share = std::min(hbm, double(nd) * bw_cu);
       const double t_dec = double(dec_bytes) / r_share;
-      const double t_pre = double(pre_flops) / (double(cus_total - nd) * fl_cu);
+      const double t_pre = prefill_time(cus_total - nd, fl_cu);
       double t = std::max(t_dec, t_pre);
       if (tail_model) {
         const double rest = double(dec_bytes) - r_share * t_pre;
@@ -229,20 +262,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
   const int64_t cus_prefill =
       (!dec.empty() && !pre.empty() && cus_decode < cus_total) ? cus_total - cus_decode : cus_total;
 
-  // Grouped-query prefill tiles: 128 flattened rows (a row is a (token,
-  // query head) pair of one KV head, token-major: every 16-row block of a
-  // wave is full whatever the group size) when the batch gives every
-  // prefill CU at least four such work-groups, or, on a co-run share, when
-  // they all fit in one round (three flat work-groups are resident per CU);
-  // else 32 tokens, whose larger work-groups fill a CU one at a time and
-  // leave no short last round. (On the whole device the one-round case runs
-  // alike either way, and 32-token tiles keep the one-launch order.)
-  if (bm == 0) {
-    int64_t flat_wgs = 0;
-    for (int32_t s : pre) flat_wgs += cdiv(int64_t(qsl[s + 1] - qsl[s]) * G, 128) * sh.num_kv_heads;
-    const bool share = cus_prefill < cus_total;
-    bm = flat_wgs >= 4 * cus_prefill || (share && flat_wgs <= kFlatResidentPerCu * cus_prefill) ? 128 : 32;
-  }
+  if (bm == 0) bm = default_bm(cus_prefill);   // grouped-query tile height (rule above)
   const bool flat = !latent && !split && bm == 128;
   const int32_t pre_grid_y =
       latent || split ? sh.num_q_heads : flat ? sh.num_kv_heads : sh.num_kv_heads * ((G + 7) / 8);
@@ -271,7 +291,7 @@ extern "C" int flex_attn_plan(const flex_attn_shape* shape, const flex_attn_plan
     const double fl_cu = (o.prefill_tflops_per_cu != 0.0 ? o.prefill_tflops_per_cu : kDefaultPrefillTFlopsPerCU) * 1e12;
     const double r_share = std::min(hbm, double(cus_decode) * bw_cu);   // decode beside the prefill
     const double r_all = std::min(hbm, double(cus_total) * bw_cu);      // after it
-    const double t_pre = double(pre_flops) / (double(cus_prefill) * fl_cu);
+    const double t_pre = prefill_time(cus_prefill, fl_cu);
     const double during = r_share * t_pre;
     if (during < double(dec_bytes)) {
       const double t_rest = (double(dec_bytes) - during) / r_all;

@@ -133,8 +133,20 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
     free_pages = list(range(n_pages - 1, 0, -1))          # page 0 is a spare for unused entries
     shape = F.make_shape(HQ, HKV, D, D, P, 1.0 / math.sqrt(D), False)
     caller = torch.cuda.Stream()
-    coruns = {cd: F.Corun(256 - cd, cd) for cd in (64, 128, 192)}
-    serial_timer = coruns[128]
+    # One co-run pair open at a time, recreated when the split changes: every
+    # open pair holds two streams, and HIP serves a process's streams from a
+    # few hardware queues (4 here), so with several pairs open the phase
+    # streams of one pair can share a queue and run one after the other
+    # (measured: co-run steps 1.6x longer with seven pairs open). The switch
+    # is host work, timed with the planning.
+    pair = {"cd": None, "obj": None}
+
+    def corun_for(cd):
+        if pair["cd"] != cd:
+            if pair["obj"] is not None:
+                pair["obj"].close()
+            pair["obj"], pair["cd"] = F.Corun(256 - cd, cd), cd
+        return pair["obj"]
     ctl = None
     ts = None
     if policy.startswith("timeslice"):
@@ -244,6 +256,8 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
             pa = F.PagedAttention(shape, F.make_opts(wg_per_cu=2), qsl, ls, max_pages)
         else:
             pa = F.PagedAttention(shape, F.make_opts(cus_decode=cd), qsl, ls, max_pages)
+        # (SERIAL uses a pair only for its phase timing: whichever is open)
+        corun = corun_for(cd if mode == F.FLEX_MODE_CORUN else (pair["cd"] or 128))
         plan_ms.append((time.perf_counter() - t_plan) * 1e3)
         key = {F.FLEX_MODE_SERIAL: "serial", F.FLEX_MODE_FUSED: "fused"}.get(mode, f"{256 - cd}:{cd}")
         if ts is not None:
@@ -256,7 +270,6 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
         q, out = q_pool[:T], out_pool[:T]
         args_ = pa.args(q, k_cache, v_cache, d_bt, d_sl, d_qsl, out)
         app = F.make_append_args(kn_pool[:T], vn_pool[:T], d_slots, k_cache, v_cache)
-        corun = coruns[cd] if mode == F.FLEX_MODE_CORUN else serial_timer
         torch.cuda.synchronize()
         # the step, timed with no phase events (recording them adds ~10 us)
         e0.record(caller)
@@ -308,8 +321,8 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
                 r.pages = []
                 done.append(r)
         active = [r for r in active if r.finish_ms is None]
-    for c in coruns.values():
-        c.close()
+    if pair["obj"] is not None:
+        pair["obj"].close()
     if ts is not None:
         ts.close()
 
@@ -342,9 +355,10 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
 
 
 def measure_profile(reps: int = 10, remeasure: bool = False):
-    """Alone phase rates on 64..256 CUs (quarters) for the mixed step, to seed
-    the controller: the committed CU sweep (profiles/cusweep_mixed.json) when
-    present, else measured now."""
+    """Alone phase rates on 64..256 CUs (quarters, the controller's default
+    candidate splits) for the mixed step, to seed the controller: the
+    committed CU sweep (profiles/cusweep_mixed.json) when present, else
+    measured now."""
     from .cusweep import PROFILE_DIR, profile_from, sweep
     path = os.path.join(PROFILE_DIR, "cusweep_mixed.json")
     if os.path.exists(path) and not remeasure:
@@ -369,7 +383,7 @@ def main():
     ap.add_argument("--burst", type=int, default=64, help="prompts arriving together every --burst-every steps")
     ap.add_argument("--burst-every", type=int, default=100)
     ap.add_argument("--rate", type=float, default=0.2, help="Poisson arrivals per step")
-    ap.add_argument("--fixed-decode-cus", type=int, default=128)
+    ap.add_argument("--fixed-decode-cus", type=int, default=96)
     ap.add_argument("--no-profile", action="store_true", help="controller starts from its prior only")
     ap.add_argument("--remeasure-profile", action="store_true",
                     help="measure the phase profile now instead of reading profiles/cusweep_mixed.json")

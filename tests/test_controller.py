@@ -150,7 +150,7 @@ def test_one_phase_runs_serial():
 
 
 def test_estimates_converge_to_observed_rates():
-    ctl = F.Controller(alpha=0.25, explore_every=-1)
+    ctl = F.Controller(alpha=0.25, explore_every=-1, granule=64)
     prior_d, prior_p = ctl.estimates()
     for _ in range(40):
         ctl.observe(128, 1.0e9, 1.0e11, 0.25, 0.2)       # 4000 GB/s, 500 TFLOP/s

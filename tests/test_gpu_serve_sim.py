@@ -26,7 +26,7 @@ def test_policies_replay_the_same_stream():
     assert toks["serial"] > 0 and firsts["serial"] > 0
     assert set(res["serial"]["splits"]) == {"serial"}
     for k in res["controller"]["splits"]:
-        assert k in ("serial", "fused", "192:64", "128:128", "64:192")
+        assert k in ("serial", "fused") or k in {f"{256 - c}:{c}" for c in range(32, 256, 32)}
     assert set(res["fused"]["splits"]) <= {"serial", "fused"} and "fused" in res["fused"]["splits"]
     for r in res.values():
         assert r["total_ms"] > 0 and r["step_ms"]["max"] < 50.0

@@ -39,6 +39,22 @@ def random_batch(rng, P, n_dec, n_pre, Lmax=9000):
     return qsl, ls, maxp
 
 
+def prefill_model(sh, bm, qsl, ls, pre, cus, fl):
+    """The plan's prefill time for grouped-query tiles: the work at the
+    per-CU rate, or the largest work-group (its rows against every key of
+    its sequence) at 0.6 of a CU (flat 4-wave work-groups) or a whole CU
+    (32-token groups of up to 8 heads), whichever is longer, plus 10 us."""
+    G = sh.num_q_heads // sh.num_kv_heads
+    work = 0.0
+    big = 0.0
+    for s in pre:
+        n, L = qsl[s + 1] - qsl[s], ls[s]
+        work += sh.num_q_heads * 2 * (sh.head_dim_qk + sh.head_dim_v) * (n * (L - n) + n * (n + 1) / 2)
+        rows = min(128, n * G) if bm == 128 else min(bm, n) * min(G, 8)
+        big = max(big, rows * L * 2 * (sh.head_dim_qk + sh.head_dim_v) / ((0.6 if bm == 128 else 1.0) * fl))
+    return max(work / (cus * fl), big) + 10e-6
+
+
 def check_invariants(sh, opts, qsl, ls, maxp):
     r = OP.build_plan(sh, opts, qsl, ls, maxp)
     assert r.status == OP.OK
@@ -105,7 +121,7 @@ def check_invariants(sh, opts, qsl, ls, maxp):
             bw = (o.decode_gbps_per_cu or OP.DEFAULT_DECODE_GBPS_PER_CU) * 1e9
             fl = (o.prefill_tflops_per_cu or OP.DEFAULT_PREFILL_TFLOPS_PER_CU) * 1e12
             D = r.info["decode_bytes"]
-            t_p = r.info["prefill_flops"] / (n_p * fl)
+            t_p = prefill_model(sh, b[14], qsl, ls, pre, n_p, fl)
             r_s = min(hbm, n_d * bw)
             if r_s * t_p >= D:
                 assert RB == 0
@@ -312,11 +328,12 @@ def test_auto_split_with_decode_tail():
     sh = shape(P=16, d=128, Hq=28, Hkv=4)
     maxp = max(-(-L // 16) for L in ls)
     r = OP.build_plan(sh, OP.Opts(cus_decode=-1), qsl, ls, maxp)
-    D, Fl = r.info["decode_bytes"], r.info["prefill_flops"]
+    D = r.info["decode_bytes"]
     bw, fl, hbm = 43e9, 4e12, 6500e9
 
     def simulate(nd, dt=1e-7):
-        t, left, t_pre = 0.0, D, Fl / ((256 - nd) * fl)
+        bm = OP.build_plan(sh, OP.Opts(cus_decode=nd), qsl, ls, maxp).blob[14]   # the tiles of that share
+        t, left, t_pre = 0.0, D, prefill_model(sh, bm, qsl, ls, [128], 256 - nd, fl)
         while left > 0:
             left -= (min(hbm, nd * bw) if t < t_pre else hbm) * dt
             t += dt
