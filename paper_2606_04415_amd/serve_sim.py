@@ -147,6 +147,7 @@ def simulate(mix: str, policy: str, args, profile=None) -> Dict:
                 pair["obj"].close()
             pair["obj"], pair["cd"] = F.Corun(256 - cd, cd), cd
         return pair["obj"]
+    corun_for(args.fixed_decode_cus if policy == "fixed" else 128)   # set-up, untimed
     ctl = None
     ts = None
     if policy.startswith("timeslice"):
