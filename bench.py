@@ -32,7 +32,9 @@ decode step, 5 us per co-run step), so the p10/p50/p90 of each leg come from
 a separate pass with an event after every step, whose mean is reported as
 `per_step_events_mean`. A further pass with HIP events around each phase's
 kernels (on the stream they run on) gives the phase durations for the
-roofline.
+roofline. Last, the fixed half-and-half split (128 / 128 CUs, its plan's
+own decode tail) runs on a co-run pair of its own, timed the same way
+(`corun_half_split`), beside the chosen split and the serial step.
 """
 from __future__ import annotations
 
@@ -336,6 +338,7 @@ def main():
     ap.add_argument("--bm", type=int, default=0, help="prefill rows per tile (0: library default)")
     ap.add_argument("--blocks", type=int, default=5, help="interleaved timing blocks per leg")
     ap.add_argument("--no-serial", action="store_true", help="skip the serial comparison leg")
+    ap.add_argument("--no-half", action="store_true", help="skip the fixed half-and-half co-run split")
     ap.add_argument("--no-fused", action="store_true", help="skip the one-launch (fused) comparison leg")
     ap.add_argument("--no-configs", action="store_true", help="skip the single-phase and latent workloads")
     ap.add_argument("--fused-wg-per-cu", type=int, default=2,
@@ -515,9 +518,29 @@ def main():
         s_pre, s_dec, _, _ = phases(F.FLEX_MODE_SERIAL, pa_s, arg_s)
     corun.close()
 
+    # The fixed half-and-half split beside the chosen one, on a pair of its own
+    # opened once the chosen split's pair is closed (pairs open together share
+    # the hardware queues); timed after the other legs, on a settled device.
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    half = None
+    if not args.no_half and cp + cd == n_cus and cd != n_cus // 2:
+        pa_h = F.PagedAttention(shape, F.make_opts(bm=args.bm, cus_decode=n_cus // 2), b.query_start_loc.tolist(),
+                                b.seq_lens.tolist(), b.block_table.shape[1])
+        arg_h = [pa_h.args(q, k, v, bt, sl, qsl, out) for k, v in kv]
+        corun_h = F.Corun(n_cus // 2, n_cus // 2)
+        step["half"] = lambda i: F.flex_attn_mixed(pa_h.plan, arg_h[i % len(arg_h)], F.FLEX_MODE_CORUN, stream=cs,
+                                                   corun=corun_h)
+        for i in range(max(100, args.warmup)):   # the new pair's first steps run slower
+            step["half"](i)
+        _, t_half = block("half", args.steps, 20000)
+        per_half, _ = block("half", args.steps, 30000, per_step=True)
+        corun_h.close()
+        half = {"cus_prefill": n_cus // 2, "cus_decode": n_cus // 2,
+                "decode_tail_ranges": pa_h.plan.info["n_decode_tail_ranges"],
+                "step_us": timed_dist(t_half / args.steps, per_half)}
+
     dec_bytes = work["decode"]["bytes"]
     pre_flops = work["prefill"]["flops"]
-    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
     # the co-run decode phase (events on the decode stream) streams the decode
     # share's ranges; a decode tail runs on the prefill stream after the prefill
     tail_frac = info["decode_tail_bytes"] / info["decode_bytes"] if info["decode_bytes"] else 0.0
@@ -584,6 +607,10 @@ def main():
             result["decode_GBps_all_cus"] = round(dec_bytes / (s_dec * 1e-3) / 1e9, 1)
         if pre_flops:
             result["prefill_TFLOPs_all_cus"] = round(pre_flops / (s_pre * 1e-3) / 1e12, 2)
+        if half is not None:
+            half["speedup_vs_serial"] = round(s_ms * 1e3 / half["step_us"]["mean"], 4)
+    if half is not None:
+        result["corun_half_split"] = half
     if "fused" in legs:
         f_ms = total["fused"] / args.steps / 1e3
         result["fused_us"] = round(f_ms * 1e3, 2)
@@ -595,6 +622,8 @@ def main():
     result["max_phase_us"] = round(max(c_pre, c_dec) * 1e3, 2)
     result["kv_append"] = time_kv_append(b, kv, shape, args.steps, caller)
     del kv, arg_c, arg_s, arg_f, q
+    if half is not None:
+        del arg_h, pa_h
     torch.cuda.empty_cache()
     if not args.no_configs:
         result["configs"] = {}
