@@ -588,7 +588,12 @@ struct RowParCfg {
   static constexpr int TI_RAW = (SLOTS + 63) / 64;         // 1 KB loads per tile
   static constexpr int TI = (TI_RAW + NW - 1) / NW * NW;
   static constexpr int NI = TI / NW;                       // per wave per tile
-  static constexpr int STAGE = TI * 1024;
+  // With two stages every tile wait drains all loads, so the loads past
+  // TI_RAW that only round TI up to the wave count are skipped and the stage
+  // holds TI_RAW KB (this is what lets two 4-wave latent work-groups share a
+  // CU's LDS). With more stages each wave counts NI loads per tile.
+  static constexpr int TI_USED = NS == 2 ? TI_RAW : TI;
+  static constexpr int STAGE = TI_USED * 1024;
   static constexpr int V_OFF = K_SLOTS * 16;
   static constexpr int NT = NW * 64;
   static constexpr int NACC = DV / 16;
@@ -659,7 +664,12 @@ struct TileLoader {
   const uint8_t* kbase;
   const uint8_t* vbase;
   uint32_t ksp, kss, vsp, vss;
-  uint32_t ld_lane_off[C::NI];
+  // Per-lane byte offsets of the loads, fixed for the launch. The two-stage
+  // latent form (four waves, ten loads each per tile, two work-groups per
+  // CU) forms them again at each tile instead of holding them: beside its
+  // accumulators and Q they would spill.
+  static constexpr bool kHoldOff = !(VALIAS && NS == 2);
+  uint32_t ld_lane_off[kHoldOff ? C::NI : 1];
 
   __device__ __forceinline__ TileLoader(const AttnParams& p, int head_kv, uint8_t* lds_, const int* s_pt_, int w_,
                                         int lane_, int key_end_)
@@ -671,23 +681,40 @@ struct TileLoader {
     kss = uint32_t(p.kc.ss) * 2u;
     vsp = uint32_t(VALIAS ? p.kc.sp : p.vc.sp) * 2u;
     vss = uint32_t(VALIAS ? p.kc.ss : p.vc.ss) * 2u;
+    if constexpr (kHoldOff) {
 #pragma unroll
-    for (int j = 0; j < C::NI; ++j) {
-      int row;
-      uint32_t xoff;
-      slot_of(j, row, xoff);
-      ld_lane_off[j] = (P <= BN ? uint32_t(row % P) : uint32_t(row)) * (is_v(j) ? vss : kss) + xoff;
+      for (int j = 0; j < C::NI; ++j) ld_lane_off[j] = form_lane_off(j, lane);
+    }
+  }
+  __device__ __forceinline__ uint32_t form_lane_off(int j, int ln) const {
+    int row;
+    uint32_t xoff;
+    slot_of(j, ln, row, xoff);
+    return (P <= BN ? uint32_t(row % P) : uint32_t(row)) * (is_v(j) ? vss : kss) + xoff;
+  }
+  __device__ __forceinline__ uint32_t lane_off(int j) const {
+    if constexpr (kHoldOff) {
+      return ld_lane_off[j];
+    } else {
+      int ln = lane;
+      asm volatile("" : "+v"(ln));   // keeps the arithmetic at the load, out of the loop
+      return form_lane_off(j, ln);
     }
   }
   // Whether load j of this wave fills V rows (wave-uniform).
   __device__ __forceinline__ bool is_v(int j) const { return !VALIAS && (w * C::NI + j) * 64 >= C::K_SLOTS; }
   // Row and byte offset within the row of the chunk lane slot s loads.
-  __device__ __forceinline__ void slot_of(int j, int& row, uint32_t& xoff) const {
+  __device__ __forceinline__ void slot_of(int j, int ln, int& row, uint32_t& xoff) const {
     const int blk = w * C::NI + j;
-    const int s = blk * 64 + lane;
+    const int s = blk * 64 + ln;
     int x = 0;
     row = 0;
-    if (VALIAS || blk * 64 < C::K_SLOTS) {   // wave-uniform
+    if constexpr (!kHoldOff) {   // branch-free: formed again at every tile
+      const int r = s / C::ROWB, pc = s - r * C::ROWB;
+      const bool in = s < C::K_SLOTS;
+      row = in ? r : 0;
+      x = in && pc < C::CPR ? pc : 0;
+    } else if (VALIAS || blk * 64 < C::K_SLOTS) {   // wave-uniform
       if (s < C::K_SLOTS) {
         row = s / C::ROWB;
         const int pc = s % C::ROWB;
@@ -718,6 +745,9 @@ struct TileLoader {
     const uint32_t in_page = P > BN ? uint32_t(kb % P) : 0u;   // first slot of the tile in its page
 #pragma unroll
     for (int j = 0; j < C::NI; ++j) {
+      if constexpr (C::TI_USED < C::TI) {
+        if (w * C::NI + j >= C::TI_USED) break;   // wave-uniform
+      }
       const bool isv = is_v(j);
       const uint8_t* base = isv ? vbase : kbase;
       const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
@@ -726,7 +756,7 @@ struct TileLoader {
 #pragma unroll
       for (int t = 1; t < PPT; ++t) page = tp == t ? pg[t] : page;
       const i32x4 r = uniform_rsrc(base + (uint64_t(uint32_t(page)) * sp + in_page * ss), uint32_t(min(P, BN)) * ss);
-      dma16_buf(r, ld_lane_off[j], sbase + (w * C::NI + j) * 1024);
+      dma16_buf(r, lane_off(j), sbase + (w * C::NI + j) * 1024);
     }
   }
   // Issue this wave's loads of the key tile starting at kb into stage st.
@@ -743,6 +773,9 @@ struct TileLoader {
     }
 #pragma unroll
     for (int j = 0; j < C::NI; ++j) {
+      if constexpr (C::TI_USED < C::TI) {
+        if (w * C::NI + j >= C::TI_USED) break;   // wave-uniform
+      }
       const bool isv = is_v(j);
       const uint8_t* base = isv ? vbase : kbase;
       const uint32_t sp = isv ? vsp : ksp, ss = isv ? vss : kss;
@@ -752,14 +785,14 @@ struct TileLoader {
         int row = 0;
         if constexpr (VALIAS && P <= BN) {
           uint32_t xoff;
-          slot_of(j, row, xoff);
+          slot_of(j, lane, row, xoff);
         }
         pidx = kb / P - pt_base + tile_page(j, row);
-        off = P <= BN ? ld_lane_off[j] : ld_lane_off[j] + uint32_t(kb % P) * ss;
+        off = P <= BN ? lane_off(j) : lane_off(j) + uint32_t(kb % P) * ss;
       } else {
         int row;
         uint32_t xoff;
-        slot_of(j, row, xoff);
+        slot_of(j, lane, row, xoff);
         const uint32_t key = uint32_t(min(kb + row, key_end - 1));
         pidx = int(key / P) - pt_base;
         off = (key % P) * ss + xoff;
@@ -1185,7 +1218,7 @@ __device__ __forceinline__ void rowpar_body(const AttnParams& p, int item, int c
 }
 
 template <int DQK, int DV, int NW, int RB, int BN, bool VALIAS, int MODE, int P, int NS, int TB>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)))
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(VALIAS && NS == 2 ? 2 : NW / 4)))
 void rowpar_kernel(AttnParams p) {
   // Work-group -> (item, column). Decode pieces launch longest first; prefill
   // tiles are listed that way. Grouped-query prefill with a column count
@@ -1529,20 +1562,23 @@ static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 gr
                       : launch_prefill_grouped<64, P>(q, bm, grid, stream);
   }
   // One work-group per (tile, query head), a wave per 16 rows; XCD-aware
-  // 1-D grid when the head count is a multiple of 8.
+  // 1-D grid when the head count is a multiple of 8. Latent 64-row tiles run
+  // four waves over two LDS stages, so that two work-groups share a CU
+  // (with three stages one work-group of four waves held the CU alone: 1.8x
+  // slower).
   if (p.grid_y % 8 == 0) {
     AttnParams q = p;
     q.xcd_remap = 1;
     const dim3 g1(p.n_items * p.grid_y, 1);
     if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(q, g1, stream);
-    if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(q, g1, stream);
+    if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 2>(q, g1, stream);
     if constexpr (P == 64) {
       if (dqk == 192 && bm == 128) return launch_rowpar<192, 128, 8, 1, 32, false, kPrefillPerHead, 64, 3>(q, g1, stream);
     }
     return hipErrorInvalidValue;
   }
   if (dqk == 576 && bm == 128) return launch_rowpar<576, 512, 8, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
-  if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 3>(p, grid, stream);
+  if (dqk == 576 && bm == 64) return launch_rowpar<576, 512, 4, 1, 32, true, kPrefillPerHead, P, 2>(p, grid, stream);
   // Heads split out (keys 192, values 128): one work-group per (128-token
   // tile, query head); 32-key tiles (three stages in 74 KB of LDS, 122
   // VGPRs), so two work-groups share a CU.
