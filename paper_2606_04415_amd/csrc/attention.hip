@@ -1465,12 +1465,13 @@ static hipError_t launch_decode_kernel(const AttnParams& p, int dqk, hipStream_t
   switch (dqk) {
     case 128: return p16 ? launch_decode_gqa<128, 16>(p, stream) : launch_decode_gqa<128, 64>(p, stream);
     case 64: return p16 ? launch_decode_gqa<64, 16>(p, stream) : launch_decode_gqa<64, 64>(p, stream);
-    case 576:   // one work-group per (piece, group of 128 or 64 heads), a wave per 16 heads
+    case 576:   // one work-group per (piece, group of 128 or 64 heads), a wave per 16 heads;
+                // 64-head groups take two LDS stages so that two work-groups share a CU
       if (p.rows_per_wg == 128)
         return p16 ? launch_rowpar<576, 512, 8, 1, 32, true, kDecodeLatent, 16, 3>(p, pieces, stream)
                    : launch_rowpar<576, 512, 8, 1, 32, true, kDecodeLatent, 64, 3>(p, pieces, stream);
-      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16, 3>(p, pieces, stream)
-                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64, 3>(p, pieces, stream);
+      return p16 ? launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 16, 2>(p, pieces, stream)
+                 : launch_rowpar<576, 512, 4, 1, 32, true, kDecodeLatent, 64, 2>(p, pieces, stream);
     default: return hipErrorInvalidValue;
   }
 }
