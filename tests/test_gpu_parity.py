@@ -345,6 +345,17 @@ def test_accepted_gqa_shapes(geo, bm):
     full_check(b, F.make_opts(bm=bm, min_split_tokens=64), f"gqa-{geo}-bm{bm}")
 
 
+@pytest.mark.parametrize("page", [64, 16])
+def test_latent_prefill_64_row_tiles(page):
+    """Latent prefill on 64-row tiles (four waves over two LDS stages, two
+    work-groups per CU) on ragged chunks at both page sizes, with split
+    decodes in the same batch."""
+    ns, ls = [1, 130, 70, 1, 200, 64], [900, 130, 300, 65, 2000, 64]
+    b = custom_batch(MLA, ns, ls, seed=61, page_size=page)
+    log(f"latent prefill bm 64, page {page}")
+    full_check(b, F.make_opts(bm=64, min_split_tokens=128), f"latent-bm64-p{page}")
+
+
 @pytest.mark.parametrize("hq", [64, 128])
 def test_latent_page16(hq):
     ns, ls = [1, 1, 1, 100, 1, 40], [1, 33, 700, 130, 2000, 40]
