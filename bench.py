@@ -153,9 +153,10 @@ KERNEL_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_
 
 
 def kernel_source_hash():
-    import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel source's code (comments and whitespace removed),
+    the key of the committed counter summary."""
+    from paper_2606_04415_amd.profsum import source_hash
+    return source_hash(KERNEL_SOURCE)
 
 
 def measured_traffic(workload, kernel):

@@ -1590,8 +1590,9 @@ static hipError_t launch_prefill_p(const AttnParams& p, int dqk, int bm, dim3 gr
     return dqk == 128 ? launch_prefill_grouped<128, P>(q, bm, grid, stream)
                       : launch_prefill_grouped<64, P>(q, bm, grid, stream);
   }
-  // One work-group per (tile, query head), a wave per 16 rows; XCD-aware
-  // 1-D grid when the head count is a multiple of 8. Latent 64-row tiles run
+  // One work-group per (tile, query head), a wave per 16 rows (32 with the
+  // heads split out); XCD-aware 1-D grid when the head count is a multiple
+  // of 8. Latent 64-row tiles run
   // four waves over two LDS stages, so that two work-groups share a CU
   // (with three stages one work-group of four waves held the CU alone: 1.8x
   // slower).

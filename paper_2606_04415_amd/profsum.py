@@ -18,6 +18,7 @@ import csv
 import hashlib
 import json
 import os
+import re
 import sys
 from collections import defaultdict
 
@@ -25,9 +26,17 @@ KERNEL_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc",
 COPY_BYTES = 1 << 30
 
 
-def source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def code_text(src: str) -> str:
+    """The kernel source with its comments and whitespace removed: edits of
+    comments leave what is measured unchanged."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
+def source_hash(path: str = KERNEL_SOURCE) -> str:
+    with open(path, encoding="utf-8") as f:
+        return hashlib.sha256(code_text(f.read()).encode()).hexdigest()[:16]
 
 
 def stats_table(path, title, command):

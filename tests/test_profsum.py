@@ -62,3 +62,16 @@ def test_traffic_scaling_and_merge(tmp_path):
     first.write_text(json.dumps(stale))
     t3 = profsum.traffic(args("prefill", "pf.csv", "pw.csv", into=str(first)))
     assert set(t3["entries"]) == {"prefill:prefill"}
+
+
+def test_source_hash_ignores_comments_only(tmp_path):
+    """The counter summary stays keyed to a kernel source whose comments
+    change, and not to one whose code changes."""
+    a = tmp_path / "a.hip"
+    a.write_text("// kernel\n__global__ void k(int* p) { p[0] = 1; /* one */ }\n")
+    b = tmp_path / "b.hip"
+    b.write_text("// the kernel, reworded\n__global__ void k(int* p) {\n  p[0] = 1;   // still one\n}\n")
+    c = tmp_path / "c.hip"
+    c.write_text("__global__ void k(int* p) { p[0] = 2; }\n")
+    assert profsum.source_hash(str(a)) == profsum.source_hash(str(b))
+    assert profsum.source_hash(str(a)) != profsum.source_hash(str(c))
